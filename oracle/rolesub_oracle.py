@@ -1,0 +1,354 @@
+"""Float64 CPU oracle of RoleSub's inference hot path.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg; never by the product path.
+
+Written from the paper (Role-Conditioned Sub-Token Routing, Sec. 3):
+plain, slow, obviously checkable numpy float64. Each function names the
+passage it follows. Inputs arrive as arrays whose values are exactly
+representable in the workload's storage type; everything here is computed in
+float64 except where a discrete decision is taken (group selection), which is
+taken on the scores exactly as given.
+
+Readings of points the paper leaves open (listed with reasons in the design
+notes of the repository):
+  * one orthonormal R_h per head, groups are equal slices of each head's
+    rotated value, one mask per token shared by all heads;
+  * z = R^T v (row form z_j = sum_k R[k, j] v_k) and back-rotation o = R u;
+  * router "MLP2": [h | e | mean_lang(h)] -> Hr -> exact-erf GELU -> G, with
+    e = a E the role-mixed vector and a = softmax(W_r h + b_r);
+  * router "additive": the paper's routing-score equation with linear heads;
+  * top-K ties go to the lower group index, -0 equals +0, NaN ranks lowest;
+  * threshold budgets keep count(gamma > tau) groups clamped to [kmin, kmax];
+  * attention: scale 1/sqrt(dh), no mask, keys unchanged, routed values.
+
+Parity: every function here is pinned by CPU tests against closed forms, the
+paper's printed KV fractions, brute-force enumeration and textbook special
+cases; none is "parity unpinned".
+"""
+from __future__ import annotations
+
+import numpy as np
+from scipy.special import erf as _erf
+
+VIS, LANG, PROP, ACT = 0, 1, 2, 3
+TOPK, THRESHOLD = 0, 1
+
+__all__ = [
+    "VIS", "LANG", "PROP", "ACT", "TOPK", "THRESHOLD",
+    "rotate", "back_rotate", "latent_role", "language_pool", "gelu",
+    "router_mlp2", "router_additive", "group_budget", "select_groups",
+    "mask_to_idx", "popcount", "pack", "unpack", "expand_mask", "routed_values",
+    "attend_packed", "attend_plain", "softmax", "pipeline",
+    "kv_fraction", "packed_groups",
+]
+
+
+def _f64(x):
+    return np.asarray(x, dtype=np.float64)
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.2, orthogonal value-space decomposition
+# ----------------------------------------------------------------------------
+
+def rotate(v, R):
+    """z = R^T v for every token and head (Sec. 3.2, value into routing space).
+
+    v: [..., H, dh]; R: [H, dh, dh] with R[h] the orthonormal matrix of head h.
+    Returns z with the same shape as v; z[..., h, j] = sum_k R[h, k, j] v[..., h, k].
+    """
+    v, R = _f64(v), _f64(R)
+    return np.einsum("hkj,...hk->...hj", R, v)
+
+
+def back_rotate(u, R):
+    """o = R u per head (Sec. 3.2, routed representation back to value space)."""
+    u, R = _f64(u), _f64(R)
+    return np.einsum("hkj,...hj->...hk", R, u)
+
+
+def expand_mask(mask, G, dh):
+    """Diagonal of M_i = diag(m_{i,1} I_ds, ..., m_{i,S} I_ds) (Sec. 3.2).
+
+    mask: integer bitmask array (bit s set = group s kept). Returns a float64
+    array [..., dh] of 0/1 entries."""
+    ds = dh // G
+    mask = np.asarray(mask, dtype=np.uint64)
+    bits = (mask[..., None] >> np.arange(G, dtype=np.uint64)) & np.uint64(1)
+    return np.repeat(bits.astype(np.float64), ds, axis=-1)
+
+
+def routed_values(v, mask, R, G):
+    """v~ = R M R^T v with explicit dh x dh matrices per token and head (Sec. 3.2).
+
+    v: [B,T,H,dh]; mask [B,T]; R [H,dh,dh]. Plain but slow: builds each
+    projection matrix R_h M_i R_h^T."""
+    v, R = _f64(v), _f64(R)
+    B, T, H, dh = v.shape
+    mdiag = expand_mask(mask, G, dh)
+    out = np.zeros_like(v)
+    for b in range(B):
+        for t in range(T):
+            M = np.diag(mdiag[b, t])
+            for h in range(H):
+                P = R[h] @ M @ R[h].T
+                out[b, t, h] = P @ v[b, t, h]
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.3 latent role, Sec. 3.4 role-conditioned value routing
+# ----------------------------------------------------------------------------
+
+def softmax(x, axis=-1):
+    x = _f64(x)
+    m = np.max(x, axis=axis, keepdims=True)
+    e = np.exp(x - m)
+    return e / np.sum(e, axis=axis, keepdims=True)
+
+
+def latent_role(h, W_r, b_r):
+    """a = softmax(f_role(h)) with f_role linear (Eq. latentrole, Sec. 3.3)."""
+    return softmax(_f64(h) @ _f64(W_r).T + _f64(b_r), axis=-1)
+
+
+def language_pool(h, types):
+    """Pool of the retained language tokens' hidden states (Sec. 3.4).
+
+    h: [B,T,d]; types: [T] or [B,T]. Arithmetic mean per sample; the zero
+    vector when a sample has no language token."""
+    h = _f64(h)
+    types = np.broadcast_to(np.asarray(types), h.shape[:2])
+    out = np.zeros((h.shape[0], h.shape[2]))
+    for b in range(h.shape[0]):
+        sel = types[b] == LANG
+        if sel.any():
+            out[b] = h[b][sel].mean(axis=0)
+    return out
+
+
+def gelu(x, activation="gelu"):
+    """Exact GELU, x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)); 'identity' passes x."""
+    x = _f64(x)
+    if activation == "identity":
+        return x
+    return 0.5 * x * (1.0 + _erf(x / np.sqrt(2.0)))
+
+
+def router_mlp2(h, types, W_r, b_r, E, W1, b1, W2, b2, activation="gelu"):
+    """Group scores from [token state | role-mixed vector | pooled language].
+
+    Sec. 3.4 conditions the scores on the token's hidden state, its latent role
+    (Eq. latentrole) and the pooled language context. This learned form feeds
+    the concatenation [h | e | h_lang] with e = a E through one hidden layer:
+    gamma = W2 act(W1 [h|e|h_lang] + b1) + b2.
+    h: [B,T,d]; returns [B,T,G] float64."""
+    h = _f64(h)
+    B, T, d = h.shape
+    a = latent_role(h, W_r, b_r)                     # [B,T,C]
+    e = a @ _f64(E)                                  # [B,T,d_e]
+    hl = language_pool(h, types)                     # [B,d]
+    x = np.concatenate([h, e, np.broadcast_to(hl[:, None, :], (B, T, d))], axis=-1)
+    pre = x @ _f64(W1).T + _f64(b1)
+    return gelu(pre, activation) @ _f64(W2).T + _f64(b2)
+
+
+def router_additive(h, types, W_tok, b_tok, W_r, b_r, W_role, W_lang, b_lang,
+                    alpha_role=0.1, alpha_lang=0.1):
+    """Eq. routingscore: gamma = f_v(h) + alpha_role W_role a + alpha_lang f_lang(h_lang).
+
+    f_v and f_lang are linear heads d -> G with bias; W_role is G x C (Sec. 3.4).
+    alpha_role = alpha_lang = 0.1 in the paper's setup (Sec. 4.1)."""
+    h = _f64(h)
+    g_tok = h @ _f64(W_tok).T + _f64(b_tok)
+    a = latent_role(h, W_r, b_r)
+    g_role = a @ _f64(W_role).T
+    g_lang = language_pool(h, types) @ _f64(W_lang).T + _f64(b_lang)   # [B,G]
+    return g_tok + alpha_role * g_role + alpha_lang * g_lang[:, None, :]
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.4 Top-K_i selection, Sec. 3.5 token-type budgets
+# ----------------------------------------------------------------------------
+
+def group_budget(scores, types, mode, k_by_type, G, tau=0.0, kmin=0, kmax=0):
+    """K_i for every token (Sec. 3.5).
+
+    TOPK: K_i = min(K_type(i), G) (a fixed per-type budget K_m, Sec. 3.5).
+    THRESHOLD: K_i = clamp(#{s : gamma_s > tau}, kmin, kmax), then capped at G."""
+    scores = np.asarray(scores)
+    types = np.broadcast_to(np.asarray(types), scores.shape[:-1])
+    if mode == TOPK:
+        k = np.asarray(k_by_type)[types.astype(np.int64)]
+        return np.minimum(k, G).astype(np.int64)
+    cnt = np.sum(scores > tau, axis=-1)
+    return np.minimum(np.clip(cnt, kmin, kmax), G).astype(np.int64)
+
+
+def select_groups(scores, K):
+    """Keep the K_i groups with the highest routing scores (Sec. 3.4).
+
+    Order: larger score first; equal scores (with -0 equal to +0) by lower
+    group index; NaN after every number. Returns the bitmask [...] uint32.
+    The decision is taken on the scores exactly as given (no rounding)."""
+    scores = np.asarray(scores)
+    G = scores.shape[-1]
+    flat = scores.reshape(-1, G)
+    kf = np.broadcast_to(np.asarray(K), scores.shape[:-1]).reshape(-1)
+    isnan = np.isnan(flat)
+    val = np.where(isnan, 0.0, flat.astype(np.float64))
+    idx = np.broadcast_to(np.arange(G), flat.shape)
+    # lexsort: last key is primary -> NaN flag, then descending value, then index
+    order = np.lexsort((idx, -val, isnan), axis=-1)
+    masks = np.zeros(flat.shape[0], dtype=np.uint64)
+    for n in range(flat.shape[0]):
+        for s in order[n, : int(kf[n])]:
+            masks[n] |= np.uint64(1) << np.uint64(int(s))
+    return masks.astype(np.uint32).reshape(scores.shape[:-1])
+
+
+def popcount(mask):
+    mask = np.asarray(mask, dtype=np.uint64)
+    return np.array([bin(int(m)).count("1") for m in mask.reshape(-1)],
+                    dtype=np.int64).reshape(mask.shape)
+
+
+def mask_to_idx(mask, G):
+    """Kept group ids in ascending order, padded with 0xFF; and the counts."""
+    mask = np.asarray(mask, dtype=np.uint64)
+    idx = np.full(mask.shape + (G,), 0xFF, dtype=np.uint8)
+    cnt = np.zeros(mask.shape, dtype=np.uint8)
+    for pos in np.ndindex(mask.shape):
+        kept = [s for s in range(G) if (int(mask[pos]) >> s) & 1]
+        idx[pos][: len(kept)] = kept
+        cnt[pos] = len(kept)
+    return idx, cnt
+
+
+# ----------------------------------------------------------------------------
+# Compact group-indexed value cache (masked representation z~ = M z, Sec. 3.2)
+# ----------------------------------------------------------------------------
+
+def pack(z, mask, G, cap):
+    """Store only the kept groups of M_i z_i.
+
+    offsets[b, i] = number of groups kept by tokens 0..i-1 of sample b, and
+    offsets[b, T] is the sample's total. Vp[b, h, offsets[b,i] + r] holds the
+    r-th kept group (ascending group id) of token i, head h. Groups whose slot
+    would be >= cap are not stored (the offsets still count them).
+    z: [B,T,H,dh]; returns (offsets int64 [B,T+1], Vp float64 [B,H,cap,ds])."""
+    z = _f64(z)
+    B, T, H, dh = z.shape
+    ds = dh // G
+    pc = popcount(np.asarray(mask, dtype=np.uint64) & np.uint64((1 << G) - 1))
+    offsets = np.zeros((B, T + 1), dtype=np.int64)
+    offsets[:, 1:] = np.cumsum(pc, axis=1)
+    Vp = np.zeros((B, H, cap, ds))
+    for b in range(B):
+        for t in range(T):
+            m = int(mask[b, t])
+            r = 0
+            for s in range(G):
+                if (m >> s) & 1:
+                    slot = offsets[b, t] + r
+                    if slot < cap:
+                        Vp[b, :, slot, :] = z[b, t, :, s * ds:(s + 1) * ds]
+                    r += 1
+    return offsets, Vp
+
+
+def unpack(offsets, Vp, mask, G, T):
+    """Rebuild M_i z_i [B,T,H,dh] from the compact cache (dropped groups are 0)."""
+    Vp = _f64(Vp)
+    B, H, cap, ds = Vp.shape
+    out = np.zeros((B, T, H, G * ds))
+    for b in range(B):
+        for t in range(T):
+            m = int(mask[b, t])
+            r = 0
+            for s in range(G):
+                if (m >> s) & 1:
+                    slot = int(offsets[b, t]) + r
+                    if slot < cap:
+                        out[b, t, :, s * ds:(s + 1) * ds] = Vp[b, :, slot, :]
+                    r += 1
+    return out
+
+
+def packed_groups(offsets):
+    """Total groups stored per sample."""
+    return np.asarray(offsets)[:, -1]
+
+
+def kv_fraction(n_tokens_by_kind, kept_groups, G):
+    """Retained KV relative to dense KV (Sec. 4.2 and the language-KV equation).
+
+    Keys stay full width and values keep K_i / S of their width, so token i
+    costs (1 + K_i/S)/2 of a dense token. n_tokens_by_kind: total tokens in
+    the dense prefix; kept_groups: array of K_i for the tokens kept (a token not
+    routed has K_i = S)."""
+    kept_groups = np.asarray(kept_groups, dtype=np.float64)
+    return float(np.sum((1.0 + kept_groups / G) / 2.0) / n_tokens_by_kind)
+
+
+# ----------------------------------------------------------------------------
+# Attention with unchanged queries/keys over routed values (Sec. 3, Sec. 3.2)
+# ----------------------------------------------------------------------------
+
+def _scale(dh, scale):
+    return 1.0 / np.sqrt(dh) if (scale is None or scale == 0.0) else float(scale)
+
+
+def attend_packed(q, k, mask, offsets, Vp, R, G, scale=None):
+    """Method form: softmax(q k^T * scale) over all tokens, P.V accumulated in the
+    rotated space over each token's kept groups only, then o = R_h u.
+
+    q [B,Tq,H,dh], k [B,T,H,dh], mask [B,T], offsets [B,T+1], Vp [B,H,cap,ds],
+    R [H,dh,dh]. Returns [B,Tq,H,dh] float64."""
+    q, k = _f64(q), _f64(k)
+    B, Tq, H, dh = q.shape
+    T = k.shape[1]
+    zt = unpack(offsets, Vp, mask, G, T)                          # M z in rotated coords
+    s = np.einsum("bqhd,bthd->bhqt", q, k) * _scale(dh, scale)
+    p = softmax(s, axis=-1)
+    u = np.einsum("bhqt,bthd->bqhd", p, zt)
+    return back_rotate(u, R)
+
+
+def attend_plain(q, k, v, mask, R, G, scale=None):
+    """Plain form: textbook softmax attention whose values are the routed values
+    v~_i = R M_i R^T v_i built as explicit matrices (Sec. 3.2)."""
+    q, k = _f64(q), _f64(k)
+    B, Tq, H, dh = q.shape
+    vt = routed_values(v, mask, R, G)
+    s = np.einsum("bqhd,bthd->bhqt", q, k) * _scale(dh, scale)
+    p = softmax(s, axis=-1)
+    return np.einsum("bhqt,bthd->bqhd", p, vt)
+
+
+# ----------------------------------------------------------------------------
+# Whole path
+# ----------------------------------------------------------------------------
+
+def pipeline(h, q, k, v, types, weights, mode, k_by_type, G, tau=0.0, kmin=0, kmax=0,
+             scores=None, cap=None):
+    """route -> rotate -> pack -> attend for one layer.
+
+    weights: dict with R and the MLP2 router weights (W_r, b_r, E, W1, b1, W2, b2).
+    scores: optional given logits (selection only). Returns a dict of every
+    intermediate."""
+    T = np.asarray(k).shape[1]
+    if scores is None:
+        scores = router_mlp2(h, types, weights["W_r"], weights["b_r"], weights["E"],
+                             weights["W1"], weights["b1"], weights["W2"], weights["b2"])
+    K = group_budget(scores, types, mode, k_by_type, G, tau, kmin, kmax)
+    mask = select_groups(scores, K)
+    z = rotate(v, weights["R"])
+    if cap is None:
+        cap = T * G
+    offsets, Vp = pack(z, mask, G, cap)
+    out = attend_packed(q, k, mask, offsets, Vp, weights["R"], G)
+    return {"scores": scores, "K": K, "mask": mask, "z": z, "offsets": offsets,
+            "Vp": Vp, "out": out}
+
