@@ -1,0 +1,193 @@
+/*
+ * librolesub: the inference hot path of Role-Conditioned Sub-Token Routing
+ * (RoleSub) on AMD Instinct MI355X (gfx950).
+ *
+ * The four calls follow the paper's statement of the method (Sec. 3):
+ *   rolesub_rotate_values  z = R^T v per head              (Sec. 3.2)
+ *   rolesub_route          latent role + routing score + Top-K_i groups
+ *                                                           (Eq. latentrole,
+ *                                                            Eq. routingscore,
+ *                                                            Sec. 3.4, 3.5)
+ *   rolesub_pack_kv        compact cache of the kept groups of M z (Sec. 3.2)
+ *   rolesub_attend         attention with unchanged queries and keys over the
+ *                          routed values v~ = R M R^T v     (Sec. 3, 3.2)
+ *
+ * Conventions shared by every call
+ *   - Layouts are dense, row-major, innermost dimension last, no padding.
+ *   - Every tensor argument is a DEVICE pointer into memory the caller owns;
+ *     the library never allocates, frees or keeps device memory and holds no
+ *     state between calls. Descriptor structs are HOST pointers read during
+ *     the call only.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream). All
+ *     work is enqueued asynchronously on it; the call returns before the GPU
+ *     finishes. Inputs must stay valid and unmodified until then.
+ *   - Validation happens on the host before anything is enqueued. On any
+ *     non-OK status nothing was enqueued and the outputs are untouched, except
+ *     ROLESUB_ERR_HIP, where a launch failed (the message says which).
+ *     rolesub_last_error() returns a thread-local description of the most
+ *     recent failure on the calling thread.
+ *   - Element type: ROLESUB_F32 (float) or ROLESUB_BF16 (bfloat16). One dtype
+ *     covers all floating-point tensors of a call except scores (always f32).
+ *     Inside kernels accumulation and softmax are f32; bf16 outputs are
+ *     rounded to nearest even.
+ *   - Supported shapes: dh in {64, 128}; G divides dh; 1 <= G <= 32.
+ *     The bf16 path uses matrix-core kernels for dh = 128 and vector kernels
+ *     otherwise.
+ *
+ * Routing space reading: every head h has its own orthonormal R_h (dh x dh);
+ * group s of a token is the s-th slice of width ds = dh/G of each head's
+ * rotated value, and one group mask per token is shared by all heads. This is
+ * the paper's single R with R = blockdiag(R_h) up to a fixed permutation of
+ * coordinates, so the paper's losslessness property (all groups kept gives
+ * back v) holds unchanged.
+ */
+#ifndef ROLESUB_H
+#define ROLESUB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rolesub_status {
+  ROLESUB_OK = 0,
+  ROLESUB_ERR_INVALID_ARG = 1,  /* null pointer, negative size, K > G, ... */
+  ROLESUB_ERR_UNSUPPORTED = 2,  /* valid but not implemented: dh, G, dtype  */
+  ROLESUB_ERR_CAPACITY = 3,     /* packed-cache capacity below the budget   */
+  ROLESUB_ERR_HIP = 4           /* a HIP launch or runtime call failed      */
+} rolesub_status;
+
+typedef enum rolesub_dtype { ROLESUB_F32 = 0, ROLESUB_BF16 = 1 } rolesub_dtype;
+
+/* Token types of the multimodal sequence X = [X^vis, X^lang, X^prop, X^act]
+ * (Sec. 3). */
+enum { ROLESUB_VIS = 0, ROLESUB_LANG = 1, ROLESUB_PROP = 2, ROLESUB_ACT = 3 };
+
+/* B independent prefixes of T key/value tokens; H heads of width dh; G value
+ * groups per head (S in the paper); d hidden size of the router input. */
+typedef struct rolesub_dims {
+  int32_t B, T, H, dh, G, d;
+} rolesub_dims;
+
+/* Group budget per token (Sec. 3.5).
+ * TOPK:      K_i = k_by_type[type_i]           (0 <= k <= G; k = G keeps all)
+ * THRESHOLD: K_i = clamp(#{s : gamma_s > tau}, kmin, kmax)  (0<=kmin<=kmax<=G)
+ * Then the K_i groups with the largest scores are kept; equal scores go to
+ * the lower group index, -0 equals +0 and NaN ranks below every number. */
+enum { ROLESUB_BUDGET_TOPK = 0, ROLESUB_BUDGET_THRESHOLD = 1 };
+typedef struct rolesub_budget {
+  int32_t mode;
+  int32_t k_by_type[4];   /* indexed by ROLESUB_VIS .. ROLESUB_ACT */
+  float tau;
+  int32_t kmin, kmax;
+} rolesub_budget;
+
+/* Router weights (Sec. 3.3, 3.4). All matrices row-major [out][in] in the
+ * call's dtype; biases [out] in the call's dtype; device pointers.
+ *
+ * ROLESUB_ROUTER_MLP2 (learned scoring functions):
+ *   a     = softmax(W_r h + b_r)                 W_r [C][d], b_r [C]
+ *   e     = sum_c a_c E_c                        E [C][d_e]
+ *   hl    = mean of the sample's LANG rows of h (zero if it has none)
+ *   gamma = W2 gelu(W1 [h | e | hl] + b1) + b2   W1 [Hr][2d+d_e], b1 [Hr],
+ *                                                W2 [G][Hr], b2 [G]
+ *   gelu is the exact form x * Phi(x).
+ * ROLESUB_ROUTER_ADDITIVE (Eq. routingscore with linear heads):
+ *   gamma = W_tok h + b_tok + alpha_role W_role a + alpha_lang (W_lang hl + b_lang)
+ *   W_tok [G][d], b_tok [G], W_role [G][C], W_lang [G][d], b_lang [G];
+ *   a as above (W_r, b_r). */
+enum { ROLESUB_ROUTER_MLP2 = 0, ROLESUB_ROUTER_ADDITIVE = 1 };
+typedef struct rolesub_router {
+  int32_t kind;
+  int32_t C, d_e, Hr;
+  float alpha_role, alpha_lang;
+  const void *W_r, *b_r;
+  const void *E, *W1, *b1, *W2, *b2;                  /* MLP2     */
+  const void *W_tok, *b_tok, *W_role, *W_lang, *b_lang; /* ADDITIVE */
+} rolesub_router;
+
+const char* rolesub_status_str(rolesub_status s);
+const char* rolesub_last_error(void);
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t rolesub_version(void);
+
+/* ---------------------------------------------------------------------------
+ * rolesub_rotate_values: value into the orthogonal routing space (Sec. 3.2).
+ *   z[b,t,h,j] = sum_k R[h,k,j] * v[b,t,h,k]      (z = R_h^T v)
+ * v, z: [B,T,H,dh]; R: [H,dh,dh] (R[h] is R_h, orthonormal by contract, not
+ * checked). z must not overlap v. dims->G and dims->d are not used.
+ * ------------------------------------------------------------------------ */
+rolesub_status rolesub_rotate_values(const rolesub_dims* dims, rolesub_dtype dtype,
+                                     const void* v, const void* R, void* z, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * rolesub_route: routing scores and group selection (Eq. latentrole,
+ * Eq. routingscore, Sec. 3.4 Top-K_i, Sec. 3.5 budgets).
+ *   h          [B,T,d] hidden states (dtype)
+ *   token_type [B,T]   uint8, ROLESUB_VIS..ROLESUB_ACT
+ *   scores_in  [B,T,G] f32 or NULL. Non-NULL: the router is skipped and the
+ *              selection runs on these scores (router may then be NULL and h
+ *              is not read).
+ *   scores_out [B,T,G] f32 or NULL: the scores the selection used.
+ *   mask       [B,T]   uint32: bit s set = group s kept.
+ *   idx        [B,T,G] uint8 or NULL: kept group ids ascending, then 0xFF.
+ *   count      [B,T]   uint8 or NULL: K_i actually kept.
+ *   workspace  device scratch of at least rolesub_route_workspace_size()
+ *              bytes (may be NULL if that size is 0).
+ * ------------------------------------------------------------------------ */
+size_t rolesub_route_workspace_size(const rolesub_dims* dims, const rolesub_router* router);
+rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype,
+                             const rolesub_router* router, const rolesub_budget* budget,
+                             const void* h, const uint8_t* token_type, const float* scores_in,
+                             float* scores_out, uint32_t* mask, uint8_t* idx, uint8_t* count,
+                             void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * rolesub_pack_kv: the compact group-indexed value cache, i.e. the kept
+ * groups of z~ = M z (Sec. 3.2).
+ *   offsets[b,i] = sum_{j<i} popcount(mask[b,j] & (2^G-1)); offsets[b,T] = total
+ *   Vp[b,h,offsets[b,i]+r,:] = z[b,i,h, g_r*ds : (g_r+1)*ds]
+ * where g_r is the r-th set bit of mask[b,i] in ascending order.
+ *   z       [B,T,H,dh] (dtype), mask [B,T] uint32 (bits >= G ignored)
+ *   offsets [B,T+1] int32 (written)
+ *   Vp      [B,H,cap_groups,ds] (dtype, written; slots past offsets[b,T]
+ *           are not touched)
+ * Capacity: if budget and type_counts (host array [4], tokens of each type per
+ * sample) are both non-NULL, the call fails with ROLESUB_ERR_CAPACITY unless
+ * cap_groups >= sum_t type_counts[t]*min(k_by_type[t],G) (TOPK) or
+ * T*min(kmax,G) (THRESHOLD). Independently the kernel never writes a slot
+ * >= cap_groups; offsets still count every kept group, so offsets[b,T] >
+ * cap_groups reveals a mask that exceeded the capacity.
+ * ------------------------------------------------------------------------ */
+rolesub_status rolesub_pack_kv(const rolesub_dims* dims, rolesub_dtype dtype,
+                               const rolesub_budget* budget, const int32_t* type_counts,
+                               const void* z, const uint32_t* mask, int32_t* offsets, void* Vp,
+                               int64_t cap_groups, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * rolesub_attend: attention with full queries and keys over the routed
+ * values (Sec. 3: queries and keys unchanged; Sec. 3.2: v~ = R M R^T v).
+ *   s[q,i] = scale * <q_q, k_i> over all T tokens (no causal mask)
+ *   P      = softmax_i(s)
+ *   u_q    = sum_i P[q,i] * (M_i z_i)      accumulated from the packed groups
+ *   out_q  = R_h u_q
+ *   q   [B,Tq,H,dh], k [B,T,H,dh] (dtype); mask [B,T]; offsets [B,T+1] and
+ *   Vp [B,H,cap_groups,ds] as written by rolesub_pack_kv; R [H,dh,dh].
+ *   scale: 0 means 1/sqrt(dh).
+ *   out [B,Tq,H,dh] in out_dtype (f32 or the call's dtype).
+ * Packed slots >= cap_groups read as zero. workspace: at least
+ * rolesub_attend_workspace_size() bytes (0 for the current kernels).
+ * ------------------------------------------------------------------------ */
+size_t rolesub_attend_workspace_size(const rolesub_dims* dims, int32_t Tq);
+rolesub_status rolesub_attend(const rolesub_dims* dims, rolesub_dtype dtype, int32_t Tq,
+                              const void* q, const void* k, const uint32_t* mask,
+                              const int32_t* offsets, const void* Vp, int64_t cap_groups,
+                              const void* R, float scale, void* out, rolesub_dtype out_dtype,
+                              void* workspace, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ROLESUB_H */

@@ -1,0 +1,10 @@
+"""librolesub: RoleSub's inference hot path (rotate, route, pack, attend) on MI355X.
+
+The compute runs in hand-written HIP kernels for gfx950 behind a C ABI
+(include/rolesub.h); this package is its ctypes binding.
+"""
+from .rolesub import (  # noqa: F401
+    ACT, ADDITIVE, BF16, EXPORTS, F32, LANG, LIB_PATH, MLP2, PROP, THRESHOLD, TOPK, VIS, Budget, Dims,
+    Router, RouterDesc, RolesubError, attend, load, make_budget, pack_kv, rotate_values, route,
+    route_workspace_size, status_name,
+)

@@ -1,0 +1,85 @@
+// Shared device types and helpers of librolesub (gfx950 / CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rolesub {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float tof(float x) { return x; }
+__device__ __forceinline__ float tof(bf16 x) { return static_cast<float>(x); }
+
+template <class T> __device__ __forceinline__ T fromf(float x);
+template <> __device__ __forceinline__ float fromf<float>(float x) { return x; }
+// float -> bf16 conversion rounds to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+template <> __device__ __forceinline__ bf16 fromf<bf16>(float x) { return static_cast<bf16>(x); }
+
+// D = A(16x32) * B(32x16) + C on the bf16 matrix cores.
+// Lane l holds: A row l%16, k = 8*(l/16) .. +8;  B column l%16, same k;
+//               C/D column l%16, rows 4*(l/16) .. +4.
+__device__ __forceinline__ f32x4 mfma_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  bf16 a = static_cast<bf16>(lo), b = static_cast<bf16>(hi);
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
+         (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+}
+
+// Group-selection order (top-K_i, Sec. 3.4): a larger score ranks first,
+// -0 and +0 are equal, NaN ranks after every number, equal keys go to the
+// lower group index.
+__device__ __forceinline__ bool key_above(float a, float b) {
+  return !__builtin_isnan(a) && (__builtin_isnan(b) || a > b);
+}
+__device__ __forceinline__ bool key_equal(float a, float b) {
+  return (a == b) || (__builtin_isnan(a) && __builtin_isnan(b));
+}
+
+// Number of groups kept by one token (Sec. 3.5).
+__device__ __forceinline__ int budget_k(int mode, const int* k_by_type, int type, float tau,
+                                        int kmin, int kmax, int G, int n_above) {
+  int k;
+  if (mode == 0) {
+    k = (type >= 0 && type < 4) ? k_by_type[type] : G;
+  } else {
+    k = n_above < kmin ? kmin : (n_above > kmax ? kmax : n_above);
+  }
+  return k < G ? k : G;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, kWave);
+  return x;
+}
+
+__device__ __forceinline__ float gelu_exact(float x) {
+  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+}
+
+// Workgroup-to-XCD placement: consecutive workgroup ids go round-robin to the
+// 8 XCDs. Given a linear id over `n` items that are naturally grouped by a
+// "key" (heads) of size nkey, return an item order that keeps every key on a
+// single XCD so its shared operands stay in that XCD's L2.
+__device__ __forceinline__ void xcd_split(int lin, int nkey, int& key, int& rest) {
+  if ((nkey & 7) == 0) {
+    const int xcd = lin & 7, slot = lin >> 3, per = nkey >> 3;
+    key = xcd + 8 * (slot % per);
+    rest = slot / per;
+  } else {
+    key = lin % nkey;
+    rest = lin / nkey;
+  }
+}
+
+}  // namespace rolesub

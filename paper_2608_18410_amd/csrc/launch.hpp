@@ -1,0 +1,62 @@
+// Internal launcher interface between the C-ABI layer and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rolesub {
+
+struct RouteParams {
+  int B, T, d, G, C, d_e, Hr, kind;
+  float alpha_role, alpha_lang;
+  const void* h;
+  const uint8_t* types;
+  const void *W_r, *b_r, *E, *W1, *b1, *W2, *b2;
+  const void *W_tok, *b_tok, *W_role, *W_lang, *b_lang;
+  float* cb;  // [B][Hr or G] per-sample language term (workspace)
+  float* F;   // [Hr or G][C] folded role term (workspace)
+  int mode;
+  int k_by_type[4];
+  float tau;
+  int kmin, kmax;
+  const float* scores_in;
+  float* scores_out;
+  uint32_t* mask;
+  uint8_t* idx;
+  uint8_t* count;
+};
+
+// Sizes of the route workspace pieces (floats).
+inline size_t route_cb_floats(int B, int Hr, int G, int kind) {
+  return static_cast<size_t>(B) * (kind == 0 ? Hr : G);
+}
+inline size_t route_F_floats(int Hr, int G, int C, int kind) {
+  return static_cast<size_t>(kind == 0 ? Hr : G) * C;
+}
+
+hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s);
+// LDS bytes the generic (one token per workgroup) router needs.
+size_t route_generic_shm(int d, int G, int C, int Hr, int kind);
+hipError_t launch_select(const RouteParams& p, hipStream_t s);
+
+hipError_t launch_rotate(bool bf16, int ntok, int H, int dh, const void* v, const void* R, void* z,
+                         hipStream_t s);
+
+hipError_t launch_pack(bool bf16, int B, int T, int H, int dh, int G, const void* z,
+                       const uint32_t* mask, int32_t* offsets, void* Vp, int64_t cap,
+                       hipStream_t s);
+
+struct AttendParams {
+  int B, T, H, dh, G, Tq;
+  const void *q, *k;
+  const uint32_t* mask;
+  const int32_t* offsets;
+  const void* Vp;
+  int64_t cap;
+  const void* R;
+  float scale;
+  void* out;
+  int out_f32;
+};
+hipError_t launch_attend(const AttendParams& p, bool bf16, hipStream_t s);
+
+}  // namespace rolesub

@@ -1,0 +1,299 @@
+// C ABI of librolesub: host-side validation, then asynchronous launches on the
+// caller's stream. No allocation, no state between calls.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "launch.hpp"
+#include "rolesub.h"
+
+using namespace rolesub;
+
+namespace {
+
+thread_local std::string g_err;
+
+rolesub_status fail(rolesub_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+rolesub_status from_hip(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ROLESUB_OK;
+  return fail(ROLESUB_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool valid_dtype(rolesub_dtype t) { return t == ROLESUB_F32 || t == ROLESUB_BF16; }
+size_t esize(rolesub_dtype t) { return t == ROLESUB_F32 ? 4 : 2; }
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+// B, T >= 0; H >= 1; dh in {64, 128}.
+rolesub_status check_value_dims(const rolesub_dims* d, const char* fn) {
+  if (!d) return fail(ROLESUB_ERR_INVALID_ARG, "%s: dims is NULL", fn);
+  if (d->B < 0 || d->T < 0 || d->H < 1)
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: need B >= 0, T >= 0, H >= 1 (got B=%d T=%d H=%d)", fn,
+                d->B, d->T, d->H);
+  if (d->dh != 64 && d->dh != 128)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: head dim %d not supported (64 or 128)", fn, d->dh);
+  return ROLESUB_OK;
+}
+
+rolesub_status check_groups(const rolesub_dims* d, const char* fn, bool need_dh) {
+  if (d->G < 1 || d->G > 32)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: G=%d groups not supported (1..32)", fn, d->G);
+  if (need_dh && d->dh % d->G != 0)
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: G=%d does not divide dh=%d", fn, d->G, d->dh);
+  return ROLESUB_OK;
+}
+
+rolesub_status check_budget(const rolesub_budget* bu, int G, const char* fn) {
+  if (!bu) return fail(ROLESUB_ERR_INVALID_ARG, "%s: budget is NULL", fn);
+  if (bu->mode == ROLESUB_BUDGET_TOPK) {
+    for (int t = 0; t < 4; ++t)
+      if (bu->k_by_type[t] < 0 || bu->k_by_type[t] > G)
+        return fail(ROLESUB_ERR_INVALID_ARG, "%s: k_by_type[%d]=%d outside 0..G=%d", fn, t,
+                    bu->k_by_type[t], G);
+  } else if (bu->mode == ROLESUB_BUDGET_THRESHOLD) {
+    if (bu->kmin < 0 || bu->kmin > bu->kmax || bu->kmax > G)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: need 0 <= kmin <= kmax <= G (kmin=%d kmax=%d G=%d)",
+                  fn, bu->kmin, bu->kmax, G);
+    if (std::isnan(bu->tau)) return fail(ROLESUB_ERR_INVALID_ARG, "%s: tau is NaN", fn);
+  } else {
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: unknown budget mode %d", fn, bu->mode);
+  }
+  return ROLESUB_OK;
+}
+
+bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const char* x = static_cast<const char*>(a);
+  const char* y = static_cast<const char*>(b);
+  return x < y + nb && y < x + na;
+}
+
+size_t route_ws_bytes(const rolesub_dims* d, const rolesub_router* r) {
+  if (!d || !r || d->B <= 0) return 0;
+  return align256(route_cb_floats(d->B, r->Hr, d->G, r->kind) * sizeof(float)) +
+         align256(route_F_floats(r->Hr, d->G, r->C, r->kind) * sizeof(float));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rolesub_status_str(rolesub_status s) {
+  switch (s) {
+    case ROLESUB_OK: return "ROLESUB_OK";
+    case ROLESUB_ERR_INVALID_ARG: return "ROLESUB_ERR_INVALID_ARG";
+    case ROLESUB_ERR_UNSUPPORTED: return "ROLESUB_ERR_UNSUPPORTED";
+    case ROLESUB_ERR_CAPACITY: return "ROLESUB_ERR_CAPACITY";
+    case ROLESUB_ERR_HIP: return "ROLESUB_ERR_HIP";
+  }
+  return "ROLESUB_UNKNOWN_STATUS";
+}
+
+const char* rolesub_last_error(void) { return g_err.c_str(); }
+
+int32_t rolesub_version(void) { return 100; }
+
+rolesub_status rolesub_rotate_values(const rolesub_dims* dims, rolesub_dtype dtype, const void* v,
+                                     const void* R, void* z, void* stream) {
+  const char* fn = "rolesub_rotate_values";
+  rolesub_status st = check_value_dims(dims, fn);
+  if (st) return st;
+  if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+  const size_t ntok = static_cast<size_t>(dims->B) * dims->T;
+  if (ntok == 0) return ROLESUB_OK;
+  if (!v || !R || !z) return fail(ROLESUB_ERR_INVALID_ARG, "%s: v, R and z must be non-NULL", fn);
+  if (ntok > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
+  const size_t bytes = ntok * dims->H * dims->dh * esize(dtype);
+  if (ranges_overlap(v, bytes, z, bytes)) return fail(ROLESUB_ERR_INVALID_ARG, "%s: z overlaps v", fn);
+  return from_hip(launch_rotate(dtype == ROLESUB_BF16, static_cast<int>(ntok), dims->H, dims->dh, v, R,
+                                z, static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+size_t rolesub_route_workspace_size(const rolesub_dims* dims, const rolesub_router* router) {
+  return route_ws_bytes(dims, router);
+}
+
+rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype, const rolesub_router* router,
+                             const rolesub_budget* budget, const void* h, const uint8_t* token_type,
+                             const float* scores_in, float* scores_out, uint32_t* mask, uint8_t* idx,
+                             uint8_t* count, void* workspace, size_t ws_bytes, void* stream) {
+  const char* fn = "rolesub_route";
+  if (!dims) return fail(ROLESUB_ERR_INVALID_ARG, "%s: dims is NULL", fn);
+  if (dims->B < 0 || dims->T < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: need B >= 0, T >= 0", fn);
+  rolesub_status st = check_groups(dims, fn, false);
+  if (st) return st;
+  if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+  st = check_budget(budget, dims->G, fn);
+  if (st) return st;
+  const size_t ntok = static_cast<size_t>(dims->B) * dims->T;
+  if (ntok == 0) return ROLESUB_OK;
+  if (ntok > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
+  if (!mask) return fail(ROLESUB_ERR_INVALID_ARG, "%s: mask must be non-NULL", fn);
+  const bool need_types = budget->mode == ROLESUB_BUDGET_TOPK || scores_in == nullptr;
+  if (need_types && !token_type)
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: token_type must be non-NULL", fn);
+
+  RouteParams p = {};
+  p.B = dims->B;
+  p.T = dims->T;
+  p.d = dims->d;
+  p.G = dims->G;
+  p.types = token_type;
+  p.mode = budget->mode;
+  for (int t = 0; t < 4; ++t) p.k_by_type[t] = budget->k_by_type[t];
+  p.tau = budget->tau;
+  p.kmin = budget->kmin;
+  p.kmax = budget->kmax;
+  p.scores_in = scores_in;
+  p.scores_out = scores_out;
+  p.mask = mask;
+  p.idx = idx;
+  p.count = count;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (scores_in) return from_hip(launch_select(p, s), fn);
+
+  if (!router) return fail(ROLESUB_ERR_INVALID_ARG, "%s: router is NULL and no scores_in given", fn);
+  if (!h) return fail(ROLESUB_ERR_INVALID_ARG, "%s: h must be non-NULL", fn);
+  if (dims->d < 1) return fail(ROLESUB_ERR_INVALID_ARG, "%s: hidden size d=%d", fn, dims->d);
+  if (router->C < 1 || router->C > 64)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: C=%d latent roles not supported (1..64)", fn, router->C);
+  if (!router->W_r || !router->b_r) return fail(ROLESUB_ERR_INVALID_ARG, "%s: W_r/b_r are NULL", fn);
+  if (router->kind == ROLESUB_ROUTER_MLP2) {
+    if (router->d_e < 1 || router->Hr < 1)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: need d_e >= 1 and Hr >= 1", fn);
+    if (!router->E || !router->W1 || !router->b1 || !router->W2 || !router->b2)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: MLP2 router weights are NULL", fn);
+  } else if (router->kind == ROLESUB_ROUTER_ADDITIVE) {
+    if (!router->W_tok || !router->b_tok || !router->W_role || !router->W_lang || !router->b_lang)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: additive router weights are NULL", fn);
+  } else {
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: unknown router kind %d", fn, router->kind);
+  }
+  if (route_generic_shm(dims->d, dims->G, router->C, router->Hr, router->kind) > 64 * 1024 ||
+      static_cast<size_t>(dims->d) * sizeof(float) > 64 * 1024)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: hidden size d=%d too large", fn, dims->d);
+  const size_t need = route_ws_bytes(dims, router);
+  if (ws_bytes < need || (need && !workspace))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws_bytes);
+
+  p.d_e = router->d_e;
+  p.Hr = router->Hr;
+  p.C = router->C;
+  p.kind = router->kind;
+  p.alpha_role = router->alpha_role;
+  p.alpha_lang = router->alpha_lang;
+  p.h = h;
+  p.W_r = router->W_r;
+  p.b_r = router->b_r;
+  p.E = router->E;
+  p.W1 = router->W1;
+  p.b1 = router->b1;
+  p.W2 = router->W2;
+  p.b2 = router->b2;
+  p.W_tok = router->W_tok;
+  p.b_tok = router->b_tok;
+  p.W_role = router->W_role;
+  p.W_lang = router->W_lang;
+  p.b_lang = router->b_lang;
+  char* ws = static_cast<char*>(workspace);
+  p.cb = reinterpret_cast<float*>(ws);
+  p.F = reinterpret_cast<float*>(ws + align256(route_cb_floats(p.B, p.Hr, p.G, p.kind) * sizeof(float)));
+  return from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
+}
+
+rolesub_status rolesub_pack_kv(const rolesub_dims* dims, rolesub_dtype dtype, const rolesub_budget* budget,
+                               const int32_t* type_counts, const void* z, const uint32_t* mask,
+                               int32_t* offsets, void* Vp, int64_t cap_groups, void* stream) {
+  const char* fn = "rolesub_pack_kv";
+  rolesub_status st = check_value_dims(dims, fn);
+  if (st) return st;
+  st = check_groups(dims, fn, true);
+  if (st) return st;
+  if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+  if (cap_groups < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: cap_groups < 0", fn);
+  if (budget && type_counts) {
+    st = check_budget(budget, dims->G, fn);
+    if (st) return st;
+    int64_t need = 0;
+    if (budget->mode == ROLESUB_BUDGET_TOPK) {
+      for (int t = 0; t < 4; ++t) {
+        if (type_counts[t] < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: type_counts[%d] < 0", fn, t);
+        need += static_cast<int64_t>(type_counts[t]) * std::min(budget->k_by_type[t], dims->G);
+      }
+    } else {
+      need = static_cast<int64_t>(dims->T) * std::min(budget->kmax, dims->G);
+    }
+    if (cap_groups < need)
+      return fail(ROLESUB_ERR_CAPACITY, "%s: cap_groups=%lld below the budget of %lld groups", fn,
+                  static_cast<long long>(cap_groups), static_cast<long long>(need));
+  }
+  if (dims->B == 0) return ROLESUB_OK;
+  if (!mask || !offsets || (dims->T > 0 && !z) || (cap_groups > 0 && dims->T > 0 && !Vp))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: z, mask, offsets and Vp must be non-NULL", fn);
+  if (static_cast<size_t>(dims->B) * dims->T > 0x7FFFFFFF)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
+  return from_hip(launch_pack(dtype == ROLESUB_BF16, dims->B, dims->T, dims->H, dims->dh, dims->G, z, mask,
+                              offsets, Vp, cap_groups, static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+size_t rolesub_attend_workspace_size(const rolesub_dims* dims, int32_t Tq) {
+  (void)dims;
+  (void)Tq;
+  return 0;
+}
+
+rolesub_status rolesub_attend(const rolesub_dims* dims, rolesub_dtype dtype, int32_t Tq, const void* q,
+                              const void* k, const uint32_t* mask, const int32_t* offsets, const void* Vp,
+                              int64_t cap_groups, const void* R, float scale, void* out,
+                              rolesub_dtype out_dtype, void* workspace, size_t ws_bytes, void* stream) {
+  const char* fn = "rolesub_attend";
+  (void)workspace;
+  (void)ws_bytes;
+  rolesub_status st = check_value_dims(dims, fn);
+  if (st) return st;
+  st = check_groups(dims, fn, true);
+  if (st) return st;
+  if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+  if (out_dtype != ROLESUB_F32 && out_dtype != dtype)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: out_dtype must be f32 or the input dtype", fn);
+  if (Tq < 0 || cap_groups < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: Tq and cap_groups must be >= 0", fn);
+  if (!std::isfinite(scale)) return fail(ROLESUB_ERR_INVALID_ARG, "%s: scale is not finite", fn);
+  if (dims->B == 0 || Tq == 0) return ROLESUB_OK;
+  if (dims->T < 1) return fail(ROLESUB_ERR_INVALID_ARG, "%s: attention over T=0 tokens is undefined", fn);
+  if (!q || !k || !mask || !offsets || !R || !out || (cap_groups > 0 && !Vp))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: a tensor pointer is NULL", fn);
+  if (static_cast<size_t>(dims->B) * dims->H > 0x7FFFFFFF ||
+      static_cast<size_t>(dims->B) * dims->H * Tq > 0x7FFFFFFF)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: grid too large", fn);
+  AttendParams p = {};
+  p.B = dims->B;
+  p.T = dims->T;
+  p.H = dims->H;
+  p.dh = dims->dh;
+  p.G = dims->G;
+  p.Tq = Tq;
+  p.q = q;
+  p.k = k;
+  p.mask = mask;
+  p.offsets = offsets;
+  p.Vp = Vp;
+  p.cap = cap_groups;
+  p.R = R;
+  p.scale = scale == 0.f ? 1.f / std::sqrt(static_cast<float>(dims->dh)) : scale;
+  p.out = out;
+  p.out_f32 = out_dtype == ROLESUB_F32;
+  return from_hip(launch_attend(p, dtype == ROLESUB_BF16, static_cast<hipStream_t>(stream)), fn);
+}
+
+}  // extern "C"

@@ -1,0 +1,60 @@
+"""One layer of the hot path, route -> rotate -> pack -> attend, through the C ABI.
+
+Orchestration only: buffers are allocated once per shape and reused, and the
+four library calls are issued in order on one stream.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from . import rolesub as rs
+
+
+def pack_capacity(mode: int, k_by_type, type_counts, T: int, G: int, kmax: int = 0) -> int:
+    """Groups per (sample, head) the packed cache must hold for a budget."""
+    if mode == rs.TOPK:
+        return int(sum(n * min(k, G) for n, k in zip(type_counts, k_by_type)))
+    return int(T * min(kmax, G))
+
+
+@dataclass
+class LayerBuffers:
+    mask: torch.Tensor
+    idx: torch.Tensor
+    count: torch.Tensor
+    scores: torch.Tensor
+    z: torch.Tensor
+    offsets: torch.Tensor
+    Vp: torch.Tensor
+    out: torch.Tensor
+    workspace: torch.Tensor
+
+    @staticmethod
+    def allocate(B, T, H, dh, G, Tq, cap, dtype, out_dtype=None, ws_bytes=0, device="cuda"):
+        u8, i32, f32 = torch.uint8, torch.int32, torch.float32
+        return LayerBuffers(
+            mask=torch.empty((B, T), dtype=i32, device=device),
+            idx=torch.empty((B, T, G), dtype=u8, device=device),
+            count=torch.empty((B, T), dtype=u8, device=device),
+            scores=torch.empty((B, T, G), dtype=f32, device=device),
+            z=torch.empty((B, T, H, dh), dtype=dtype, device=device),
+            offsets=torch.empty((B, T + 1), dtype=i32, device=device),
+            Vp=torch.empty((B, H, cap, dh // G), dtype=dtype, device=device),
+            out=torch.empty((B, Tq, H, dh), dtype=out_dtype or dtype, device=device),
+            workspace=torch.empty(max(int(ws_bytes), 256), dtype=u8, device=device),
+        )
+
+
+def run_layer(h, q, k, v, types, R, budget: rs.Budget, G: int, bufs: LayerBuffers,
+              router: rs.Router | None = None, scores_in=None, type_counts=None, stream=None):
+    """route -> rotate -> pack -> attend. Returns the buffers (filled asynchronously)."""
+    rs.route(types, budget, G, h=h, router=router, scores_in=scores_in, workspace=bufs.workspace,
+             out={"mask": bufs.mask, "idx": bufs.idx, "count": bufs.count, "scores": bufs.scores},
+             stream=stream)
+    rs.rotate_values(v, R, out=bufs.z, stream=stream)
+    rs.pack_kv(bufs.z, bufs.mask, G, bufs.Vp.shape[2], budget=budget, type_counts=type_counts,
+               out=(bufs.offsets, bufs.Vp), stream=stream)
+    rs.attend(q, k, bufs.mask, bufs.offsets, bufs.Vp, R, G, out=bufs.out, stream=stream)
+    return bufs

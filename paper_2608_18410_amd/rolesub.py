@@ -1,0 +1,238 @@
+"""ctypes binding of librolesub.
+
+Argument marshalling only: every step of the hot path runs in the library's
+HIP kernels. torch tensors supply device memory (data_ptr) and the current
+HIP stream. Loading fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "librolesub.so")
+
+F32, BF16 = 0, 1
+VIS, LANG, PROP, ACT = 0, 1, 2, 3
+TOPK, THRESHOLD = 0, 1
+MLP2, ADDITIVE = 0, 1
+
+EXPORTS = (
+    "rolesub_status_str", "rolesub_last_error", "rolesub_version",
+    "rolesub_rotate_values", "rolesub_route_workspace_size", "rolesub_route",
+    "rolesub_pack_kv", "rolesub_attend_workspace_size", "rolesub_attend",
+)
+
+
+class RolesubError(RuntimeError):
+    def __init__(self, fn: str, status: int, message: str):
+        super().__init__(f"{fn} -> {status_name(status)}: {message}")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "T", "H", "dh", "G", "d")]
+
+
+class Budget(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("k_by_type", ctypes.c_int32 * 4), ("tau", ctypes.c_float),
+                ("kmin", ctypes.c_int32), ("kmax", ctypes.c_int32)]
+
+
+class RouterDesc(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("C", ctypes.c_int32), ("d_e", ctypes.c_int32),
+                ("Hr", ctypes.c_int32), ("alpha_role", ctypes.c_float), ("alpha_lang", ctypes.c_float)] + \
+               [(n, ctypes.c_void_p) for n in ("W_r", "b_r", "E", "W1", "b1", "W2", "b2",
+                                               "W_tok", "b_tok", "W_role", "W_lang", "b_lang")]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load librolesub.so (built in-tree by paper_2608_18410_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"librolesub is not built ({path} is missing); "
+                          "run `python -m paper_2608_18410_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.rolesub_status_str.argtypes = [ctypes.c_int]
+    lib.rolesub_status_str.restype = ctypes.c_char_p
+    lib.rolesub_last_error.argtypes = []
+    lib.rolesub_last_error.restype = ctypes.c_char_p
+    lib.rolesub_version.argtypes = []
+    lib.rolesub_version.restype = I32
+    lib.rolesub_rotate_values.argtypes = [P, ctypes.c_int, P, P, P, P]
+    lib.rolesub_route_workspace_size.argtypes = [P, P]
+    lib.rolesub_route_workspace_size.restype = SZ
+    lib.rolesub_route.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.rolesub_pack_kv.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, I64, P]
+    lib.rolesub_attend_workspace_size.argtypes = [P, I32]
+    lib.rolesub_attend_workspace_size.restype = SZ
+    lib.rolesub_attend.argtypes = [P, ctypes.c_int, I32, P, P, P, P, P, I64, P, ctypes.c_float, P,
+                                   ctypes.c_int, P, SZ, P]
+    for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_attend"):
+        getattr(lib, fn).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_name(status: int) -> str:
+    return load().rolesub_status_str(status).decode()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise RolesubError(fn, status, load().rolesub_last_error().decode())
+
+
+def _code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t, dtype=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch tensor")
+    if not t.is_cuda:
+        raise ValueError("librolesub takes device tensors only")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"expected {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def make_budget(mode=TOPK, k_by_type=(0, 0, 0, 0), tau=0.0, kmin=0, kmax=0) -> Budget:
+    b = Budget()
+    b.mode = mode
+    for i, k in enumerate(k_by_type):
+        b.k_by_type[i] = int(k)
+    b.tau, b.kmin, b.kmax = float(tau), int(kmin), int(kmax)
+    return b
+
+
+@dataclass
+class Router:
+    """Router weights as device tensors (kept alive while calls are in flight)."""
+    kind: int
+    C: int
+    tensors: dict
+    d_e: int = 0
+    Hr: int = 0
+    alpha_role: float = 0.1
+    alpha_lang: float = 0.1
+
+    def desc(self) -> RouterDesc:
+        r = RouterDesc()
+        r.kind, r.C, r.d_e, r.Hr = self.kind, self.C, self.d_e, self.Hr
+        r.alpha_role, r.alpha_lang = self.alpha_role, self.alpha_lang
+        for name, t in self.tensors.items():
+            setattr(r, name, _ptr(t).value)
+        return r
+
+    @staticmethod
+    def mlp2(W_r, b_r, E, W1, b1, W2, b2) -> "Router":
+        return Router(MLP2, W_r.shape[0], dict(W_r=W_r, b_r=b_r, E=E, W1=W1, b1=b1, W2=W2, b2=b2),
+                      d_e=E.shape[1], Hr=W1.shape[0])
+
+    @staticmethod
+    def additive(W_tok, b_tok, W_r, b_r, W_role, W_lang, b_lang, alpha_role=0.1, alpha_lang=0.1):
+        return Router(ADDITIVE, W_r.shape[0], dict(W_tok=W_tok, b_tok=b_tok, W_r=W_r, b_r=b_r,
+                                                   W_role=W_role, W_lang=W_lang, b_lang=b_lang),
+                      alpha_role=alpha_role, alpha_lang=alpha_lang)
+
+
+# ----------------------------------------------------------------------------
+# The four calls
+# ----------------------------------------------------------------------------
+
+def rotate_values(v: torch.Tensor, R: torch.Tensor, out: torch.Tensor | None = None, stream=None):
+    """z = R_h^T v per head. v [B,T,H,dh], R [H,dh,dh]."""
+    B, T, H, dh = v.shape
+    z = torch.empty_like(v) if out is None else out
+    dims = Dims(B, T, H, dh, 1, 0)
+    _check("rolesub_rotate_values", load().rolesub_rotate_values(
+        ctypes.byref(dims), _code(v), _ptr(v), _ptr(R, v.dtype), _ptr(z, v.dtype), _stream(stream)))
+    return z
+
+
+def route_workspace_size(B, T, G, d, router: Router) -> int:
+    dims = Dims(B, T, 1, 64, G, d)
+    desc = router.desc()
+    return load().rolesub_route_workspace_size(ctypes.byref(dims), ctypes.byref(desc))
+
+
+def route(token_type: torch.Tensor, budget: Budget, G: int, h: torch.Tensor | None = None,
+          router: Router | None = None, scores_in: torch.Tensor | None = None, *,
+          want_scores=True, want_idx=True, want_count=True, workspace=None, out=None, stream=None):
+    """Routing scores and group selection. Returns dict(mask, idx, count, scores)."""
+    B, T = token_type.shape
+    dev = token_type.device
+    d = 0 if h is None else h.shape[2]
+    dtype = torch.float32 if h is None else h.dtype
+    o = out or {}
+    mask = o.get("mask", torch.empty((B, T), dtype=torch.int32, device=dev))
+    idx = o.get("idx", torch.empty((B, T, G), dtype=torch.uint8, device=dev)) if want_idx else None
+    cnt = o.get("count", torch.empty((B, T), dtype=torch.uint8, device=dev)) if want_count else None
+    sco = o.get("scores", torch.empty((B, T, G), dtype=torch.float32, device=dev)) if want_scores else None
+    dims = Dims(B, T, 1, 64, G, d)
+    desc = router.desc() if router is not None else None
+    ws_ptr, ws_bytes = None, 0
+    if scores_in is None and router is not None:
+        ws_bytes = load().rolesub_route_workspace_size(ctypes.byref(dims), ctypes.byref(desc))
+        if workspace is None:
+            workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel()
+    _check("rolesub_route", load().rolesub_route(
+        ctypes.byref(dims), _code(torch.empty(0, dtype=dtype)),
+        ctypes.byref(desc) if desc is not None else None, ctypes.byref(budget),
+        _ptr(h), _ptr(token_type, torch.uint8), _ptr(scores_in, torch.float32), _ptr(sco),
+        _ptr(mask), _ptr(idx), _ptr(cnt), ws_ptr, ws_bytes, _stream(stream)))
+    return {"mask": mask, "idx": idx, "count": cnt, "scores": sco}
+
+
+def pack_kv(z: torch.Tensor, mask: torch.Tensor, G: int, cap: int, budget: Budget | None = None,
+            type_counts=None, out=None, stream=None):
+    """Compact group-indexed cache. Returns (offsets [B,T+1] int32, Vp [B,H,cap,ds])."""
+    B, T, H, dh = z.shape
+    ds = dh // G
+    offsets = torch.empty((B, T + 1), dtype=torch.int32, device=z.device) if out is None else out[0]
+    Vp = torch.empty((B, H, cap, ds), dtype=z.dtype, device=z.device) if out is None else out[1]
+    dims = Dims(B, T, H, dh, G, 0)
+    tc = (ctypes.c_int32 * 4)(*type_counts) if type_counts is not None else None
+    _check("rolesub_pack_kv", load().rolesub_pack_kv(
+        ctypes.byref(dims), _code(z), ctypes.byref(budget) if budget is not None else None, tc,
+        _ptr(z), _ptr(mask), _ptr(offsets, torch.int32), _ptr(Vp, z.dtype), int(cap), _stream(stream)))
+    return offsets, Vp
+
+
+def attend(q, k, mask, offsets, Vp, R, G: int, scale: float = 0.0, out_dtype=None, out=None, stream=None):
+    """Attention with full q, k over the packed routed values; returns [B,Tq,H,dh]."""
+    B, Tq, H, dh = q.shape
+    T = k.shape[1]
+    cap = Vp.shape[2]
+    odt = q.dtype if out_dtype is None else out_dtype
+    o = torch.empty((B, Tq, H, dh), dtype=odt, device=q.device) if out is None else out
+    dims = Dims(B, T, H, dh, G, 0)
+    _check("rolesub_attend", load().rolesub_attend(
+        ctypes.byref(dims), _code(q), Tq, _ptr(q), _ptr(k, q.dtype), _ptr(mask), _ptr(offsets, torch.int32),
+        _ptr(Vp, q.dtype), int(cap), _ptr(R, q.dtype), float(scale), _ptr(o), _code(o), None, 0,
+        _stream(stream)))
+    return o

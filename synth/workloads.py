@@ -207,15 +207,12 @@ def additive_weights(w: Workload, layer: int) -> dict:
     return {k: round_to(v, w.dtype) for k, v in out.items()}
 
 
-def sample_activations(w: Workload, layer: int, b: int) -> dict:
+def sample_activations(w: Workload, layer: int, b: int, names=("h", "q", "k", "v")) -> dict:
     """Hidden states h [T,d] and q [Tq,H,dh], k/v [T,H,dh] of one prefix, all N(0,1)."""
     s, T = w.seed, w.T
-    return {
-        "h": round_to(_normal(s, (layer, 1, b, _A_H), (T, w.d)), w.dtype),
-        "q": round_to(_normal(s, (layer, 1, b, _A_Q), (w.Tq, w.H, w.dh)), w.dtype),
-        "k": round_to(_normal(s, (layer, 1, b, _A_K), (T, w.H, w.dh)), w.dtype),
-        "v": round_to(_normal(s, (layer, 1, b, _A_V), (T, w.H, w.dh)), w.dtype),
-    }
+    spec = {"h": (_A_H, (T, w.d)), "q": (_A_Q, (w.Tq, w.H, w.dh)),
+            "k": (_A_K, (T, w.H, w.dh)), "v": (_A_V, (T, w.H, w.dh))}
+    return {n: round_to(_normal(s, (layer, 1, b, spec[n][0]), spec[n][1]), w.dtype) for n in names}
 
 
 def sample_scores(w: Workload, layer: int, b: int) -> np.ndarray:

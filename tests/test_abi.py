@@ -1,0 +1,124 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before touching the GPU (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_18410_amd as rs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rolesub.h")
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation first
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(rolesub_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rs.LIB_PATH):
+        pytest.fail("librolesub.so is not built; run python -m paper_2608_18410_amd.build")
+    return rs.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(rs.EXPORTS) == set(names)
+
+
+def test_status_strings_and_version(lib):
+    for code, name in enumerate(["ROLESUB_OK", "ROLESUB_ERR_INVALID_ARG", "ROLESUB_ERR_UNSUPPORTED",
+                                 "ROLESUB_ERR_CAPACITY", "ROLESUB_ERR_HIP"]):
+        assert rs.status_name(code) == name
+    assert lib.rolesub_version() >= 100
+
+
+def _dims(B=1, T=4, H=2, dh=64, G=8, d=32):
+    return rs.Dims(B, T, H, dh, G, d)
+
+
+def _last():
+    return rs.load().rolesub_last_error().decode()
+
+
+def test_rotate_validation(lib):
+    d = _dims(dh=96)
+    assert lib.rolesub_rotate_values(ctypes.byref(d), rs.BF16, FAKE, FAKE, FAKE, None) == 2
+    assert "head dim" in _last()
+    d = _dims()
+    assert lib.rolesub_rotate_values(ctypes.byref(d), rs.BF16, None, FAKE, FAKE, None) == 1
+    assert lib.rolesub_rotate_values(ctypes.byref(d), 7, FAKE, FAKE, FAKE, None) == 2
+    assert lib.rolesub_rotate_values(None, rs.BF16, FAKE, FAKE, FAKE, None) == 1
+    # z aliasing v
+    assert lib.rolesub_rotate_values(ctypes.byref(d), rs.BF16, FAKE, FAKE, FAKE, None) == 1
+    assert "overlaps" in _last()
+    # empty problem is a no-op success
+    d0 = _dims(T=0)
+    assert lib.rolesub_rotate_values(ctypes.byref(d0), rs.BF16, None, None, None, None) == 0
+
+
+def test_route_validation(lib):
+    d = _dims(G=8)
+    bad_k = rs.make_budget(rs.TOPK, (9, 1, 8, 8))
+    assert lib.rolesub_route(ctypes.byref(d), rs.BF16, None, ctypes.byref(bad_k), FAKE, FAKE, FAKE,
+                             None, FAKE, None, None, None, 0, None) == 1
+    assert "k_by_type" in _last()
+    d33 = _dims(G=33)
+    ok = rs.make_budget(rs.TOPK, (4, 6, 8, 8))
+    assert lib.rolesub_route(ctypes.byref(d33), rs.BF16, None, ctypes.byref(ok), FAKE, FAKE, FAKE,
+                             None, FAKE, None, None, None, 0, None) == 2
+    thr = rs.make_budget(rs.THRESHOLD, (0, 0, 0, 0), 0.0, 5, 2)
+    assert lib.rolesub_route(ctypes.byref(d), rs.BF16, None, ctypes.byref(thr), None, None, FAKE,
+                             None, FAKE, None, None, None, 0, None) == 1
+    # router missing and no scores
+    assert lib.rolesub_route(ctypes.byref(d), rs.BF16, None, ctypes.byref(ok), FAKE, FAKE, None,
+                             None, FAKE, None, None, None, 0, None) == 1
+    # workspace too small
+    desc = rs.RouterDesc()
+    desc.kind, desc.C, desc.d_e, desc.Hr = rs.MLP2, 4, 8, 16
+    for n in ("W_r", "b_r", "E", "W1", "b1", "W2", "b2"):
+        setattr(desc, n, 0x1000)
+    need = lib.rolesub_route_workspace_size(ctypes.byref(d), ctypes.byref(desc))
+    assert need > 0
+    assert lib.rolesub_route(ctypes.byref(d), rs.BF16, ctypes.byref(desc), ctypes.byref(ok), FAKE, FAKE,
+                             None, None, FAKE, None, None, FAKE, need - 1, None) == 1
+    assert "workspace" in _last()
+    desc.W2 = None
+    assert lib.rolesub_route(ctypes.byref(d), rs.BF16, ctypes.byref(desc), ctypes.byref(ok), FAKE, FAKE,
+                             None, None, FAKE, None, None, FAKE, need, None) == 1
+
+
+def test_pack_capacity_check(lib):
+    d = _dims(T=10, G=8)
+    bu = rs.make_budget(rs.TOPK, (4, 6, 8, 8))
+    tc = (ctypes.c_int32 * 4)(6, 3, 1, 0)     # need 6*4 + 3*6 + 1*8 = 50
+    assert lib.rolesub_pack_kv(ctypes.byref(d), rs.BF16, ctypes.byref(bu), tc, FAKE, FAKE, FAKE, FAKE,
+                               49, None) == 3
+    assert "budget" in _last()
+    thr = rs.make_budget(rs.THRESHOLD, (0, 0, 0, 0), 0.0, 1, 3)
+    assert lib.rolesub_pack_kv(ctypes.byref(d), rs.BF16, ctypes.byref(thr), tc, FAKE, FAKE, FAKE, FAKE,
+                               29, None) == 3
+    d_bad = _dims(dh=64, G=12)
+    assert lib.rolesub_pack_kv(ctypes.byref(d_bad), rs.BF16, None, None, FAKE, FAKE, FAKE, FAKE, 10, None) == 1
+    assert lib.rolesub_pack_kv(ctypes.byref(d), rs.BF16, None, None, FAKE, FAKE, FAKE, FAKE, -1, None) == 1
+
+
+def test_attend_validation(lib):
+    d = _dims()
+    args = (FAKE, FAKE, FAKE, FAKE, FAKE, 32, FAKE, ctypes.c_float(0.0), FAKE)
+    assert lib.rolesub_attend(ctypes.byref(d), rs.BF16, 4, *args, 7, None, 0, None) == 2   # out dtype
+    assert lib.rolesub_attend(ctypes.byref(d), rs.F32, 4, *args, rs.BF16, None, 0, None) == 2
+    d0 = _dims(T=0)
+    assert lib.rolesub_attend(ctypes.byref(d0), rs.BF16, 4, *args, rs.F32, None, 0, None) == 1
+    assert "T=0" in _last()
+    assert lib.rolesub_attend(ctypes.byref(d), rs.BF16, -1, *args, rs.F32, None, 0, None) == 1
+    nan_args = args[:7] + (ctypes.c_float(float("nan")),) + args[8:]
+    assert lib.rolesub_attend(ctypes.byref(d), rs.BF16, 4, *nan_args, rs.F32, None, 0, None) == 1
+    assert lib.rolesub_attend_workspace_size(ctypes.byref(d), 4) == 0

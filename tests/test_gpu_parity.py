@@ -1,0 +1,359 @@
+"""GPU parity of librolesub against the float64 oracle, through the C ABI.
+
+Bars: integer/index/byte outputs (masks, idx, counts, offsets, packed cache)
+bit-exact; f32 outputs within 1e-4 and bf16 outputs within 2e-2 maximum
+relative error (max |x - ref| / max |ref| over the tensor). The oracle takes
+the same seeded inputs and never sees a GPU result; when routing scores come
+from the GPU router, masks must match on every token whose decisive margin
+exceeds 8x the observed score error (near-margin tokens are reported).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2608_18410_amd as rs
+import synth
+from paper_2608_18410_amd.pipeline import LayerBuffers, pack_capacity, run_layer
+from tests._gpu_util import (DEV, TOL, decisive_margin, host, host_mask, layer_on_device, max_rel, put,
+                             put_mask, put_u8, router_tensors, stack_types, synth_pack_inputs, tdtype)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    rs.load()   # fails loudly if the library is not built
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+# ----------------------------------------------------------------------------
+# Group selection from given scores: bit-exact
+# ----------------------------------------------------------------------------
+
+def _check_selection(scores, types, budget, G, mode, kbt, tau=0.0, kmin=0, kmax=0):
+    B, T = types.shape
+    r = rs.route(put_u8(types), budget, G, scores_in=put(scores, torch.float32))
+    torch.cuda.synchronize()
+    K = O.group_budget(scores, types, mode, kbt, G, tau, kmin, kmax)
+    want = O.select_groups(scores, K)
+    got = host_mask(r["mask"])
+    assert np.array_equal(got, want), f"{int(np.sum(got != want))} masks differ"
+    idx, cnt = O.mask_to_idx(want, G)
+    assert np.array_equal(host(r["count"]), cnt)
+    assert np.array_equal(host(r["idx"]), idx)
+    assert np.array_equal(host(r["scores"]), scores)
+
+
+def test_select_threshold_stress_logits():
+    w = synth.workload(5)
+    B = 4
+    scores = np.stack([synth.sample_scores(w, 0, b) for b in range(B)])
+    types = stack_types(w, B)
+    bu = rs.make_budget(rs.THRESHOLD, (0, 0, 0, 0), 0.0, 1, 32)
+    _say("select: threshold stress, 4 x 2048 tokens, G=32")
+    _check_selection(scores, types, bu, 32, O.THRESHOLD, (0, 0, 0, 0), 0.0, 1, 32)
+
+
+def test_select_topk_ties_zero_signs_nan():
+    r = np.random.default_rng(7)
+    G, B, T = 8, 3, 333
+    grid = np.array([-1.0, -0.5, -0.0, 0.0, 0.5, 1.0, np.nan, np.inf, -np.inf], dtype=np.float32)
+    scores = grid[r.integers(0, len(grid), size=(B, T, G))]
+    scores[1] = r.standard_normal((T, G)).astype(np.float32)
+    types = r.integers(0, 4, size=(B, T)).astype(np.uint8)
+    kbt = (2, 5, 8, 0)
+    _say("select: top-k with ties, signed zeros, NaN, infinities")
+    _check_selection(scores, types, rs.make_budget(rs.TOPK, kbt), G, O.TOPK, kbt)
+
+
+@pytest.mark.parametrize("G,kmin,kmax", [(16, 2, 5), (32, 0, 32), (5, 1, 1)])
+def test_select_threshold_clamps(G, kmin, kmax):
+    r = np.random.default_rng(G)
+    B, T = 2, 517
+    scores = (r.integers(-3, 4, size=(B, T, G)) * 0.25).astype(np.float32)
+    types = np.zeros((B, T), dtype=np.uint8)
+    bu = rs.make_budget(rs.THRESHOLD, (0, 0, 0, 0), 0.0, kmin, kmax)
+    _check_selection(scores, types, bu, G, O.THRESHOLD, (0, 0, 0, 0), 0.0, kmin, kmax)
+
+
+# ----------------------------------------------------------------------------
+# Pack: bit-exact
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cid,B,T,H,dh,G", [
+    (1, 1, 80, 4, 64, 8),        # f32, 32-byte groups
+    (2, 1, 305, 32, 128, 8),     # bf16, 32-byte groups, 7B layer shape
+    (3, 3, 77, 8, 128, 8),       # ragged token count
+    (5, 2, 301, 9, 128, 32),     # bf16, 8-byte groups, heads not a multiple of 8
+    (5, 2, 70, 4, 64, 32),       # bf16, 4-byte groups
+])
+def test_pack_bit_exact(cid, B, T, H, dh, G):
+    w = synth.workload(cid).replace(n_vis=T, n_lang=0, n_prop=0, H=H, dh=dh, G=G)
+    z, m = synth_pack_inputs(w, B)
+    dt = tdtype(w)
+    cap = T * G
+    zd = put(z, dt)
+    Vp = torch.full((B, H, cap, dh // G), 7.0, dtype=dt, device=DEV)
+    off = torch.empty((B, T + 1), dtype=torch.int32, device=DEV)
+    rs.pack_kv(zd, put_mask(m), G, cap, out=(off, Vp))
+    torch.cuda.synchronize()
+    o_ref, Vp_ref = O.pack(z, m, G, cap)
+    assert np.array_equal(host(off), o_ref)
+    got = host(Vp)
+    for b in range(B):
+        n = int(o_ref[b, -1])
+        assert np.array_equal(got[b, :, :n], Vp_ref[b, :, :n])
+        assert np.all(got[b, :, n:] == 7.0)          # slots past the total untouched
+
+
+def test_pack_capacity_clips_writes():
+    w = synth.workload(2).replace(H=8)
+    B, G = 2, 8
+    z, m = synth_pack_inputs(w, B)
+    budget = w.n_vis * w.k_vis + w.n_lang * w.k_lang + w.n_prop * G
+    cap = budget - 50
+    Vp = torch.zeros((B, 8, cap, 16), dtype=torch.bfloat16, device=DEV)
+    off = torch.empty((B, w.T + 1), dtype=torch.int32, device=DEV)
+    rs.pack_kv(put(z, torch.bfloat16), put_mask(m), G, cap, out=(off, Vp))
+    torch.cuda.synchronize()
+    o_ref, Vp_ref = O.pack(z, m, G, cap)
+    assert np.array_equal(host(off), o_ref) and int(o_ref[0, -1]) == budget
+    assert np.array_equal(host(Vp), Vp_ref)
+    with pytest.raises(rs.RolesubError) as e:
+        rs.pack_kv(put(z, torch.bfloat16), put_mask(m), G, cap,
+                   budget=rs.make_budget(rs.TOPK, w.k_by_type), type_counts=w.type_counts())
+    assert e.value.status == 3
+
+
+# ----------------------------------------------------------------------------
+# Rotation
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cid,B,T,H,dh", [(1, 1, 80, 4, 64), (2, 1, 305, 32, 128), (3, 2, 113, 8, 64),
+                                          (3, 3, 1000, 32, 128)])
+def test_rotate(cid, B, T, H, dh):
+    w = synth.workload(cid).replace(B=B, n_vis=T, n_lang=0, n_prop=0, H=H, dh=dh)
+    dt = tdtype(w)
+    R = synth.layer_weights(w, 0)["R"]
+    v = np.stack([synth.sample_activations(w, 0, b, ("v",))["v"] for b in range(B)])
+    z = rs.rotate_values(put(v, dt), put(R, dt))
+    torch.cuda.synchronize()
+    err = max_rel(host(z), O.rotate(v, R))
+    _say(f"rotate {w.dtype} B={B} T={T} H={H} dh={dh}: max rel err {err:.2e}")
+    assert err <= TOL[w.dtype]
+
+
+# ----------------------------------------------------------------------------
+# Attention over the packed cache
+# ----------------------------------------------------------------------------
+
+def _attend_case(w, B, T, Tq, H, dh, G, counts=None, out_dtype=None, seed=0):
+    w = w.replace(B=B, n_vis=T, n_lang=0, n_prop=0, Tq=Tq, H=H, dh=dh, G=G)
+    dt = tdtype(w)
+    acts = [synth.sample_activations(w, seed, b, ("q", "k")) for b in range(B)]
+    q = np.stack([a["q"] for a in acts])
+    k = np.stack([a["k"] for a in acts])
+    z = np.stack([synth.synthetic_z(w, seed, b) for b in range(B)])
+    m = np.stack([synth.synthetic_masks(w, seed, b, counts=counts) for b in range(B)])
+    R = synth.layer_weights(w, seed)["R"]
+    cap = T * G
+    off, Vp = rs.pack_kv(put(z, dt), put_mask(m), G, cap)
+    out = rs.attend(put(q, dt), put(k, dt), put_mask(m), off, Vp, put(R, dt), G, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    o_ref, Vp_ref = O.pack(z, m, G, cap)
+    ref = O.attend_packed(q, k, m, o_ref, Vp_ref, R, G)
+    return host(out), ref, (q, k, z, m, R)
+
+
+@pytest.mark.parametrize("cid,B,T,Tq,H,dh,G", [
+    (1, 1, 80, 8, 4, 64, 8),           # tiny f32 (vector kernel)
+    (2, 1, 305, 56, 32, 128, 8),       # 7B layer shape (matrix cores)
+    (3, 3, 113, 56, 32, 128, 8),
+    (5, 2, 301, 70, 8, 128, 32),       # G=32 (4-dim groups), 2 query blocks, ragged T
+    (3, 2, 97, 20, 8, 64, 8),          # head dim 64 on matrix cores
+    (3, 2, 65, 16, 8, 64, 32),         # 2-dim groups
+    (1, 2, 33, 3, 4, 128, 4),          # f32, head dim 128
+])
+def test_attend(cid, B, T, Tq, H, dh, G):
+    w = synth.workload(cid)
+    counts = np.random.default_rng(T).integers(0, G + 1, size=T)
+    got, ref, _ = _attend_case(w, B, T, Tq, H, dh, G, counts=counts)
+    err = max_rel(got, ref)
+    _say(f"attend {w.dtype} B={B} T={T} Tq={Tq} H={H} dh={dh} G={G}: max rel err {err:.2e}")
+    assert err <= TOL[w.dtype]
+
+
+def test_attend_f32_output_from_bf16():
+    w = synth.workload(2)
+    got, ref, _ = _attend_case(w, 2, 150, 56, 16, 128, 8, out_dtype=torch.float32)
+    err = max_rel(got, ref)
+    _say(f"attend bf16 in, f32 out: max rel err {err:.2e}")
+    assert err <= 2e-2
+
+
+def test_attend_no_groups_is_zero_and_all_groups_is_standard_attention():
+    w = synth.workload(2)
+    T, G = 90, 8
+    got0, _, _ = _attend_case(w, 1, T, 56, 8, 128, G, counts=np.zeros(T, dtype=int))
+    assert np.all(got0 == 0.0)
+    got, _, (q, k, z, m, R) = _attend_case(w, 1, T, 56, 8, 128, G, counts=np.full(T, G))
+    v = O.back_rotate(z, R)        # the values whose rotation is z
+    s = np.einsum("bqhd,bthd->bhqt", q, k) / np.sqrt(128)
+    ref = np.einsum("bhqt,bthd->bqhd", O.softmax(s, -1), v)
+    err = max_rel(got, ref)
+    _say(f"attend all groups vs standard attention: max rel err {err:.2e}")
+    assert err <= 2e-2
+
+
+# ----------------------------------------------------------------------------
+# Router end to end (scores from h)
+# ----------------------------------------------------------------------------
+
+def _route_check(w, h, types, router, wt_or_scores_fn, label):
+    dt = tdtype(w)
+    budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
+    r = rs.route(put_u8(types), budget, w.G, h=put(h, dt), router=router)
+    torch.cuda.synchronize()
+    ref_scores = wt_or_scores_fn(h, types)
+    got_scores = host(r["scores"])
+    serr = max_rel(got_scores, ref_scores)
+    abs_err = float(np.max(np.abs(got_scores - ref_scores)))
+    K = O.group_budget(ref_scores, types, w.mode, w.k_by_type, w.G, w.tau, w.kmin, w.kmax)
+    want = O.select_groups(ref_scores, K)
+    got = host_mask(r["mask"])
+    margin = decisive_margin(ref_scores, K, w.tau if w.mode == O.THRESHOLD else None)
+    safe = margin > 8 * abs_err
+    n_near = int(np.sum(~safe))
+    _say(f"route {label}: score max rel err {serr:.2e} (abs {abs_err:.1e}); "
+         f"{n_near} near-margin tokens of {safe.size}; mismatches on safe tokens "
+         f"{int(np.sum((got != want) & safe))}")
+    assert serr <= 1e-4
+    assert np.array_equal(got[safe], want[safe])
+    assert np.array_equal(host(r["count"])[safe], O.popcount(want)[safe])
+    return r
+
+
+@pytest.mark.parametrize("cid,B", [(1, 1), (2, 1), (3, 16), (5, 2)])
+def test_route_mlp2(cid, B):
+    w = synth.workload(cid).replace(B=B)
+    wt = synth.layer_weights(w, 0)
+    h = np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(B)])
+    types = stack_types(w, B)
+    ref = lambda hh, tt: O.router_mlp2(hh, tt, wt["W_r"], wt["b_r"], wt["E"], wt["W1"], wt["b1"],
+                                       wt["W2"], wt["b2"])
+    _route_check(w, h, types, router_tensors(wt, tdtype(w)), ref, f"mlp2 workload {cid} B={B}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_route_additive(dtype):
+    w = synth.workload(2).replace(B=2, dtype=dtype, d=512, G=16, C=6, n_vis=40, n_lang=9, n_prop=1,
+                                  k_vis=3, k_lang=5, k_prop=16)
+    aw = synth.additive_weights(w, 0)
+    dt = tdtype(w)
+    router = rs.Router.additive(*(put(aw[n], dt) for n in ("W_tok", "b_tok", "W_r", "b_r", "W_role",
+                                                          "W_lang", "b_lang")))
+    h = np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(2)])
+    types = stack_types(w, 2)
+    ref = lambda hh, tt: O.router_additive(hh, tt, aw["W_tok"], aw["b_tok"], aw["W_r"], aw["b_r"],
+                                           aw["W_role"], aw["W_lang"], aw["b_lang"], 0.1, 0.1)
+    _route_check(w, h, types, router, ref, f"additive {dtype}")
+
+
+def test_route_sample_without_language_tokens():
+    w = synth.workload(3).replace(B=2)
+    wt = synth.layer_weights(w, 0)
+    h = np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(2)])
+    types = stack_types(w, 2)
+    types[1][types[1] == O.LANG] = O.VIS       # sample 1 has no language token: pool is zero
+    ref = lambda hh, tt: O.router_mlp2(hh, tt, wt["W_r"], wt["b_r"], wt["E"], wt["W1"], wt["b1"],
+                                       wt["W2"], wt["b2"])
+    _route_check(w, h, types, router_tensors(wt, torch.bfloat16), ref, "no-language sample")
+
+
+# ----------------------------------------------------------------------------
+# Whole path: route -> rotate -> pack -> attend
+# ----------------------------------------------------------------------------
+
+def _run_gpu_layer(w, layer, acts_dev, types_np, scores_in=None):
+    dt = tdtype(w)
+    wt = synth.layer_weights(w, layer)
+    router = router_tensors(wt, dt)
+    budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
+    cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
+    ws = rs.route_workspace_size(w.B, w.T, w.G, w.d, router)
+    bufs = LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, dt, ws_bytes=ws, device=DEV)
+    run_layer(acts_dev.get("h"), acts_dev["q"], acts_dev["k"], acts_dev["v"], put_u8(types_np),
+              put(wt["R"], dt), budget, w.G, bufs, router=router if scores_in is None else None,
+              scores_in=scores_in, type_counts=w.type_counts())
+    torch.cuda.synchronize()
+    return bufs, wt, cap
+
+
+def _check_sample(w, layer, b, bufs, wt, cap, scores=None):
+    a = synth.sample_activations(w, layer, b)
+    h, q, k, v = (a[n][None] for n in ("h", "q", "k", "v"))
+    if scores is None:
+        ref_scores = O.router_mlp2(h, w.types(), wt["W_r"], wt["b_r"], wt["E"], wt["W1"], wt["b1"],
+                                   wt["W2"], wt["b2"])
+    else:
+        ref_scores = scores[None]
+    ref = O.pipeline(h, q, k, v, w.types(), wt, w.mode, w.k_by_type, w.G, w.tau, w.kmin, w.kmax,
+                     scores=ref_scores, cap=cap)
+    got_mask = host_mask(bufs.mask[b:b + 1])
+    got_scores = host(bufs.scores[b:b + 1])
+    abs_err = float(np.max(np.abs(got_scores - ref_scores)))
+    margin = decisive_margin(ref_scores, ref["K"], w.tau if w.mode == O.THRESHOLD else None)
+    safe = margin > 8 * abs_err if scores is None else np.ones_like(margin, dtype=bool)
+    assert np.array_equal(got_mask[safe], ref["mask"][safe])
+    flips = int(np.sum(got_mask != ref["mask"]))
+    z_err = max_rel(host(bufs.z[b:b + 1]), ref["z"])
+    out_err = max_rel(host(bufs.out[b:b + 1]), ref["out"])
+    _say(f"  layer {layer} sample {b}: mask flips {flips} (near-margin {int(np.sum(~safe))}), "
+         f"z err {z_err:.2e}, out err {out_err:.2e}")
+    if flips == 0:
+        assert np.array_equal(host(bufs.offsets[b:b + 1]), ref["offsets"])
+    assert z_err <= TOL[w.dtype] and out_err <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3])
+def test_pipeline_small_workloads(cid):
+    w = synth.workload(cid)
+    _say(f"pipeline workload {cid} ({w.name})")
+    acts = layer_on_device(w, 0)
+    bufs, wt, cap = _run_gpu_layer(w, 0, acts, stack_types(w))
+    for b in range(w.B):
+        _check_sample(w, 0, b, bufs, wt, cap)
+
+
+@pytest.mark.parametrize("layer", [0, 31])
+def test_pipeline_stack_full_batch_sampled(layer):
+    """The 32-layer, batch-64 workload at full size; the oracle checks sampled prefixes."""
+    w = synth.workload(4)
+    _say(f"pipeline workload 4 layer {layer}, B={w.B}")
+    acts = layer_on_device(w, layer)
+    bufs, wt, cap = _run_gpu_layer(w, layer, acts, stack_types(w))
+    for b in (0, 17, 63):
+        _check_sample(w, layer, b, bufs, wt, cap)
+    cnt = host(bufs.count)
+    assert np.all(cnt[:, :w.n_vis] == w.k_vis) and np.all(cnt[:, w.n_vis:w.n_vis + w.n_lang] == w.k_lang)
+    assert np.all(host(bufs.offsets)[:, -1] == cap)
+
+
+def test_pipeline_stress_full_batch_sampled():
+    """G=32 threshold workload at full size (B=128, T=2048); sampled oracle checks."""
+    w = synth.workload(5)
+    _say(f"pipeline workload 5, B={w.B}, T={w.T}")
+    acts = layer_on_device(w, 0, need_h=False)
+    scores = np.stack([synth.sample_scores(w, 0, b) for b in range(w.B)])
+    bufs, wt, cap = _run_gpu_layer(w, 0, acts, stack_types(w), scores_in=put(scores, torch.float32))
+    for b in (0, 77, 127):
+        _check_sample(w, 0, b, bufs, wt, cap, scores=scores[b])
+    K = O.group_budget(scores, stack_types(w), O.THRESHOLD, w.k_by_type, w.G, 0.0, 1, 32)
+    assert np.array_equal(host(bufs.count).astype(np.int64), K)
+    assert np.array_equal(host(bufs.offsets)[:, -1], K.sum(axis=1))
