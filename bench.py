@@ -1,0 +1,259 @@
+"""Benchmark of the RoleSub hot path on one MI355X.
+
+A step is one pass of the whole hot path (route -> rotate -> pack -> attend)
+over one batch: by default the 32-layer compressed-attention stack at the
+OpenVLA-OFT-7B shape (hidden 4096, 32 heads x 128), 64 prefixes of 177 KV
+tokens (128 retained visual + 48 language + 1 proprio), 56 action queries,
+8 groups of 16 dims, keeping 4/8 visual and 6/8 language groups; every layer
+has its own rotations, router weights and activations, all resident in HBM
+before timing starts. Each layer's four calls are captured once in HIP graphs
+and replayed (the kernels are the same as the eager calls).
+
+Prints ONE JSON line. `value` counts query tokens per second per layer call,
+B * Tq * L / step time. `roofline` is measured live for the attention kernel
+with HIP events over the timed region; `cpu_baseline` times the float64
+oracle on a bounded sample on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "compressed-KV attention query-tokens/sec at 7B shape; achieved HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_hbm_traffic.json")
+
+
+def attend_bytes(w, sum_k: int, out_esize: int) -> int:
+    """Algorithmic HBM bytes of one attention call: q, k, packed values,
+    mask + offsets, output, rotations (everything read or written once)."""
+    e = 2 if w.dtype == "bf16" else 4
+    per = (w.Tq * w.H * w.dh * e + w.T * w.H * w.dh * e + sum_k * w.ds * w.H * e + 8 * w.T
+           + w.Tq * w.H * w.dh * out_esize)
+    return w.B * per + w.H * w.dh * w.dh * e
+
+
+def stage_bytes(w, sum_k: int) -> dict:
+    e = 2 if w.dtype == "bf16" else 4
+    route_w = (w.Hr * w.router_in + w.C * w.d + w.G * w.Hr + w.C * w.d_e) * e
+    return {
+        "route": w.B * w.T * w.d * e + route_w + 4 * w.B * w.T * (w.G + 2),
+        "rotate": 2 * w.B * w.T * w.H * w.dh * e + w.H * w.dh * w.dh * e,
+        "pack": 2 * w.B * sum_k * w.ds * w.H * e + 8 * w.B * w.T,
+        "attend": attend_bytes(w, sum_k, e),
+    }
+
+
+def _source_hash() -> str:
+    p = os.path.join(ROOT, "paper_2608_18410_amd", "csrc", "k_attend.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def _traffic(launches_bytes_hint):
+    """HBM traffic per attention launch from committed rocprofv3 counter runs,
+    or None when absent or taken on a different kernel source."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("k_attend_sha256_16") != _source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(w, budget_s: float = 12.0) -> dict:
+    """The float64 oracle (test infrastructure) on whole prefixes of layer 0."""
+    import oracle as O
+    import synth
+    from threadpoolctl import threadpool_info
+
+    wt = synth.layer_weights(w, 0)
+    cap = sum(n * min(k, w.G) for n, k in zip(w.type_counts(), w.k_by_type))
+    done, spent = 0, 0.0
+    while spent < budget_s and done < w.B:
+        a = synth.sample_activations(w, 0, done)
+        t0 = time.perf_counter()
+        O.pipeline(a["h"][None], a["q"][None], a["k"][None], a["v"][None], w.types(), wt, w.mode,
+                   w.k_by_type, w.G, w.tau, w.kmin, w.kmax, cap=cap)
+        spent += time.perf_counter() - t0
+        done += 1
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": done * w.Tq / spent, "unit": "query-tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"layer 0, prefixes 0..{done - 1} of {w.B}: route->rotate->pack->attend in float64 "
+                      f"({spent:.1f} s); BLAS pool {threads} threads, Python loops on one core"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=4, help="workload id (4: 32-layer 7B stack)")
+    ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: workload's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="issue the calls directly, no HIP graphs")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the path shards by prefix or head with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_18410_amd as rs
+    import synth
+    from paper_2608_18410_amd.pipeline import LayerBuffers, pack_capacity, run_layer
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    rs.load()
+    dev = torch.device("cuda:0")
+    w = synth.workload(args.workload)
+    if args.layers:
+        w = w.replace(L=args.layers)
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
+    cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
+    types = torch.from_numpy(np.broadcast_to(w.types(), (w.B, w.T)).copy()).to(dev)
+
+    # ---- inputs resident in HBM
+    t_gen = time.time()
+    layers = []
+    for l in range(w.L):
+        wt = synth.layer_weights(w, l)
+        put = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+        router = rs.Router.mlp2(*(put(wt[n]) for n in ("W_r", "b_r", "E", "W1", "b1", "W2", "b2")))
+        names = ("q", "k", "v") if w.scores_in else ("h", "q", "k", "v")
+        acts = {n: torch.empty(s, dtype=dt, device=dev) for n, s in
+                (("h", (w.B, w.T, w.d)), ("q", (w.B, w.Tq, w.H, w.dh)), ("k", (w.B, w.T, w.H, w.dh)),
+                 ("v", (w.B, w.T, w.H, w.dh))) if n in names}
+        import concurrent.futures as cf
+        with cf.ThreadPoolExecutor(16) as ex:
+            for b0 in range(0, w.B, 16):
+                parts = list(ex.map(lambda b: synth.sample_activations(w, l, b, names),
+                                    range(b0, min(w.B, b0 + 16))))
+                for i, p in enumerate(parts):
+                    for n in names:
+                        acts[n][b0 + i].copy_(torch.from_numpy(p[n]))
+        scores = None
+        if w.scores_in:
+            scores = torch.from_numpy(np.stack([synth.sample_scores(w, l, b) for b in range(w.B)])).to(dev)
+        ws = rs.route_workspace_size(w.B, w.T, w.G, w.d, router)
+        bufs = LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, dt, ws_bytes=ws, device=dev)
+        layers.append(dict(acts=acts, router=router if scores is None else None, scores=scores,
+                           R=put(wt["R"]), bufs=bufs))
+        print(f"# layer {l} inputs resident ({time.time() - t_gen:.1f} s)", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+
+    def pre(L):
+        a, bf = L["acts"], L["bufs"]
+        rs.route(types, budget, w.G, h=a.get("h"), router=L["router"], scores_in=L["scores"],
+                 workspace=bf.workspace,
+                 out={"mask": bf.mask, "idx": bf.idx, "count": bf.count, "scores": bf.scores})
+        rs.rotate_values(a["v"], L["R"], out=bf.z)
+        rs.pack_kv(bf.z, bf.mask, w.G, cap, out=(bf.offsets, bf.Vp))
+
+    def att(L):
+        a, bf = L["acts"], L["bufs"]
+        rs.attend(a["q"], a["k"], bf.mask, bf.offsets, bf.Vp, L["R"], w.G, out=bf.out)
+
+    # ---- one eager pass (also the reference for the graph replays)
+    for L in layers:
+        pre(L)
+        att(L)
+    torch.cuda.synchronize()
+    eager_out = layers[-1]["bufs"].out.clone()
+
+    if not args.eager:
+        stream = torch.cuda.Stream()
+        for L in layers:
+            g1, g2 = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g1, stream=stream):
+                pre(L)
+            with torch.cuda.graph(g2, stream=stream):
+                att(L)
+            L["g_pre"], L["g_att"] = g1, g2
+        run_pre = lambda L: L["g_pre"].replay()
+        run_att = lambda L: L["g_att"].replay()
+    else:
+        run_pre, run_att = pre, att
+
+    def step(ev=None):
+        for i, L in enumerate(layers):
+            run_pre(L)
+            if ev is not None:
+                ev[i][0].record()
+            run_att(L)
+            if ev is not None:
+                ev[i][1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if not torch.equal(layers[-1]["bufs"].out, eager_out):
+        raise RuntimeError("graph replay output differs from the eager pass")
+
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in layers] for _ in range(args.steps)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for s in range(args.steps):
+        step(ev[s])
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    att_ms = float(np.mean([a.elapsed_time(b) for e in ev for (a, b) in e]))
+
+    sum_k = int(layers[0]["bufs"].offsets[:, -1].sum().item()) // w.B
+    per_stage = stage_bytes(w, sum_k)
+    a_bytes = per_stage["attend"]
+    achieved = a_bytes / (att_ms * 1e-3) / 1e9
+    value = w.B * w.Tq * w.L / (ms_step * 1e-3)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "query-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded Gaussian activations/weights, Haar rotations; no trained weights)",
+        "config": {"workload": w.name, "layers": w.L, "prefixes": w.B, "kv_tokens": w.T,
+                   "visual": w.n_vis, "language": w.n_lang, "proprio": w.n_prop, "queries": w.Tq,
+                   "heads": w.H, "head_dim": w.dh, "hidden": w.d, "groups": w.G,
+                   "keep": {"vis": w.k_vis, "lang": w.k_lang, "prop": w.k_prop}
+                   if w.mode == 0 else {"threshold": w.tau, "kmin": w.kmin, "kmax": w.kmax},
+                   "value_counts": "query tokens x layers per second (B*Tq*L / step time)",
+                   "graphs": not args.eager},
+        "roofline": {"kernel": "rolesub_attend (k_attend_bf16)", "bound": "hbm",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": _traffic(a_bytes),
+                     "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": att_ms * 1e3},
+        "detail": {"attend_query_tokens_per_s": w.B * w.Tq / (att_ms * 1e-3),
+                   "layers_per_s": w.L / (ms_step * 1e-3),
+                   "stage_algorithmic_bytes": per_stage,
+                   "step_algorithmic_GBs": w.L * sum(per_stage.values()) / (ms_step * 1e-3) / 1e9},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

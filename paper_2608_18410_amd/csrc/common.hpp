@@ -35,6 +35,31 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
          (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
 }
 
+// Raw buffer loads. A load whose byte offset is at or past the resource's
+// size returns zeros without touching memory, so masked or out-of-range
+// elements need no branch around the load (a branch would force a wait for
+// every outstanding load at its join). Resources must cover < 2 GiB so that
+// kOOB is always out of range.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9 family: 32-bit data format, untyped access
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), kRsrcWord3);
+}
+__device__ __forceinline__ u32x4 bload16(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0));
+}
+__device__ __forceinline__ u32x2 bload8(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(off), 0, 0));
+}
+__device__ __forceinline__ uint32_t bload4(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, static_cast<int>(off), 0, 0);
+}
+__device__ __forceinline__ uint32_t clamp_bytes(size_t n) {
+  return n < kOOB ? static_cast<uint32_t>(n) : kOOB;
+}
+
 // Group-selection order (top-K_i, Sec. 3.4): a larger score ranks first,
 // -0 and +0 are equal, NaN ranks after every number, equal keys go to the
 // lower group index.

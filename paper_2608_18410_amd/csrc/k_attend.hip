@@ -17,39 +17,52 @@ __device__ __forceinline__ uint32_t group_mask(int G) { return G >= 32 ? 0xFFFFF
 
 // ---------------------------------------------------------------------------
 // bf16 matrix-core kernel. One workgroup = one (sample, head) and up to 64
-// queries; wave w owns queries 16w..16w+15. KV tokens stream in tiles of 32:
-//   * K tile (32 x DH) -> LDS, shared by the four waves;
+// queries; wave w owns queries 16w..16w+15. KV tokens stream in tiles of 64:
+//   * K tile (64 x DH) -> LDS, shared by the four waves;
 //   * the tile's packed groups -> a zero-filled, transposed LDS tile
 //     Zt[dim][token] (token pairs packed in one dword);
 //   * S^T = K Q^T on MFMA (queries are the B operand held in registers), so
-//     each lane owns one query column and 8 token rows;
-//   * online softmax per query: 8 values in-lane, then 2 cross-lane steps;
+//     each lane owns one query column and 16 token rows;
+//   * online softmax per query: 16 values in-lane, then 2 cross-lane steps;
 //   * O^T += Z~^T P^T on MFMA. The lane's own softmax values form the P^T
 //     fragment directly once the A fragment lists its tokens in the same
-//     order (tokens 4q..4q+3 and 16+4q..16+4q+3 of the tile).
+//     order (tokens 4q..4q+3 and 16+4q..16+4q+3 of each 32-token half).
+// Loads are software-pipelined: while tile i is computed from LDS, the K rows
+// and packed groups of tile i+1 are in flight into registers, and the group
+// masks and cache offsets of tile i+2 (which address tile i+2's packed groups)
+// are in flight too.
 // After the last tile, O^T = R_h U^T (one more MFMA chain, U in bf16) and
 // each lane stores 4 consecutive outputs of its query.
-template <int DH>
+// VM: how the 8-dim chunks of the value tile map to packed groups:
+//   kWide  groups of >= 8 dims (one 16-byte load per token and chunk)
+//   kDs4   4-dim groups (two 8-byte loads), kDs2  2-dim groups (four 4-byte loads)
+constexpr int kWide = 0, kDs4 = 1, kDs2 = 2;
+
+template <int DH, int VM>
 __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
-  constexpr int TK = 32, MT = DH / 16, KS = DH / 32, KLD = DH + 8, ZLD = TK / 2 + 2;
+  constexpr int TK = 64, MT = DH / 16, KS = DH / 32, KLD = DH + 8, ZLD = TK / 2 + 4;
+  constexpr int NKP = TK * DH / 8 / 256;          // 16-byte K pieces per thread per tile
+  constexpr int NVI = (TK / 2) * (DH / 8) / 256;  // (token pair, 8-dim chunk) items per thread
   __shared__ __attribute__((aligned(16))) bf16 Ks[TK * KLD];
   __shared__ __attribute__((aligned(16))) uint32_t Zt[DH * ZLD];
+  __shared__ uint32_t s_mask[2][TK];
+  __shared__ int32_t s_off[2][TK];
   int h, b;
   xcd_split(blockIdx.x, p.H, h, b);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
   const int T = p.T, H = p.H, G = p.G, ds = DH / G;
   const uint32_t gm = group_mask(G);
-  const bf16* q = static_cast<const bf16*>(p.q);
-  const bf16* k = static_cast<const bf16*>(p.k);
   const int qq = blockIdx.y * 64 + 16 * w + l16;
   const bool qvalid = qq < p.Tq;
-  const bf16x8 zero8 = {};
 
   bf16x8 qf[KS];
   {
-    const bf16* qr = q + ((static_cast<size_t>(b) * p.Tq + (qvalid ? qq : 0)) * H + h) * DH + 8 * g4;
+    const rsrc_t r_q = make_rsrc(static_cast<const bf16*>(p.q) + (static_cast<size_t>(b) * p.Tq * H + h) * DH,
+                                 clamp_bytes((static_cast<size_t>(p.Tq - 1) * H + 1) * DH * 2));
+    const uint32_t qo = static_cast<uint32_t>(qq) * H * DH * 2 + 16u * g4;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = qvalid ? *reinterpret_cast<const bf16x8*>(qr + 32 * ks) : zero8;
+    for (int ks = 0; ks < KS; ++ks)
+      qf[ks] = __builtin_bit_cast(bf16x8, bload16(r_q, qvalid ? qo + 64u * ks : kOOB));
   }
   f32x4 acc[MT];
 #pragma unroll
@@ -57,82 +70,120 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
   float m_run = -INFINITY, l_run = 0.f;
   const float sl2 = p.scale * 1.4426950408889634f;  // softmax in base 2
 
-  const int pp = tid & 15, cc = tid >> 4;  // Zt fill: token pair, 8-dim chunk
-  const int32_t* ob = p.offsets + static_cast<size_t>(b) * (T + 1);
-  const uint32_t* mb = p.mask + static_cast<size_t>(b) * T;
-  const bf16* Vh = static_cast<const bf16*>(p.Vp) + (static_cast<size_t>(b) * H + h) * p.cap * ds;
-  const bf16* kb = k + (static_cast<size_t>(b) * T * H + h) * DH;
+  // Buffer resources: a masked or out-of-range element loads as zero with no
+  // memory access, so every load below is unconditional.
+  const rsrc_t r_off = make_rsrc(p.offsets + static_cast<size_t>(b) * (T + 1), (T + 1) * 4u);
+  const rsrc_t r_mask = make_rsrc(p.mask + static_cast<size_t>(b) * T, T * 4u);
+  const rsrc_t r_v = make_rsrc(static_cast<const bf16*>(p.Vp) + (static_cast<size_t>(b) * H + h) * p.cap * ds,
+                               clamp_bytes(static_cast<size_t>(p.cap) * ds * 2));
+  const uint32_t kstride = static_cast<uint32_t>(H) * DH * 2;  // bytes between tokens
+  const rsrc_t r_k = make_rsrc(static_cast<const bf16*>(p.k) + (static_cast<size_t>(b) * T * H + h) * DH,
+                               clamp_bytes(static_cast<size_t>(T - 1) * kstride + DH * 2));
 
-  for (int t0 = 0; t0 < T; t0 += TK) {
-    // ---- K tile
+  // mask/offset of token t0+tid of a tile (threads 0..TK-1)
+  auto load_meta = [&](int t0, uint32_t& m, int32_t& o) {
+    const int t = t0 + tid;
+    const bool ok = tid < TK && t < T;
+    m = bload4(r_mask, ok ? 4u * t : kOOB);  // masked to G bits when stored (no wait here)
+    o = static_cast<int32_t>(bload4(r_off, ok ? 4u * t : kOOB));
+  };
+  u32x4 kreg[NKP];
+  auto load_k = [&](int t0) {
 #pragma unroll
-    for (int r = 0; r < TK * DH / 8 / 256; ++r) {
+    for (int r = 0; r < NKP; ++r) {
       const int pc = tid + 256 * r;
       const int row = pc / (DH / 8), c8 = pc % (DH / 8);
       const int t = t0 + row;
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (t < T) val = *reinterpret_cast<const u32x4*>(kb + static_cast<size_t>(t) * H * DH + 8 * c8);
-      *reinterpret_cast<u32x4*>(Ks + row * KLD + 8 * c8) = val;
+      kreg[r] = bload16(r_k, t < T ? t * kstride + 16u * c8 : kOOB);
     }
-    // ---- routed value tile, transposed, dropped groups = 0
-    if (cc < DH / 8) {
-      uint32_t ev[2][4];
+  };
+  // packed groups of 2 tokens x 8 dims for each item, addressed through the LDS masks/offsets
+  u32x4 vreg[NVI][2];
+  const int64_t cap = p.cap;
+  auto slot_off = [&](uint32_t m, int o, int g, bool tok_ok, int elem) -> uint32_t {
+    const int64_t sl = o + __popc(m & ((1u << g) - 1u));
+    const bool ok = tok_ok && ((m >> g) & 1u) && sl < cap;
+    return ok ? static_cast<uint32_t>((sl * ds + elem) * 2) : kOOB;
+  };
+  auto load_v = [&](int t0, int slot) {
+#pragma unroll
+    for (int r = 0; r < NVI; ++r) {
+      const int it = tid + 256 * r;
+      const int pp = it % (TK / 2), cc = it / (TK / 2);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        ev[e][0] = ev[e][1] = ev[e][2] = ev[e][3] = 0u;
-        const int t = t0 + 2 * pp + e;
-        if (t < T) {
-          const uint32_t m = mb[t] & gm;
-          const int o = ob[t];
-          if (ds >= 8) {
-            const int g = (8 * cc) / ds;
-            if ((m >> g) & 1u) {
-              const int64_t slot = o + __popc(m & ((1u << g) - 1u));
-              if (slot < p.cap) {
-                const u32x4 val = *reinterpret_cast<const u32x4*>(Vh + slot * ds + (8 * cc - g * ds));
-                ev[e][0] = val[0]; ev[e][1] = val[1]; ev[e][2] = val[2]; ev[e][3] = val[3];
-              }
-            }
-          } else if (ds == 4) {
-            // the 8-dim chunk spans two groups of 4
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              const int g = 2 * cc + u;
-              if ((m >> g) & 1u) {
-                const int64_t slot = o + __popc(m & ((1u << g) - 1u));
-                if (slot < p.cap) {
-                  const u32x2 val = *reinterpret_cast<const u32x2*>(Vh + slot * 4);
-                  ev[e][2 * u] = val[0];
-                  ev[e][2 * u + 1] = val[1];
-                }
-              }
-            }
-          } else {
-            // ds == 2: the chunk spans four groups of 2
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const int g = 4 * cc + u;
-              if ((m >> g) & 1u) {
-                const int64_t slot = o + __popc(m & ((1u << g) - 1u));
-                if (slot < p.cap) ev[e][u] = *reinterpret_cast<const uint32_t*>(Vh + slot * 2);
-              }
-            }
-          }
+        const int tl = 2 * pp + e;
+        const bool tok_ok = t0 + tl < T;
+        const uint32_t m = s_mask[slot][tl];
+        const int o = s_off[slot][tl];
+        if constexpr (VM == kWide) {
+          const int g = (8 * cc) / ds;
+          vreg[r][e] = bload16(r_v, slot_off(m, o, g, tok_ok, 8 * cc - g * ds));
+        } else if constexpr (VM == kDs4) {
+          const u32x2 x0 = bload8(r_v, slot_off(m, o, 2 * cc, tok_ok, 0));
+          const u32x2 x1 = bload8(r_v, slot_off(m, o, 2 * cc + 1, tok_ok, 0));
+          vreg[r][e] = u32x4{x0[0], x0[1], x1[0], x1[1]};
+        } else {
+          vreg[r][e] = u32x4{bload4(r_v, slot_off(m, o, 4 * cc, tok_ok, 0)),
+                             bload4(r_v, slot_off(m, o, 4 * cc + 1, tok_ok, 0)),
+                             bload4(r_v, slot_off(m, o, 4 * cc + 2, tok_ok, 0)),
+                             bload4(r_v, slot_off(m, o, 4 * cc + 3, tok_ok, 0))};
         }
       }
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int r = 0; r < NKP; ++r) {
+      const int pc = tid + 256 * r;
+      const int row = pc / (DH / 8), c8 = pc % (DH / 8);
+      *reinterpret_cast<u32x4*>(Ks + row * KLD + 8 * c8) = kreg[r];
+    }
+#pragma unroll
+    for (int r = 0; r < NVI; ++r) {
+      const int it = tid + 256 * r;
+      const int pp = it % (TK / 2), cc = it / (TK / 2);
       uint32_t* zc = Zt + 8 * cc * ZLD + pp;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        zc[(2 * j) * ZLD] = (ev[0][j] & 0xFFFFu) | (ev[1][j] << 16);
-        zc[(2 * j + 1) * ZLD] = (ev[0][j] >> 16) | (ev[1][j] & 0xFFFF0000u);
+        zc[(2 * j) * ZLD] = (vreg[r][0][j] & 0xFFFFu) | (vreg[r][1][j] << 16);
+        zc[(2 * j + 1) * ZLD] = (vreg[r][0][j] >> 16) | (vreg[r][1][j] & 0xFFFF0000u);
       }
     }
+  };
+
+  // ---- prologue: metadata of tiles 0 and 1, operands of tile 0
+  uint32_t mreg;
+  int32_t oreg;
+  load_meta(0, mreg, oreg);
+  if (tid < TK) {
+    s_mask[0][tid] = mreg & gm;
+    s_off[0][tid] = oreg;
+  }
+  load_meta(TK, mreg, oreg);
+  __syncthreads();
+  load_k(0);
+  load_v(0, 0);
+
+  int it = 0;
+  for (int t0 = 0; t0 < T; t0 += TK, ++it) {
+    const int nslot = (it + 1) & 1;
+    store_tile();
+    if (tid < TK) {
+      s_mask[nslot][tid] = mreg & gm;
+      s_off[nslot][tid] = oreg;
+    }
     __syncthreads();
+    if (t0 + TK < T) {
+      load_k(t0 + TK);
+      load_v(t0 + TK, nslot);
+      load_meta(t0 + 2 * TK, mreg, oreg);
+    }
 
     // ---- S^T = K Q^T (rows: tile tokens 16*m2 + 4*g4 + i; column: this lane's query)
-    f32x4 s[2];
+    f32x4 s[4];
 #pragma unroll
-    for (int m2 = 0; m2 < 2; ++m2) {
+    for (int m2 = 0; m2 < 4; ++m2) {
       s[m2] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -143,7 +194,7 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
     // ---- online softmax (base 2)
     float mx = -INFINITY;
 #pragma unroll
-    for (int m2 = 0; m2 < 2; ++m2)
+    for (int m2 = 0; m2 < 4; ++m2)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int t = t0 + 16 * m2 + 4 * g4 + i;
@@ -156,25 +207,30 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
     const float m_new = fmaxf(m_run, mx);
     const float alpha = exp2f(m_run - m_new);
     float psum = 0.f;
-    bf16x8 pb;
+    bf16x8 pb[2];
 #pragma unroll
-    for (int m2 = 0; m2 < 2; ++m2)
+    for (int m2 = 0; m2 < 4; ++m2)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float pr = exp2f(s[m2][i] - m_new);
         psum += pr;
-        pb[4 * m2 + i] = static_cast<bf16>(pr);
+        pb[m2 >> 1][4 * (m2 & 1) + i] = static_cast<bf16>(pr);
       }
     l_run = l_run * alpha + psum;
     m_run = m_new;
-    // ---- O^T += Z~^T P^T
+    // ---- O^T += Z~^T P^T, two 32-token halves
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-      const uint32_t* zr = Zt + (16 * m + l16) * ZLD;
-      const u32x2 lo = *reinterpret_cast<const u32x2*>(zr + 2 * g4);
-      const u32x2 hi = *reinterpret_cast<const u32x2*>(zr + 8 + 2 * g4);
-      const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
-      acc[m] = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), pb, acc[m] * alpha);
+      const uint32_t* zr = Zt + (16 * m + l16) * ZLD + 2 * g4;
+      f32x4 a = acc[m] * alpha;
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(zr + 16 * hf);
+        const u32x2 hi = *reinterpret_cast<const u32x2*>(zr + 16 * hf + 8);
+        const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
+        a = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), pb[hf], a);
+      }
+      acc[m] = a;
     }
     __syncthreads();
   }
@@ -193,15 +249,21 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
     }
   const bf16* Rh = static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH;
   const size_t obase = ((static_cast<size_t>(b) * p.Tq + (qvalid ? qq : 0)) * H + h) * DH + 4 * g4;
+  u32x2 ra[MT][KS][2];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16* rr = Rh + (16 * m + l16) * DH + 4 * g4 + 32 * ks;
+      ra[m][ks][0] = *reinterpret_cast<const u32x2*>(rr);
+      ra[m][ks][1] = *reinterpret_cast<const u32x2*>(rr + 16);
+    }
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    const bf16* rr = Rh + (16 * m + l16) * DH + 4 * g4;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const u32x2 lo = *reinterpret_cast<const u32x2*>(rr + 32 * ks);
-      const u32x2 hi = *reinterpret_cast<const u32x2*>(rr + 32 * ks + 16);
-      const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
+      const u32x4 av = {ra[m][ks][0][0], ra[m][ks][0][1], ra[m][ks][1][0], ra[m][ks][1][1]};
       o = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), ub[ks], o);
     }
     if (qvalid) {
@@ -280,10 +342,13 @@ hipError_t launch_attend(const AttendParams& p, bool bf16, hipStream_t s) {
   if (p.B == 0 || p.Tq == 0 || p.H == 0) return hipSuccess;
   if (bf16 && (p.dh == 128 || p.dh == 64)) {
     const dim3 grid(static_cast<unsigned>(p.B * p.H), static_cast<unsigned>((p.Tq + 63) / 64));
-    if (p.dh == 128)
-      hipLaunchKernelGGL(k_attend_bf16<128>, grid, dim3(256), 0, s, p);
-    else
-      hipLaunchKernelGGL(k_attend_bf16<64>, grid, dim3(256), 0, s, p);
+    const int ds = p.dh / p.G;
+    const int vm = ds >= 8 ? kWide : (ds == 4 ? kDs4 : kDs2);
+    auto k = p.dh == 128 ? (vm == kWide ? k_attend_bf16<128, kWide> : vm == kDs4 ? k_attend_bf16<128, kDs4>
+                                                                                : k_attend_bf16<128, kDs2>)
+                         : (vm == kWide ? k_attend_bf16<64, kWide> : vm == kDs4 ? k_attend_bf16<64, kDs4>
+                                                                               : k_attend_bf16<64, kDs2>);
+    hipLaunchKernelGGL(k, grid, dim3(256), 0, s, p);
   } else {
     const dim3 grid(static_cast<unsigned>(static_cast<size_t>(p.B) * p.H * p.Tq));
     if (bf16)

@@ -76,21 +76,35 @@ __global__ __launch_bounds__(256) void k_pack_scatter(const char* __restrict__ z
     }
   }
   __syncthreads();
-  const size_t zrow = static_cast<size_t>(H) * dh * esz;
+  const uint32_t zrow = static_cast<uint32_t>(H) * dh * esz;
+  // this workgroup's source rows; out-of-range items load as zero and are not stored
+  const rsrc_t r_z = make_rsrc(z + (static_cast<size_t>(b) * T + t0) * zrow, static_cast<uint32_t>(nt) * zrow);
   const int items = nh * n * pieces;
-  for (int i = threadIdx.x; i < items; i += 256) {
-    const int piece = i % pieces;
-    const int rest = i / pieces;
-    const int sl = rest % n;
-    const int h = h0 + rest / n;
-    const int64_t slot = static_cast<int64_t>(base) + sl;
-    if (slot >= cap) continue;
-    const int e = src_of_slot[sl];
-    const int tl = e >> 5, g = e & 31;
-    const char* src = z + static_cast<size_t>(b * static_cast<size_t>(T) + t0 + tl) * zrow +
-                      (static_cast<size_t>(h) * dh + static_cast<size_t>(g) * ds) * esz + piece * VB;
-    char* dst = Vp + ((static_cast<size_t>(b) * H + h) * cap + slot) * gbytes + piece * VB;
-    *reinterpret_cast<V*>(dst) = *reinterpret_cast<const V*>(src);
+  constexpr int U = 4;  // loads issued before their stores
+  for (int i0 = threadIdx.x; i0 < items; i0 += 256 * U) {
+    V val[U];
+    char* dst[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + 256 * u;
+      const int piece = i % pieces;
+      const int rest = i / pieces;
+      const int sl = n ? rest % n : 0;
+      const int h = h0 + (n ? rest / n : 0);
+      const int64_t slot = static_cast<int64_t>(base) + sl;
+      const bool ok = i < items && slot < cap;
+      const int e = src_of_slot[ok ? sl : 0];
+      const int tl = e >> 5, g = e & 31;
+      const uint32_t so = static_cast<uint32_t>(tl) * zrow + static_cast<uint32_t>((h * dh + g * ds) * esz + piece * VB);
+      const uint32_t off = ok ? so : kOOB;
+      if constexpr (VB == 16) val[u] = bload16(r_z, off);
+      else if constexpr (VB == 8) val[u] = bload8(r_z, off);
+      else val[u] = bload4(r_z, off);
+      dst[u] = ok ? Vp + ((static_cast<size_t>(b) * H + h) * cap + slot) * gbytes + piece * VB : nullptr;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (dst[u]) *reinterpret_cast<V*>(dst[u]) = val[u];
   }
 }
 

@@ -23,11 +23,21 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(const bf16* __restrict__ v,
   xcd_split(blockIdx.x, H, h, chunk);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
   const bf16* Rh = R + static_cast<size_t>(h) * DH * DH;
-  for (int pc = tid; pc < DH * DH / 8; pc += 256) {
-    const int k = pc / (DH / 8), j0 = (pc % (DH / 8)) * 8;
-    const bf16x8 val = *reinterpret_cast<const bf16x8*>(Rh + k * DH + j0);
+  {
+    constexpr int NP = DH * DH / 8 / 256;  // 16-byte pieces of R_h per thread
+    bf16x8 val[NP];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) Rt[(j0 + e) * LD + k] = val[e];
+    for (int r = 0; r < NP; ++r) {
+      const int pc = tid + 256 * r;
+      val[r] = *reinterpret_cast<const bf16x8*>(Rh + (pc / (DH / 8)) * DH + (pc % (DH / 8)) * 8);
+    }
+#pragma unroll
+    for (int r = 0; r < NP; ++r) {
+      const int pc = tid + 256 * r;
+      const int k = pc / (DH / 8), j0 = (pc % (DH / 8)) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Rt[(j0 + e) * LD + k] = val[r][e];
+    }
   }
   __syncthreads();
   bf16x8 af[MT][KS];
@@ -39,15 +49,17 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(const bf16* __restrict__ v,
 
   const int t_begin = chunk * tok_per_wg;
   const int t_end = min(t_begin + tok_per_wg, ntok);
-  const bf16x8 zero = {};
+  // this workgroup's tokens of head h; rows past t_end load as zero
+  const uint32_t tstride = static_cast<uint32_t>(H) * DH * 2;
+  const rsrc_t r_v = make_rsrc(v + (static_cast<size_t>(t_begin) * H + h) * DH,
+                               static_cast<uint32_t>(t_end - t_begin - 1) * tstride + DH * 2);
   int t0 = t_begin + 16 * w;
   bf16x8 nxt[KS];
   auto load = [&](int tt) {
     const int tok = tt + l16;
-    const bool ok = tok < t_end;
-    const bf16* vr = v + (static_cast<size_t>(ok ? tok : 0) * H + h) * DH + 8 * g4;
+    const uint32_t o = static_cast<uint32_t>(tok - t_begin) * tstride + 16u * g4;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) nxt[ks] = ok ? *reinterpret_cast<const bf16x8*>(vr + 32 * ks) : zero;
+    for (int ks = 0; ks < KS; ++ks) nxt[ks] = __builtin_bit_cast(bf16x8, bload16(r_v, tok < t_end ? o + 64u * ks : kOOB));
   };
   if (t0 < t_end) load(t0);
   for (; t0 < t_end; t0 += 64) {

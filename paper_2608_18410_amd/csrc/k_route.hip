@@ -19,62 +19,167 @@ namespace {
 constexpr int kLang = 1;
 
 // ---------------------------------------------------------------------------
-// Blocks 0..B-1: hl = mean of the sample's language rows of h (zero if none),
-//   MLP2:     cb[b][j] = W1[j, d+d_e : 2d+d_e] . hl + b1[j]
-//   ADDITIVE: cb[b][s] = alpha_lang (W_lang[s] . hl + b_lang[s])
-// Block B:  MLP2 F[j][c] = W1[j, d : d+d_e] . E[c];  ADDITIVE F[s][c] = alpha_role W_role[s][c]
+// Language pool (Sec. 3.4): hbar[b] = mean of the sample's language rows of h
+// (zero when it has none). 1D grid: B x ceil(d / (64*VEC)) blocks. A block
+// owns 64*VEC columns of one sample; its language rows are listed in LDS in
+// ascending order, the four waves take every fourth listed row, and the wave
+// partial sums are added in wave order (deterministic).
 template <class T>
-__global__ __launch_bounds__(256) void k_route_prep(RouteParams p) {
-  extern __shared__ float hl[];
+__global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int TCH = 1024;  // tokens listed per pass
+  __shared__ int s_rows[TCH];
+  __shared__ int s_wcnt[4];
+  __shared__ float s_part[4][64 * VEC];
+  const int ncb = (p.d + 64 * VEC - 1) / (64 * VEC);
+  const int b = blockIdx.x / ncb, cb = blockIdx.x % ncb;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint8_t* ty = p.types + static_cast<size_t>(b) * p.T;
+  const int col = cb * 64 * VEC + lane * VEC;
+  const bool vec = (p.d % VEC) == 0;
+  const T* hsample = static_cast<const T*>(p.h) + static_cast<size_t>(b) * p.T * p.d;
+  const rsrc_t r_h = make_rsrc(hsample, static_cast<uint32_t>(p.T) * p.d * sizeof(T));
+  float acc[VEC];
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
+  int n_total = 0;
+  for (int c0 = 0; c0 < p.T; c0 += TCH) {
+    const int nc = min(TCH, p.T - c0);
+    // ascending list of this chunk's language rows (wave ballots + prefix)
+    int base = 0;
+    for (int s0 = 0; s0 < nc; s0 += 256) {
+      const int t = c0 + s0 + tid;
+      const bool lang = (s0 + tid < nc) && ty[t] == kLang;
+      const uint64_t bal = __ballot(lang);
+      const int pre = __popcll(bal & ((1ull << lane) - 1ull));
+      if (lane == 0) s_wcnt[w] = __popcll(bal);
+      __syncthreads();
+      int woff = base;
+      for (int i = 0; i < w; ++i) woff += s_wcnt[i];
+      if (lang) s_rows[woff + pre] = t;
+      base += s_wcnt[0] + s_wcnt[1] + s_wcnt[2] + s_wcnt[3];
+      __syncthreads();
+    }
+    n_total += base;
+    if (vec && col < p.d) {
+      // wave w sums listed rows w, w+4, ...; 4 loads in flight per step
+      for (int i0 = w; i0 < base; i0 += 16) {
+        u32x4 raw[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int i = i0 + 4 * u;
+          raw[u] = bload16(r_h, i < base ? static_cast<uint32_t>((static_cast<size_t>(s_rows[i]) * p.d + col) * sizeof(T)) : kOOB);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const T* v = reinterpret_cast<const T*>(&raw[u]);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) acc[e] += tof(v[e]);
+        }
+      }
+    } else if (!vec) {
+      for (int i = w; i < base; i += 4)
+        for (int e = 0; e < VEC; ++e)
+          if (col + e < p.d) acc[e] += tof(hsample[static_cast<size_t>(s_rows[i]) * p.d + col + e]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) s_part[w][lane * VEC + e] = acc[e];
+  __syncthreads();
+  const float inv = n_total ? 1.f / static_cast<float>(n_total) : 0.f;
+  for (int i = tid; i < 64 * VEC; i += 256) {
+    const int c = cb * 64 * VEC + i;
+    if (c < p.d)
+      p.hbar[static_cast<size_t>(b) * p.d + c] = (((s_part[0][i] + s_part[1][i]) + s_part[2][i]) + s_part[3][i]) * inv;
+  }
+}
+
+// Per-sample language term and folded role term. 1D grid:
+//   blocks [0, B*nrb): 8 output rows of one sample (2 per wave),
+//     MLP2:     cb[b][j] = W1[j, d+d_e : 2d+d_e] . hbar[b] + b1[j]
+//     ADDITIVE: cb[b][s] = alpha_lang (W_lang[s] . hbar[b] + b_lang[s])
+//   blocks [B*nrb, ...): F rows, one per wave,
+//     MLP2:     F[j][c] = W1[j, d : d+d_e] . E[c]      (so W1_e e = F a)
+//     ADDITIVE: F[s][c] = alpha_role W_role[s][c]
+template <class T>
+__global__ __launch_bounds__(256) void k_route_proj(RouteParams p) {
+  extern __shared__ float hs[];
+  constexpr int VEC = 16 / sizeof(T);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nout = p.kind == 0 ? p.Hr : p.G;
+  const int nrb = (nout + 7) / 8;
   const size_t W1s = 2 * static_cast<size_t>(p.d) + p.d_e;
-  if (blockIdx.x == static_cast<unsigned>(p.B)) {
+  if (blockIdx.x >= static_cast<unsigned>(p.B * nrb)) {
+    const int j = (blockIdx.x - p.B * nrb) * 4 + wave;
     if (p.kind == 0) {
-      const T* W1 = static_cast<const T*>(p.W1);
+      if (j >= p.Hr) return;
+      const T* w1 = static_cast<const T*>(p.W1) + j * W1s + p.d;
       const T* E = static_cast<const T*>(p.E);
-      for (int o = tid; o < p.Hr * p.C; o += 256) {
-        const int j = o / p.C, c = o % p.C;
+      for (int c = 0; c < p.C; ++c) {
         float acc = 0.f;
-        for (int m = 0; m < p.d_e; ++m)
-          acc += tof(W1[j * W1s + p.d + m]) * tof(E[static_cast<size_t>(c) * p.d_e + m]);
-        p.F[o] = acc;
+        for (int m = lane; m < p.d_e; m += 64) acc += tof(w1[m]) * tof(E[static_cast<size_t>(c) * p.d_e + m]);
+        acc = wave_sum(acc);
+        if (lane == 0) p.F[j * p.C + c] = acc;
       }
     } else {
+      if (j >= p.G) return;
       const T* Wro = static_cast<const T*>(p.W_role);
-      for (int o = tid; o < p.G * p.C; o += 256) p.F[o] = p.alpha_role * tof(Wro[o]);
+      for (int c = lane; c < p.C; c += 64) p.F[j * p.C + c] = p.alpha_role * tof(Wro[j * p.C + c]);
     }
     return;
   }
-  const int b = blockIdx.x;
-  const T* h = static_cast<const T*>(p.h) + static_cast<size_t>(b) * p.T * p.d;
-  const uint8_t* ty = p.types + static_cast<size_t>(b) * p.T;
-  int n = 0;
-  for (int t = 0; t < p.T; ++t) n += (ty[t] == kLang);
-  const float inv = n ? 1.f / static_cast<float>(n) : 0.f;
-  for (int col = tid; col < p.d; col += 256) {
-    float acc = 0.f;
-    for (int t = 0; t < p.T; ++t)
-      if (ty[t] == kLang) acc += tof(h[static_cast<size_t>(t) * p.d + col]);
-    hl[col] = acc * inv;
+  const int b = blockIdx.x / nrb, j0 = (blockIdx.x % nrb) * 8;
+  const float* hb = p.hbar + static_cast<size_t>(b) * p.d;
+  {
+    // stage hbar: all of a thread's loads issued before its LDS stores
+    const rsrc_t r_hb = make_rsrc(hb, static_cast<uint32_t>(p.d) * 4u);
+    for (int k0 = 0; k0 < p.d; k0 += 256 * 4 * 8) {
+      u32x4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int k = k0 + (u * 256 + tid) * 4;
+        v[u] = bload16(r_hb, k + 4 <= p.d ? 4u * k : kOOB);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int k = k0 + (u * 256 + tid) * 4;
+        if (k + 4 <= p.d) *reinterpret_cast<u32x4*>(hs + k) = v[u];
+      }
+    }
+    for (int k = (p.d / 4) * 4 + tid; k < p.d; k += 256) hs[k] = hb[k];
   }
   __syncthreads();
-  const int nout = p.kind == 0 ? p.Hr : p.G;
-  for (int o = wave; o < nout; o += 4) {
+  const bool vec = (p.d % (64 * VEC)) == 0;
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int j = j0 + 2 * wave + r;
+    if (j >= nout) break;
     const T* wrow;
     float bias, scale;
     if (p.kind == 0) {
-      wrow = static_cast<const T*>(p.W1) + o * W1s + p.d + p.d_e;
-      bias = tof(static_cast<const T*>(p.b1)[o]);
+      wrow = static_cast<const T*>(p.W1) + j * W1s + p.d + p.d_e;
+      bias = tof(static_cast<const T*>(p.b1)[j]);
       scale = 1.f;
     } else {
-      wrow = static_cast<const T*>(p.W_lang) + static_cast<size_t>(o) * p.d;
-      bias = tof(static_cast<const T*>(p.b_lang)[o]);
+      wrow = static_cast<const T*>(p.W_lang) + static_cast<size_t>(j) * p.d;
+      bias = tof(static_cast<const T*>(p.b_lang)[j]);
       scale = p.alpha_lang;
     }
     float acc = 0.f;
-    for (int k = lane; k < p.d; k += 64) acc += tof(wrow[k]) * hl[k];
+    if (vec && (reinterpret_cast<uintptr_t>(wrow) & 15) == 0) {
+#pragma unroll 8
+      for (int k = lane * VEC; k < p.d; k += 64 * VEC) {
+        const u32x4 raw = *reinterpret_cast<const u32x4*>(wrow + k);
+        const T* v = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc += tof(v[i]) * hs[k + i];
+      }
+    } else {
+      for (int k = lane; k < p.d; k += 64) acc += tof(wrow[k]) * hs[k];
+    }
     acc = wave_sum(acc);
-    if (lane == 0) p.cb[static_cast<size_t>(b) * nout + o] = scale * (acc + bias);
+    if (lane == 0) p.cb[static_cast<size_t>(b) * nout + j] = scale * (acc + bias);
   }
 }
 
@@ -250,8 +355,8 @@ constexpr int kRtTok = 64, kRtKc = 64, kRtRows = 144, kRtLd = kRtKc + 8;
 
 __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
   __shared__ __attribute__((aligned(16))) bf16 Ws[2][kRtRows * kRtLd];
-  __shared__ float Fs[128 * 16];
-  __shared__ bf16 W2s[32 * 128];
+  __shared__ __attribute__((aligned(16))) float Fs[128 * 16];
+  __shared__ __attribute__((aligned(16))) bf16 W2s[32 * 128];
   __shared__ float b2s[32], brs[16];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
   const int d = p.d, C = p.C, G = p.G;
@@ -259,31 +364,55 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
   const size_t W1s = 2 * static_cast<size_t>(d) + p.d_e;
   const bf16* W1 = static_cast<const bf16*>(p.W1);
   const bf16* Wr = static_cast<const bf16*>(p.W_r);
-  for (int i = tid; i < Hr * C; i += 256) Fs[i] = p.F[i];
-  for (int i = tid; i < G * Hr; i += 256) W2s[i] = static_cast<const bf16*>(p.W2)[i];
-  if (tid < G) b2s[tid] = tof(static_cast<const bf16*>(p.b2)[tid]);
-  if (tid < C) brs[tid] = tof(static_cast<const bf16*>(p.b_r)[tid]);
+  {
+    // stage F (Hr x C f32) and W2 (G x Hr bf16): loads first, then LDS stores
+    const rsrc_t r_F = make_rsrc(p.F, static_cast<uint32_t>(Hr * C) * 4u);
+    const rsrc_t r_W2 = make_rsrc(p.W2, static_cast<uint32_t>(G * Hr) * 2u);
+    u32x4 f[2], w2[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int i = (u * 256 + tid) * 4;  // floats of F
+      f[u] = bload16(r_F, i < Hr * C ? 4u * i : kOOB);
+      const int j = (u * 256 + tid) * 8;  // bf16 of W2
+      w2[u] = bload16(r_W2, j < G * Hr ? 2u * j : kOOB);
+    }
+    const float b2v = tid < G ? tof(static_cast<const bf16*>(p.b2)[tid]) : 0.f;
+    const float brv = tid < C ? tof(static_cast<const bf16*>(p.b_r)[tid]) : 0.f;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int i = (u * 256 + tid) * 4;
+      if (i < Hr * C) *reinterpret_cast<u32x4*>(Fs + i) = f[u];
+      const int j = (u * 256 + tid) * 8;
+      if (j < G * Hr) *reinterpret_cast<u32x4*>(W2s + j) = w2[u];
+    }
+    if (tid < G) b2s[tid] = b2v;
+    if (tid < C) brs[tid] = brv;
+  }
 
   const int N = p.B * p.T;
-  const int tok = blockIdx.x * kRtTok + 16 * w + l16;
+  const int tok0 = blockIdx.x * kRtTok;
+  const int tok = tok0 + 16 * w + l16;
   const bool valid = tok < N;
-  const bf16* hrow = static_cast<const bf16*>(p.h) + static_cast<size_t>(valid ? tok : 0) * d + 8 * g4;
+  // buffer resources: rows past the valid range load as zero with no memory access
+  const rsrc_t r_h = make_rsrc(static_cast<const bf16*>(p.h) + static_cast<size_t>(tok0) * d,
+                               static_cast<uint32_t>(min(kRtTok, N - tok0)) * d * 2);
+  const rsrc_t r_w1 = make_rsrc(W1, static_cast<uint32_t>(Hr * W1s * 2));
+  const rsrc_t r_wr = make_rsrc(Wr, static_cast<uint32_t>(C) * d * 2);
+  const uint32_t hoff = static_cast<uint32_t>(16 * w + l16) * d * 2 + 16u * g4;
 
+  // Pieces r = 0..3 of this thread are rows < 128 of W1; piece 4 covers the
+  // role rows (wave 0: rows 128..135, wave 1: 136..143); waves 2-3 have none.
   u32x4 wr[5];
   auto load_w = [&](int kc) {
 #pragma unroll
-    for (int r = 0; r < 5; ++r) {
+    for (int r = 0; r < 4; ++r) {
       const int pc = tid + 256 * r;
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (pc < kRtRows * 8) {
-        const int row = pc >> 3, c8 = pc & 7;
-        if (row < Hr)
-          val = *reinterpret_cast<const u32x4*>(W1 + row * W1s + kc + 8 * c8);
-        else if (row - Hr < C)
-          val = *reinterpret_cast<const u32x4*>(Wr + static_cast<size_t>(row - Hr) * d + kc + 8 * c8);
-      }
-      wr[r] = val;
+      const int row = pc >> 3, c8 = pc & 7;
+      wr[r] = bload16(r_w1, static_cast<uint32_t>((row * W1s + kc + 8 * c8) * 2));
     }
+    const int pc = tid + 1024;
+    const int row = (pc >> 3) - Hr, c8 = pc & 7;
+    wr[4] = bload16(r_wr, (pc < kRtRows * 8 && row < C) ? static_cast<uint32_t>((row * d + kc + 8 * c8) * 2) : kOOB);
   };
   auto store_w = [&](int buf) {
 #pragma unroll
@@ -297,9 +426,8 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
   };
   bf16x8 hb0, hb1;
   auto load_h = [&](int kc) {
-    const bf16x8 zero = {};
-    hb0 = valid ? *reinterpret_cast<const bf16x8*>(hrow + kc) : zero;
-    hb1 = valid ? *reinterpret_cast<const bf16x8*>(hrow + kc + 32) : zero;
+    hb0 = __builtin_bit_cast(bf16x8, bload16(r_h, valid ? hoff + 2u * kc : kOOB));
+    hb1 = __builtin_bit_cast(bf16x8, bload16(r_h, valid ? hoff + 2u * kc + 64u : kOOB));
   };
 
   f32x4 acc[9];
@@ -417,11 +545,22 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
 hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s) {
   const size_t ntok = static_cast<size_t>(p.B) * p.T;
   if (ntok == 0) return hipSuccess;
-  const size_t prep_shm = static_cast<size_t>(p.d) * sizeof(float);
-  if (bf16)
-    hipLaunchKernelGGL(k_route_prep<rolesub::bf16>, dim3(p.B + 1), dim3(256), prep_shm, s, p);
-  else
-    hipLaunchKernelGGL(k_route_prep<float>, dim3(p.B + 1), dim3(256), prep_shm, s, p);
+  {
+    const int vec = bf16 ? 8 : 4;
+    const int ncb = (p.d + 64 * vec - 1) / (64 * vec);
+    const dim3 gpool(static_cast<unsigned>(p.B * ncb));
+    const int nout = p.kind == 0 ? p.Hr : p.G;
+    const int nF = ((p.kind == 0 ? p.Hr : p.G) + 3) / 4;
+    const dim3 gproj(static_cast<unsigned>(p.B * ((nout + 7) / 8) + nF));
+    const size_t shm = static_cast<size_t>(p.d) * sizeof(float);
+    if (bf16) {
+      hipLaunchKernelGGL(k_route_pool<rolesub::bf16>, gpool, dim3(256), 0, s, p);
+      hipLaunchKernelGGL(k_route_proj<rolesub::bf16>, gproj, dim3(256), shm, s, p);
+    } else {
+      hipLaunchKernelGGL(k_route_pool<float>, gpool, dim3(256), 0, s, p);
+      hipLaunchKernelGGL(k_route_proj<float>, gproj, dim3(256), shm, s, p);
+    }
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const bool mfma_ok = bf16 && p.kind == 0 && p.Hr == 128 && p.C >= 1 && p.C <= 16 &&

@@ -14,6 +14,7 @@ struct RouteParams {
   const void *W_tok, *b_tok, *W_role, *W_lang, *b_lang;
   float* cb;  // [B][Hr or G] per-sample language term (workspace)
   float* F;   // [Hr or G][C] folded role term (workspace)
+  float* hbar;  // [B][d] pooled language state (workspace)
   int mode;
   int k_by_type[4];
   float tau;
@@ -32,6 +33,7 @@ inline size_t route_cb_floats(int B, int Hr, int G, int kind) {
 inline size_t route_F_floats(int Hr, int G, int C, int kind) {
   return static_cast<size_t>(kind == 0 ? Hr : G) * C;
 }
+inline size_t route_hbar_floats(int B, int d) { return static_cast<size_t>(B) * d; }
 
 hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s);
 // LDS bytes the generic (one token per workgroup) router needs.

@@ -33,6 +33,9 @@ rolesub_status from_hip(hipError_t e, const char* what) {
 bool valid_dtype(rolesub_dtype t) { return t == ROLESUB_F32 || t == ROLESUB_BF16; }
 size_t esize(rolesub_dtype t) { return t == ROLESUB_F32 ? 4 : 2; }
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+// Kernels address each sample's (or workgroup's) slice of a tensor through a
+// buffer resource that must cover less than 2 GiB.
+constexpr size_t kMaxRegion = static_cast<size_t>(1) << 31;
 
 // B, T >= 0; H >= 1; dh in {64, 128}.
 rolesub_status check_value_dims(const rolesub_dims* d, const char* fn) {
@@ -80,7 +83,8 @@ bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
 size_t route_ws_bytes(const rolesub_dims* d, const rolesub_router* r) {
   if (!d || !r || d->B <= 0) return 0;
   return align256(route_cb_floats(d->B, r->Hr, d->G, r->kind) * sizeof(float)) +
-         align256(route_F_floats(r->Hr, d->G, r->C, r->kind) * sizeof(float));
+         align256(route_F_floats(r->Hr, d->G, r->C, r->kind) * sizeof(float)) +
+         align256(route_hbar_floats(d->B, d->d > 0 ? d->d : 0) * sizeof(float));
 }
 
 }  // namespace
@@ -114,6 +118,8 @@ rolesub_status rolesub_rotate_values(const rolesub_dims* dims, rolesub_dtype dty
   if (ntok > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
   const size_t bytes = ntok * dims->H * dims->dh * esize(dtype);
   if (ranges_overlap(v, bytes, z, bytes)) return fail(ROLESUB_ERR_INVALID_ARG, "%s: z overlaps v", fn);
+  if (static_cast<size_t>(256) * dims->H * dims->dh * esize(dtype) >= kMaxRegion)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: too many heads", fn);
   return from_hip(launch_rotate(dtype == ROLESUB_BF16, static_cast<int>(ntok), dims->H, dims->dh, v, R,
                                 z, static_cast<hipStream_t>(stream)),
                   fn);
@@ -182,6 +188,9 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype, cons
   if (route_generic_shm(dims->d, dims->G, router->C, router->Hr, router->kind) > 64 * 1024 ||
       static_cast<size_t>(dims->d) * sizeof(float) > 64 * 1024)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: hidden size d=%d too large", fn, dims->d);
+  if (static_cast<size_t>(dims->T) * dims->d * esize(dtype) >= kMaxRegion ||
+      static_cast<size_t>(router->Hr) * (2 * static_cast<size_t>(dims->d) + router->d_e) * esize(dtype) >= kMaxRegion)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: one sample's hidden states exceed 2 GiB", fn);
   const size_t need = route_ws_bytes(dims, router);
   if (ws_bytes < need || (need && !workspace))
     return fail(ROLESUB_ERR_INVALID_ARG, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws_bytes);
@@ -207,7 +216,10 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype, cons
   p.b_lang = router->b_lang;
   char* ws = static_cast<char*>(workspace);
   p.cb = reinterpret_cast<float*>(ws);
-  p.F = reinterpret_cast<float*>(ws + align256(route_cb_floats(p.B, p.Hr, p.G, p.kind) * sizeof(float)));
+  const size_t off_F = align256(route_cb_floats(p.B, p.Hr, p.G, p.kind) * sizeof(float));
+  const size_t off_h = off_F + align256(route_F_floats(p.Hr, p.G, p.C, p.kind) * sizeof(float));
+  p.F = reinterpret_cast<float*>(ws + off_F);
+  p.hbar = reinterpret_cast<float*>(ws + off_h);
   return from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
 }
 
@@ -242,6 +254,8 @@ rolesub_status rolesub_pack_kv(const rolesub_dims* dims, rolesub_dtype dtype, co
     return fail(ROLESUB_ERR_INVALID_ARG, "%s: z, mask, offsets and Vp must be non-NULL", fn);
   if (static_cast<size_t>(dims->B) * dims->T > 0x7FFFFFFF)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
+  if (static_cast<size_t>(dims->H) * cap_groups * (dims->dh / dims->G) * esize(dtype) >= kMaxRegion)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: one sample's packed cache exceeds 2 GiB", fn);
   return from_hip(launch_pack(dtype == ROLESUB_BF16, dims->B, dims->T, dims->H, dims->dh, dims->G, z, mask,
                               offsets, Vp, cap_groups, static_cast<hipStream_t>(stream)),
                   fn);
@@ -276,6 +290,10 @@ rolesub_status rolesub_attend(const rolesub_dims* dims, rolesub_dtype dtype, int
   if (static_cast<size_t>(dims->B) * dims->H > 0x7FFFFFFF ||
       static_cast<size_t>(dims->B) * dims->H * Tq > 0x7FFFFFFF)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: grid too large", fn);
+  if (static_cast<size_t>(dims->T) * dims->H * dims->dh * esize(dtype) >= kMaxRegion ||
+      static_cast<size_t>(Tq) * dims->H * dims->dh * esize(dtype) >= kMaxRegion ||
+      static_cast<size_t>(cap_groups) * (dims->dh / dims->G) * esize(dtype) >= kMaxRegion)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: one sample's keys, queries or packed cache exceed 2 GiB", fn);
   AttendParams p = {};
   p.B = dims->B;
   p.T = dims->T;

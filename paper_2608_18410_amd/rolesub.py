@@ -188,10 +188,16 @@ def route(token_type: torch.Tensor, budget: Budget, G: int, h: torch.Tensor | No
     d = 0 if h is None else h.shape[2]
     dtype = torch.float32 if h is None else h.dtype
     o = out or {}
-    mask = o.get("mask", torch.empty((B, T), dtype=torch.int32, device=dev))
-    idx = o.get("idx", torch.empty((B, T, G), dtype=torch.uint8, device=dev)) if want_idx else None
-    cnt = o.get("count", torch.empty((B, T), dtype=torch.uint8, device=dev)) if want_count else None
-    sco = o.get("scores", torch.empty((B, T, G), dtype=torch.float32, device=dev)) if want_scores else None
+
+    def buf(name, shape, dtype, want=True):
+        if not want:
+            return None
+        return o[name] if name in o else torch.empty(shape, dtype=dtype, device=dev)
+
+    mask = buf("mask", (B, T), torch.int32)
+    idx = buf("idx", (B, T, G), torch.uint8, want_idx)
+    cnt = buf("count", (B, T), torch.uint8, want_count)
+    sco = buf("scores", (B, T, G), torch.float32, want_scores)
     dims = Dims(B, T, 1, 64, G, d)
     desc = router.desc() if router is not None else None
     ws_ptr, ws_bytes = None, 0
@@ -201,7 +207,7 @@ def route(token_type: torch.Tensor, budget: Budget, G: int, h: torch.Tensor | No
             workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
         ws_ptr, ws_bytes = _ptr(workspace), workspace.numel()
     _check("rolesub_route", load().rolesub_route(
-        ctypes.byref(dims), _code(torch.empty(0, dtype=dtype)),
+        ctypes.byref(dims), F32 if dtype == torch.float32 else BF16,
         ctypes.byref(desc) if desc is not None else None, ctypes.byref(budget),
         _ptr(h), _ptr(token_type, torch.uint8), _ptr(scores_in, torch.float32), _ptr(sco),
         _ptr(mask), _ptr(idx), _ptr(cnt), ws_ptr, ws_bytes, _stream(stream)))

@@ -47,7 +47,7 @@ def _check_selection(scores, types, budget, G, mode, kbt, tau=0.0, kmin=0, kmax=
     idx, cnt = O.mask_to_idx(want, G)
     assert np.array_equal(host(r["count"]), cnt)
     assert np.array_equal(host(r["idx"]), idx)
-    assert np.array_equal(host(r["scores"]), scores)
+    assert np.array_equal(host(r["scores"]).view(np.uint32), scores.view(np.uint32))   # passed through bit for bit
 
 
 def test_select_threshold_stress_logits():
