@@ -43,12 +43,14 @@ def attend_bytes(w, sum_k: int, out_esize: int) -> int:
 
 
 def stage_bytes(w, sum_k: int) -> dict:
+    """Algorithmic HBM bytes per layer call of each stage as the step runs
+    them (rotation and pack fused: v read once, only kept groups written)."""
     e = 2 if w.dtype == "bf16" else 4
     route_w = (w.Hr * w.router_in + w.C * w.d + w.G * w.Hr + w.C * w.d_e) * e
     return {
         "route": w.B * w.T * w.d * e + route_w + 4 * w.B * w.T * (w.G + 2),
-        "rotate": 2 * w.B * w.T * w.H * w.dh * e + w.H * w.dh * w.dh * e,
-        "pack": 2 * w.B * sum_k * w.ds * w.H * e + 8 * w.B * w.T,
+        "rotate_pack": w.B * w.T * w.H * w.dh * e + w.H * w.dh * w.dh * e
+                       + w.B * sum_k * w.ds * w.H * e + 8 * w.B * w.T,
         "attend": attend_bytes(w, sum_k, e),
     }
 
@@ -102,6 +104,8 @@ def main():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="issue the calls directly, no HIP graphs")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 4 times (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -116,6 +120,16 @@ def main():
     from paper_2608_18410_amd.pipeline import LayerBuffers, pack_capacity, run_layer
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_probe:
+        # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings
+        # calibrate the HBM traffic counters (1 GiB read + 1 GiB written per copy).
+        src = torch.ones(2 ** 29, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": src.numel() * 2, "copies": 4}), flush=True)
+        return
     rs.load()
     dev = torch.device("cuda:0")
     w = synth.workload(args.workload)
@@ -149,7 +163,8 @@ def main():
         if w.scores_in:
             scores = torch.from_numpy(np.stack([synth.sample_scores(w, l, b) for b in range(w.B)])).to(dev)
         ws = rs.route_workspace_size(w.B, w.T, w.G, w.d, router)
-        bufs = LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, dt, ws_bytes=ws, device=dev)
+        bufs = LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, dt, ws_bytes=ws, device=dev,
+                                     with_z=False)
         layers.append(dict(acts=acts, router=router if scores is None else None, scores=scores,
                            R=put(wt["R"]), bufs=bufs))
         print(f"# layer {l} inputs resident ({time.time() - t_gen:.1f} s)", file=sys.stderr, flush=True)
@@ -160,8 +175,7 @@ def main():
         rs.route(types, budget, w.G, h=a.get("h"), router=L["router"], scores_in=L["scores"],
                  workspace=bf.workspace,
                  out={"mask": bf.mask, "idx": bf.idx, "count": bf.count, "scores": bf.scores})
-        rs.rotate_values(a["v"], L["R"], out=bf.z)
-        rs.pack_kv(bf.z, bf.mask, w.G, cap, out=(bf.offsets, bf.Vp))
+        rs.rotate_pack(a["v"], L["R"], bf.mask, w.G, cap, out=(bf.offsets, bf.Vp))
 
     def att(L):
         a, bf = L["acts"], L["bufs"]

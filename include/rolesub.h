@@ -9,6 +9,7 @@
  *                                                            Eq. routingscore,
  *                                                            Sec. 3.4, 3.5)
  *   rolesub_pack_kv        compact cache of the kept groups of M z (Sec. 3.2)
+ *   rolesub_rotate_pack    the two above in one pass, z never stored
  *   rolesub_attend         attention with unchanged queries and keys over the
  *                          routed values v~ = R M R^T v     (Sec. 3, 3.2)
  *
@@ -165,6 +166,19 @@ rolesub_status rolesub_pack_kv(const rolesub_dims* dims, rolesub_dtype dtype,
                                const rolesub_budget* budget, const int32_t* type_counts,
                                const void* z, const uint32_t* mask, int32_t* offsets, void* Vp,
                                int64_t cap_groups, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * rolesub_rotate_pack: rolesub_rotate_values followed by rolesub_pack_kv in
+ * one pass (Sec. 3.2: z = R^T v, then the kept groups of M z), without
+ * materialising z. Arguments, layouts, capacity rules and outputs (offsets,
+ * Vp) are those of the two calls: v and R as for rolesub_rotate_values; mask,
+ * offsets, Vp, cap_groups, budget and type_counts as for rolesub_pack_kv.
+ * Vp holds the same bits the two calls would produce.
+ * ------------------------------------------------------------------------ */
+rolesub_status rolesub_rotate_pack(const rolesub_dims* dims, rolesub_dtype dtype,
+                                   const rolesub_budget* budget, const int32_t* type_counts,
+                                   const void* v, const void* R, const uint32_t* mask,
+                                   int32_t* offsets, void* Vp, int64_t cap_groups, void* stream);
 
 /* ---------------------------------------------------------------------------
  * rolesub_attend: attention with full queries and keys over the routed

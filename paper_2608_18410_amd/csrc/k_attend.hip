@@ -31,8 +31,10 @@ __device__ __forceinline__ uint32_t group_mask(int G) { return G >= 32 ? 0xFFFFF
 // and packed groups of tile i+1 are in flight into registers, and the group
 // masks and cache offsets of tile i+2 (which address tile i+2's packed groups)
 // are in flight too.
-// After the last tile, O^T = R_h U^T (one more MFMA chain, U in bf16) and
-// each lane stores 4 consecutive outputs of its query.
+// R_h is staged into LDS in the prologue (coalesced 16-byte rows, latency
+// hidden behind the first tiles). After the last tile, O^T = R_h U^T (one
+// more MFMA chain, U in bf16, R_h fragments from LDS) and each lane stores 4
+// consecutive outputs of its query.
 // VM: how the 8-dim chunks of the value tile map to packed groups:
 //   kWide  groups of >= 8 dims (one 16-byte load per token and chunk)
 //   kDs4   4-dim groups (two 8-byte loads), kDs2  2-dim groups (four 4-byte loads)
@@ -47,6 +49,8 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
   __shared__ __attribute__((aligned(16))) uint32_t Zt[DH * ZLD];
   __shared__ uint32_t s_mask[2][TK];
   __shared__ int32_t s_off[2][TK];
+  constexpr int RLD = DH + 8;  // padded rows: conflict-free fragment reads per half-wave
+  __shared__ __attribute__((aligned(16))) bf16 Rs[DH * RLD];
   int h, b;
   xcd_split(blockIdx.x, p.H, h, b);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
@@ -152,14 +156,29 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
     }
   };
 
-  // ---- prologue: metadata of tiles 0 and 1, operands of tile 0
+  // ---- prologue: R_h into LDS (coalesced rows, used by the final
+  // back-rotation), metadata of tiles 0 and 1, operands of tile 0
+  {
+    constexpr int NRP = DH * DH / 8 / 256;  // 16-byte pieces of R_h per thread
+    const rsrc_t r_R = make_rsrc(static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH, DH * DH * 2);
+    u32x4 rv[NRP];
+#pragma unroll
+    for (int r = 0; r < NRP; ++r) rv[r] = bload16(r_R, 16u * (tid + 256 * r));
+    uint32_t m0;
+    int32_t o0;
+    load_meta(0, m0, o0);
+#pragma unroll
+    for (int r = 0; r < NRP; ++r) {
+      const int pc = tid + 256 * r;
+      *reinterpret_cast<u32x4*>(Rs + (pc / (DH / 8)) * RLD + 8 * (pc % (DH / 8))) = rv[r];
+    }
+    if (tid < TK) {
+      s_mask[0][tid] = m0 & gm;
+      s_off[0][tid] = o0;
+    }
+  }
   uint32_t mreg;
   int32_t oreg;
-  load_meta(0, mreg, oreg);
-  if (tid < TK) {
-    s_mask[0][tid] = mreg & gm;
-    s_off[0][tid] = oreg;
-  }
   load_meta(TK, mreg, oreg);
   __syncthreads();
   load_k(0);
@@ -247,23 +266,16 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
       ub[ks][i] = static_cast<bf16>(acc[2 * ks][i] * inv);
       ub[ks][4 + i] = static_cast<bf16>(acc[2 * ks + 1][i] * inv);
     }
-  const bf16* Rh = static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH;
   const size_t obase = ((static_cast<size_t>(b) * p.Tq + (qvalid ? qq : 0)) * H + h) * DH + 4 * g4;
-  u32x2 ra[MT][KS][2];
-#pragma unroll
-  for (int m = 0; m < MT; ++m)
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16* rr = Rh + (16 * m + l16) * DH + 4 * g4 + 32 * ks;
-      ra[m][ks][0] = *reinterpret_cast<const u32x2*>(rr);
-      ra[m][ks][1] = *reinterpret_cast<const u32x2*>(rr + 16);
-    }
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    const bf16* rr = Rs + (16 * m + l16) * RLD + 4 * g4;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const u32x4 av = {ra[m][ks][0][0], ra[m][ks][0][1], ra[m][ks][1][0], ra[m][ks][1][1]};
+      const u32x2 lo = *reinterpret_cast<const u32x2*>(rr + 32 * ks);
+      const u32x2 hi = *reinterpret_cast<const u32x2*>(rr + 32 * ks + 16);
+      const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
       o = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), ub[ks], o);
     }
     if (qvalid) {

@@ -110,6 +110,12 @@ __global__ __launch_bounds__(256) void k_pack_scatter(const char* __restrict__ z
 
 }  // namespace
 
+hipError_t launch_pack_offsets(int B, int T, int G, const uint32_t* mask, int32_t* offsets, hipStream_t s) {
+  if (B == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_pack_offsets, dim3(B), dim3(256), 0, s, mask, offsets, T, G);
+  return hipGetLastError();
+}
+
 hipError_t launch_pack(bool bf16, int B, int T, int H, int dh, int G, const void* z,
                        const uint32_t* mask, int32_t* offsets, void* Vp, int64_t cap,
                        hipStream_t s) {

@@ -113,14 +113,47 @@ __global__ __launch_bounds__(256) void k_route_proj(RouteParams p) {
   if (blockIdx.x >= static_cast<unsigned>(p.B * nrb)) {
     const int j = (blockIdx.x - p.B * nrb) * 4 + wave;
     if (p.kind == 0) {
+      // E staged in LDS (f32) once per block; each wave then dots its W1_e row
+      // with every role vector. Loads are batched before use.
+      const T* E = static_cast<const T*>(p.E);
+      const int ne = p.C * p.d_e;
+      float* Es = hs;  // p.d floats of dynamic LDS; C * d_e <= d is checked on the host
+      for (int i0 = 0; i0 < ne; i0 += 256 * 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = i0 + u * 256 + tid;
+          v[u] = i < ne ? tof(E[i]) : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = i0 + u * 256 + tid;
+          if (i < ne) Es[i] = v[u];
+        }
+      }
+      __syncthreads();
       if (j >= p.Hr) return;
       const T* w1 = static_cast<const T*>(p.W1) + j * W1s + p.d;
-      const T* E = static_cast<const T*>(p.E);
-      for (int c = 0; c < p.C; ++c) {
-        float acc = 0.f;
-        for (int m = lane; m < p.d_e; m += 64) acc += tof(w1[m]) * tof(E[static_cast<size_t>(c) * p.d_e + m]);
-        acc = wave_sum(acc);
-        if (lane == 0) p.F[j * p.C + c] = acc;
+      for (int m0 = 0; m0 < p.d_e; m0 += 64 * 4) {
+        float wv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int m = m0 + u * 64 + lane;
+          wv[u] = m < p.d_e ? tof(w1[m]) : 0.f;
+        }
+        for (int c = 0; c < p.C; ++c) {
+          float acc = 0.f;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int m = m0 + u * 64 + lane;
+            if (m < p.d_e) acc += wv[u] * Es[c * p.d_e + m];
+          }
+          acc = wave_sum(acc);
+          if (lane == 0) {
+            if (m0 == 0) p.F[j * p.C + c] = acc;
+            else p.F[j * p.C + c] += acc;
+          }
+        }
       }
     } else {
       if (j >= p.G) return;
@@ -131,6 +164,12 @@ __global__ __launch_bounds__(256) void k_route_proj(RouteParams p) {
   }
   const int b = blockIdx.x / nrb, j0 = (blockIdx.x % nrb) * 8;
   const float* hb = p.hbar + static_cast<size_t>(b) * p.d;
+  const bool vec = (p.d % (64 * VEC)) == 0;
+  // In the vector path lane L multiplies weights k = BK*i + VEC*L + e (one
+  // 16-byte load) with hbar[k]; hbar is stored lane-interleaved,
+  // hs[BK*i + 64*e + L], so those LDS reads hit consecutive banks.
+  constexpr int BK = 64 * VEC;
+  auto pos = [&](int k) { return vec ? (k / BK) * BK + (k % VEC) * 64 + (k % BK) / VEC : k; };
   {
     // stage hbar: all of a thread's loads issued before its LDS stores
     const rsrc_t r_hb = make_rsrc(hb, static_cast<uint32_t>(p.d) * 4u);
@@ -144,13 +183,18 @@ __global__ __launch_bounds__(256) void k_route_proj(RouteParams p) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int k = k0 + (u * 256 + tid) * 4;
-        if (k + 4 <= p.d) *reinterpret_cast<u32x4*>(hs + k) = v[u];
+        if (k + 4 <= p.d) {
+          const u32x4 x = v[u];
+          hs[pos(k)] = __uint_as_float(x.x);
+          hs[pos(k + 1)] = __uint_as_float(x.y);
+          hs[pos(k + 2)] = __uint_as_float(x.z);
+          hs[pos(k + 3)] = __uint_as_float(x.w);
+        }
       }
     }
-    for (int k = (p.d / 4) * 4 + tid; k < p.d; k += 256) hs[k] = hb[k];
+    for (int k = (p.d / 4) * 4 + tid; k < p.d; k += 256) hs[pos(k)] = hb[k];
   }
   __syncthreads();
-  const bool vec = (p.d % (64 * VEC)) == 0;
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
     const int j = j0 + 2 * wave + r;
@@ -169,14 +213,14 @@ __global__ __launch_bounds__(256) void k_route_proj(RouteParams p) {
     float acc = 0.f;
     if (vec && (reinterpret_cast<uintptr_t>(wrow) & 15) == 0) {
 #pragma unroll 8
-      for (int k = lane * VEC; k < p.d; k += 64 * VEC) {
-        const u32x4 raw = *reinterpret_cast<const u32x4*>(wrow + k);
+      for (int k0 = 0; k0 < p.d; k0 += BK) {
+        const u32x4 raw = *reinterpret_cast<const u32x4*>(wrow + k0 + lane * VEC);
         const T* v = reinterpret_cast<const T*>(&raw);
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) acc += tof(v[i]) * hs[k + i];
+        for (int i = 0; i < VEC; ++i) acc += tof(v[i]) * hs[k0 + 64 * i + lane];
       }
     } else {
-      for (int k = lane; k < p.d; k += 64) acc += tof(wrow[k]) * hs[k];
+      for (int k = lane; k < p.d; k += 64) acc += tof(wrow[k]) * hs[pos(k)];
     }
     acc = wave_sum(acc);
     if (lane == 0) p.cb[static_cast<size_t>(b) * nout + j] = scale * (acc + bias);
@@ -347,6 +391,7 @@ __global__ __launch_bounds__(256) void k_route_generic(RouteParams p) {
 // 16x16x32 bf16 MFMA with f32 accumulation. Weight chunks of 64 columns are
 // staged through LDS (double buffered) and shared by the four waves; each wave
 // streams the hidden states of its own 16 tokens straight into B fragments.
+// Loads run several chunks ahead through a ring of registers.
 // After the K loop lane (t, q) of a wave holds 36 outputs of token t:
 // hidden units 16m+4q+i (m < 8) and role logits 4q+i (m = 8). The epilogue
 // (role softmax, F a + cb, GELU, W2, selection) runs on those registers with
@@ -402,19 +447,22 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
 
   // Pieces r = 0..3 of this thread are rows < 128 of W1; piece 4 covers the
   // role rows (wave 0: rows 128..135, wave 1: 136..143); waves 2-3 have none.
-  u32x4 wr[5];
-  auto load_w = [&](int kc) {
+  // Chunks past the end load as zero.
+  const int nch = d / kRtKc;
+  auto load_w = [&](u32x4* wr, int c) {
+    const bool ok = c < nch;
+    const int kc = c * kRtKc;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int pc = tid + 256 * r;
       const int row = pc >> 3, c8 = pc & 7;
-      wr[r] = bload16(r_w1, static_cast<uint32_t>((row * W1s + kc + 8 * c8) * 2));
+      wr[r] = bload16(r_w1, ok ? static_cast<uint32_t>((row * W1s + kc + 8 * c8) * 2) : kOOB);
     }
     const int pc = tid + 1024;
     const int row = (pc >> 3) - Hr, c8 = pc & 7;
-    wr[4] = bload16(r_wr, (pc < kRtRows * 8 && row < C) ? static_cast<uint32_t>((row * d + kc + 8 * c8) * 2) : kOOB);
+    wr[4] = bload16(r_wr, (ok && pc < kRtRows * 8 && row < C) ? static_cast<uint32_t>((row * d + kc + 8 * c8) * 2) : kOOB);
   };
-  auto store_w = [&](int buf) {
+  auto store_w = [&](const u32x4* wr, int buf) {
 #pragma unroll
     for (int r = 0; r < 5; ++r) {
       const int pc = tid + 256 * r;
@@ -424,35 +472,48 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
       }
     }
   };
-  bf16x8 hb0, hb1;
-  auto load_h = [&](int kc) {
-    hb0 = __builtin_bit_cast(bf16x8, bload16(r_h, valid ? hoff + 2u * kc : kOOB));
-    hb1 = __builtin_bit_cast(bf16x8, bload16(r_h, valid ? hoff + 2u * kc + 64u : kOOB));
+  auto load_h = [&](u32x4* hr, int c) {
+    const bool ok = valid && c < nch;
+    hr[0] = bload16(r_h, ok ? hoff + 2u * c * kRtKc : kOOB);
+    hr[1] = bload16(r_h, ok ? hoff + 2u * c * kRtKc + 64u : kOOB);
   };
 
   f32x4 acc[9];
 #pragma unroll
   for (int m = 0; m < 9; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nch = d / kRtKc;
-  load_w(0);
-  load_h(0);
-  store_w(0);
-  for (int c = 0; c < nch; ++c) {
-    __syncthreads();
-    const bf16x8 h0 = hb0, h1 = hb1;
-    if (c + 1 < nch) {
-      load_w((c + 1) * kRtKc);
-      load_h((c + 1) * kRtKc);
-    }
-    const bf16* Wb = Ws[c & 1];
+  // Register ring: hidden-state chunks (HBM) are requested kDh chunks ahead,
+  // weight chunks (L2) kDw chunks ahead; weights pass through a double
+  // buffer in LDS shared by the four waves. The inner loop is fully unrolled
+  // so every ring slot is a fixed set of registers.
+  constexpr int kDh = 8, kDw = 4;
+  u32x4 hreg[kDh][2];
+  u32x4 wreg[kDw][5];
 #pragma unroll
-    for (int m = 0; m < 9; ++m) {
-      const bf16* ar = Wb + (16 * m + l16) * kRtLd + 8 * g4;
-      acc[m] = mfma_16x16x32(*reinterpret_cast<const bf16x8*>(ar), h0, acc[m]);
-      acc[m] = mfma_16x16x32(*reinterpret_cast<const bf16x8*>(ar + 32), h1, acc[m]);
+  for (int u = 0; u < kDw; ++u) load_w(wreg[u], u);
+#pragma unroll
+  for (int u = 0; u < kDh; ++u) load_h(hreg[u], u);
+  store_w(wreg[0], 0);
+  for (int c0 = 0; c0 < nch; c0 += kDh) {
+#pragma unroll
+    for (int u = 0; u < kDh; ++u) {
+      const int c = c0 + u;
+      if (c < nch) {
+        __syncthreads();
+        const bf16* Wb = Ws[c & 1];
+        const bf16x8 h0 = __builtin_bit_cast(bf16x8, hreg[u][0]);
+        const bf16x8 h1 = __builtin_bit_cast(bf16x8, hreg[u][1]);
+#pragma unroll
+        for (int m = 0; m < 9; ++m) {
+          const bf16* ar = Wb + (16 * m + l16) * kRtLd + 8 * g4;
+          acc[m] = mfma_16x16x32(*reinterpret_cast<const bf16x8*>(ar), h0, acc[m]);
+          acc[m] = mfma_16x16x32(*reinterpret_cast<const bf16x8*>(ar + 32), h1, acc[m]);
+        }
+        if (c + 1 < nch) store_w(wreg[(u + 1) % kDw], (c + 1) & 1);
+        load_w(wreg[u % kDw], c + kDw);
+        load_h(hreg[u], c + kDh);
+      }
     }
-    if (c + 1 < nch) store_w((c + 1) & 1);
   }
 
   // ---- epilogue: lanes l16, l16+16, l16+32, l16+48 hold token `tok`

@@ -40,8 +40,24 @@ hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s);
 size_t route_generic_shm(int d, int G, int C, int Hr, int kind);
 hipError_t launch_select(const RouteParams& p, hipStream_t s);
 
+struct RotateParams {
+  int ntok, T, H, G, tok_per_wg;
+  const void* v;
+  const void* R;
+  void* z;                  // rotate only
+  const uint32_t* mask;     // fused rotate + pack
+  const int32_t* offsets;
+  void* Vp;
+  int64_t cap;
+};
 hipError_t launch_rotate(bool bf16, int ntok, int H, int dh, const void* v, const void* R, void* z,
                          hipStream_t s);
+// Fused rotation + pack. Offsets must already hold the exclusive scan of the
+// kept counts.
+hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, const void* v, const void* R,
+                              const uint32_t* mask, const int32_t* offsets, void* Vp, int64_t cap,
+                              hipStream_t s);
+hipError_t launch_pack_offsets(int B, int T, int G, const uint32_t* mask, int32_t* offsets, hipStream_t s);
 
 hipError_t launch_pack(bool bf16, int B, int T, int H, int dh, int G, const void* z,
                        const uint32_t* mask, int32_t* offsets, void* Vp, int64_t cap,

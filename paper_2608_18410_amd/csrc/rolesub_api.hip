@@ -80,6 +80,27 @@ bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
   return x < y + nb && y < x + na;
 }
 
+// Packed-cache capacity against the budget (only when both are given).
+rolesub_status check_capacity(const rolesub_dims* dims, const rolesub_budget* budget, const int32_t* type_counts,
+                              int64_t cap_groups, const char* fn) {
+  if (!budget || !type_counts) return ROLESUB_OK;
+  rolesub_status st = check_budget(budget, dims->G, fn);
+  if (st) return st;
+  int64_t need = 0;
+  if (budget->mode == ROLESUB_BUDGET_TOPK) {
+    for (int t = 0; t < 4; ++t) {
+      if (type_counts[t] < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: type_counts[%d] < 0", fn, t);
+      need += static_cast<int64_t>(type_counts[t]) * std::min(budget->k_by_type[t], dims->G);
+    }
+  } else {
+    need = static_cast<int64_t>(dims->T) * std::min(budget->kmax, dims->G);
+  }
+  if (cap_groups < need)
+    return fail(ROLESUB_ERR_CAPACITY, "%s: cap_groups=%lld below the budget of %lld groups", fn,
+                static_cast<long long>(cap_groups), static_cast<long long>(need));
+  return ROLESUB_OK;
+}
+
 size_t route_ws_bytes(const rolesub_dims* d, const rolesub_router* r) {
   if (!d || !r || d->B <= 0) return 0;
   return align256(route_cb_floats(d->B, r->Hr, d->G, r->kind) * sizeof(float)) +
@@ -179,6 +200,8 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype, cons
       return fail(ROLESUB_ERR_INVALID_ARG, "%s: need d_e >= 1 and Hr >= 1", fn);
     if (!router->E || !router->W1 || !router->b1 || !router->W2 || !router->b2)
       return fail(ROLESUB_ERR_INVALID_ARG, "%s: MLP2 router weights are NULL", fn);
+    if (static_cast<int64_t>(router->C) * router->d_e > dims->d)
+      return fail(ROLESUB_ERR_UNSUPPORTED, "%s: C*d_e=%d exceeds d=%d", fn, router->C * router->d_e, dims->d);
   } else if (router->kind == ROLESUB_ROUTER_ADDITIVE) {
     if (!router->W_tok || !router->b_tok || !router->W_role || !router->W_lang || !router->b_lang)
       return fail(ROLESUB_ERR_INVALID_ARG, "%s: additive router weights are NULL", fn);
@@ -233,22 +256,8 @@ rolesub_status rolesub_pack_kv(const rolesub_dims* dims, rolesub_dtype dtype, co
   if (st) return st;
   if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
   if (cap_groups < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: cap_groups < 0", fn);
-  if (budget && type_counts) {
-    st = check_budget(budget, dims->G, fn);
-    if (st) return st;
-    int64_t need = 0;
-    if (budget->mode == ROLESUB_BUDGET_TOPK) {
-      for (int t = 0; t < 4; ++t) {
-        if (type_counts[t] < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: type_counts[%d] < 0", fn, t);
-        need += static_cast<int64_t>(type_counts[t]) * std::min(budget->k_by_type[t], dims->G);
-      }
-    } else {
-      need = static_cast<int64_t>(dims->T) * std::min(budget->kmax, dims->G);
-    }
-    if (cap_groups < need)
-      return fail(ROLESUB_ERR_CAPACITY, "%s: cap_groups=%lld below the budget of %lld groups", fn,
-                  static_cast<long long>(cap_groups), static_cast<long long>(need));
-  }
+  st = check_capacity(dims, budget, type_counts, cap_groups, fn);
+  if (st) return st;
   if (dims->B == 0) return ROLESUB_OK;
   if (!mask || !offsets || (dims->T > 0 && !z) || (cap_groups > 0 && dims->T > 0 && !Vp))
     return fail(ROLESUB_ERR_INVALID_ARG, "%s: z, mask, offsets and Vp must be non-NULL", fn);
@@ -258,6 +267,35 @@ rolesub_status rolesub_pack_kv(const rolesub_dims* dims, rolesub_dtype dtype, co
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: one sample's packed cache exceeds 2 GiB", fn);
   return from_hip(launch_pack(dtype == ROLESUB_BF16, dims->B, dims->T, dims->H, dims->dh, dims->G, z, mask,
                               offsets, Vp, cap_groups, static_cast<hipStream_t>(stream)),
+                  fn);
+}
+
+rolesub_status rolesub_rotate_pack(const rolesub_dims* dims, rolesub_dtype dtype, const rolesub_budget* budget,
+                                   const int32_t* type_counts, const void* v, const void* R,
+                                   const uint32_t* mask, int32_t* offsets, void* Vp, int64_t cap_groups,
+                                   void* stream) {
+  const char* fn = "rolesub_rotate_pack";
+  rolesub_status st = check_value_dims(dims, fn);
+  if (st) return st;
+  st = check_groups(dims, fn, true);
+  if (st) return st;
+  if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+  if (cap_groups < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: cap_groups < 0", fn);
+  st = check_capacity(dims, budget, type_counts, cap_groups, fn);
+  if (st) return st;
+  if (dims->B == 0) return ROLESUB_OK;
+  if (!mask || !offsets || (dims->T > 0 && (!v || !R)) || (cap_groups > 0 && dims->T > 0 && !Vp))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: v, R, mask, offsets and Vp must be non-NULL", fn);
+  if (static_cast<size_t>(dims->B) * dims->T > 0x7FFFFFFF)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
+  if (static_cast<size_t>(256) * dims->H * dims->dh * esize(dtype) >= kMaxRegion)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: too many heads", fn);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  rolesub_status r = from_hip(launch_pack_offsets(dims->B, dims->T, dims->G, mask, offsets, s), fn);
+  if (r) return r;
+  if (dims->T == 0) return ROLESUB_OK;
+  return from_hip(launch_rotate_pack(dtype == ROLESUB_BF16, dims->B, dims->T, dims->H, dims->dh, dims->G, v, R,
+                                     mask, offsets, Vp, cap_groups, s),
                   fn);
 }
 

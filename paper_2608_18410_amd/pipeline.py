@@ -32,14 +32,14 @@ class LayerBuffers:
     workspace: torch.Tensor
 
     @staticmethod
-    def allocate(B, T, H, dh, G, Tq, cap, dtype, out_dtype=None, ws_bytes=0, device="cuda"):
+    def allocate(B, T, H, dh, G, Tq, cap, dtype, out_dtype=None, ws_bytes=0, device="cuda", with_z=True):
         u8, i32, f32 = torch.uint8, torch.int32, torch.float32
         return LayerBuffers(
             mask=torch.empty((B, T), dtype=i32, device=device),
             idx=torch.empty((B, T, G), dtype=u8, device=device),
             count=torch.empty((B, T), dtype=u8, device=device),
             scores=torch.empty((B, T, G), dtype=f32, device=device),
-            z=torch.empty((B, T, H, dh), dtype=dtype, device=device),
+            z=torch.empty((B, T, H, dh) if with_z else (0,), dtype=dtype, device=device),
             offsets=torch.empty((B, T + 1), dtype=i32, device=device),
             Vp=torch.empty((B, H, cap, dh // G), dtype=dtype, device=device),
             out=torch.empty((B, Tq, H, dh), dtype=out_dtype or dtype, device=device),
@@ -48,13 +48,20 @@ class LayerBuffers:
 
 
 def run_layer(h, q, k, v, types, R, budget: rs.Budget, G: int, bufs: LayerBuffers,
-              router: rs.Router | None = None, scores_in=None, type_counts=None, stream=None):
-    """route -> rotate -> pack -> attend. Returns the buffers (filled asynchronously)."""
+              router: rs.Router | None = None, scores_in=None, type_counts=None, fused=True,
+              stream=None):
+    """route -> rotate -> pack -> attend. With fused=True rotation and pack run
+    as one call (rolesub_rotate_pack) and bufs.z is not written. Returns the
+    buffers (filled asynchronously)."""
     rs.route(types, budget, G, h=h, router=router, scores_in=scores_in, workspace=bufs.workspace,
              out={"mask": bufs.mask, "idx": bufs.idx, "count": bufs.count, "scores": bufs.scores},
              stream=stream)
-    rs.rotate_values(v, R, out=bufs.z, stream=stream)
-    rs.pack_kv(bufs.z, bufs.mask, G, bufs.Vp.shape[2], budget=budget, type_counts=type_counts,
-               out=(bufs.offsets, bufs.Vp), stream=stream)
+    if fused:
+        rs.rotate_pack(v, R, bufs.mask, G, bufs.Vp.shape[2], budget=budget, type_counts=type_counts,
+                       out=(bufs.offsets, bufs.Vp), stream=stream)
+    else:
+        rs.rotate_values(v, R, out=bufs.z, stream=stream)
+        rs.pack_kv(bufs.z, bufs.mask, G, bufs.Vp.shape[2], budget=budget, type_counts=type_counts,
+                   out=(bufs.offsets, bufs.Vp), stream=stream)
     rs.attend(q, k, bufs.mask, bufs.offsets, bufs.Vp, R, G, out=bufs.out, stream=stream)
     return bufs

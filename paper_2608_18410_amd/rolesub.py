@@ -23,7 +23,7 @@ MLP2, ADDITIVE = 0, 1
 EXPORTS = (
     "rolesub_status_str", "rolesub_last_error", "rolesub_version",
     "rolesub_rotate_values", "rolesub_route_workspace_size", "rolesub_route",
-    "rolesub_pack_kv", "rolesub_attend_workspace_size", "rolesub_attend",
+    "rolesub_pack_kv", "rolesub_rotate_pack", "rolesub_attend_workspace_size", "rolesub_attend",
 )
 
 
@@ -73,11 +73,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rolesub_route_workspace_size.restype = SZ
     lib.rolesub_route.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.rolesub_pack_kv.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, I64, P]
+    lib.rolesub_rotate_pack.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, I64, P]
     lib.rolesub_attend_workspace_size.argtypes = [P, I32]
     lib.rolesub_attend_workspace_size.restype = SZ
     lib.rolesub_attend.argtypes = [P, ctypes.c_int, I32, P, P, P, P, P, I64, P, ctypes.c_float, P,
                                    ctypes.c_int, P, SZ, P]
-    for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_attend"):
+    for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_rotate_pack",
+               "rolesub_attend"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -226,6 +228,22 @@ def pack_kv(z: torch.Tensor, mask: torch.Tensor, G: int, cap: int, budget: Budge
     _check("rolesub_pack_kv", load().rolesub_pack_kv(
         ctypes.byref(dims), _code(z), ctypes.byref(budget) if budget is not None else None, tc,
         _ptr(z), _ptr(mask), _ptr(offsets, torch.int32), _ptr(Vp, z.dtype), int(cap), _stream(stream)))
+    return offsets, Vp
+
+
+def rotate_pack(v: torch.Tensor, R: torch.Tensor, mask: torch.Tensor, G: int, cap: int,
+                budget: Budget | None = None, type_counts=None, out=None, stream=None):
+    """Rotation and pack in one pass (z is not materialised). Returns (offsets, Vp)."""
+    B, T, H, dh = v.shape
+    ds = dh // G
+    offsets = torch.empty((B, T + 1), dtype=torch.int32, device=v.device) if out is None else out[0]
+    Vp = torch.empty((B, H, cap, ds), dtype=v.dtype, device=v.device) if out is None else out[1]
+    dims = Dims(B, T, H, dh, G, 0)
+    tc = (ctypes.c_int32 * 4)(*type_counts) if type_counts is not None else None
+    _check("rolesub_rotate_pack", load().rolesub_rotate_pack(
+        ctypes.byref(dims), _code(v), ctypes.byref(budget) if budget is not None else None, tc,
+        _ptr(v), _ptr(R, v.dtype), _ptr(mask), _ptr(offsets, torch.int32), _ptr(Vp, v.dtype), int(cap),
+        _stream(stream)))
     return offsets, Vp
 
 
