@@ -60,6 +60,25 @@ __device__ __forceinline__ uint32_t clamp_bytes(size_t n) {
   return n < kOOB ? static_cast<uint32_t>(n) : kOOB;
 }
 
+// Asynchronous copy of 16 bytes per lane from a buffer resource into LDS:
+// lane i writes LDS bytes [lds_base + 16 i, lds_base + 16 i + 16); an
+// out-of-range offset writes zeros. The load is issued through inline
+// assembly so that the compiler does not serialise later LDS reads behind it;
+// the caller waits with wait_vmcnt<N>() before reading the data.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>((uintptr_t)((__attribute__((address_space(3))) const char*)p));
+}
+__device__ __forceinline__ void dma16(rsrc_t r, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(r)
+               : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
 // Group-selection order (top-K_i, Sec. 3.4): a larger score ranks first,
 // -0 and +0 are equal, NaN ranks after every number, equal keys go to the
 // lower group index.

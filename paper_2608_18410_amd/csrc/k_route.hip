@@ -388,27 +388,33 @@ __global__ __launch_bounds__(256) void k_route_generic(RouteParams p) {
 //
 // The token-independent product is computed transposed: for 64 tokens per
 // workgroup, [W1_h ; W_r] (144 x d, rows 128+C.. zero) times h^T (d x 64) on
-// 16x16x32 bf16 MFMA with f32 accumulation. Weight chunks of 64 columns are
-// staged through LDS (double buffered) and shared by the four waves; each wave
-// streams the hidden states of its own 16 tokens straight into B fragments.
-// Loads run several chunks ahead through a ring of registers.
-// After the K loop lane (t, q) of a wave holds 36 outputs of token t:
+// 16x16x32 bf16 MFMA with f32 accumulation. The operands stream through a
+// ring of kRtNB LDS stages, each holding one 64-column chunk of the 144
+// weight rows and of the 64 token rows. Stages are filled by asynchronous
+// LDS DMA (16 bytes per lane) issued kRtNB-1 chunks ahead, so about 100 KB
+// per workgroup is in flight without spending registers. Rows are stored with
+// their 16-byte pieces XOR-swizzled (piece c of row r at c ^ ((r >> 1) & 7)),
+// which makes the fragment reads of 16 consecutive rows conflict-free.
+// After the K loop lane (t, q) of wave w holds 36 outputs of token 16w + t:
 // hidden units 16m+4q+i (m < 8) and role logits 4q+i (m = 8). The epilogue
 // (role softmax, F a + cb, GELU, W2, selection) runs on those registers with
 // the four lanes of a token exchanging partial sums by cross-lane shuffles.
-constexpr int kRtTok = 64, kRtKc = 64, kRtRows = 144, kRtLd = kRtKc + 8;
+constexpr int kRtTok = 64, kRtKc = 64, kRtRows = 144, kRtNB = 5;
+constexpr int kRtWBytes = kRtRows * 128, kRtHBytes = kRtTok * 128, kRtStage = kRtWBytes + kRtHBytes;
+constexpr int kRtLoads = kRtRows / 8 + kRtTok / 8;  // 1 KB wave-loads per stage (26)
+
+__device__ __forceinline__ int rt_swz(int r) { return (r >> 1) & 7; }
 
 __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
-  __shared__ __attribute__((aligned(16))) bf16 Ws[2][kRtRows * kRtLd];
+  __shared__ __attribute__((aligned(16))) char ring[kRtNB * kRtStage];
   __shared__ __attribute__((aligned(16))) float Fs[128 * 16];
   __shared__ __attribute__((aligned(16))) bf16 W2s[32 * 128];
   __shared__ float b2s[32], brs[16];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
   const int d = p.d, C = p.C, G = p.G;
   constexpr int Hr = 128;
   const size_t W1s = 2 * static_cast<size_t>(d) + p.d_e;
-  const bf16* W1 = static_cast<const bf16*>(p.W1);
-  const bf16* Wr = static_cast<const bf16*>(p.W_r);
   {
     // stage F (Hr x C f32) and W2 (G x Hr bf16): loads first, then LDS stores
     const rsrc_t r_F = make_rsrc(p.F, static_cast<uint32_t>(Hr * C) * 4u);
@@ -438,83 +444,85 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
   const int tok0 = blockIdx.x * kRtTok;
   const int tok = tok0 + 16 * w + l16;
   const bool valid = tok < N;
-  // buffer resources: rows past the valid range load as zero with no memory access
+  const int nvalid = min(kRtTok, N - tok0);
   const rsrc_t r_h = make_rsrc(static_cast<const bf16*>(p.h) + static_cast<size_t>(tok0) * d,
-                               static_cast<uint32_t>(min(kRtTok, N - tok0)) * d * 2);
-  const rsrc_t r_w1 = make_rsrc(W1, static_cast<uint32_t>(Hr * W1s * 2));
-  const rsrc_t r_wr = make_rsrc(Wr, static_cast<uint32_t>(C) * d * 2);
-  const uint32_t hoff = static_cast<uint32_t>(16 * w + l16) * d * 2 + 16u * g4;
-
-  // Pieces r = 0..3 of this thread are rows < 128 of W1; piece 4 covers the
-  // role rows (wave 0: rows 128..135, wave 1: 136..143); waves 2-3 have none.
-  // Chunks past the end load as zero.
+                               static_cast<uint32_t>(nvalid) * d * 2);
+  const rsrc_t r_w1 = make_rsrc(p.W1, static_cast<uint32_t>(Hr * W1s * 2));
+  const rsrc_t r_wr = make_rsrc(p.W_r, static_cast<uint32_t>(C) * d * 2);
   const int nch = d / kRtKc;
-  auto load_w = [&](u32x4* wr, int c) {
-    const bool ok = c < nch;
-    const int kc = c * kRtKc;
+  const uint32_t ring_base = lds_addr(ring);
+
+  // This wave's wave-loads of a stage: j = w, w+4, ... < kRtLoads (7 for waves
+  // 0-1, 6 for waves 2-3). Load j < 18 brings weight rows 8j..8j+7 (W1 for
+  // j < 16, W_r rows for j = 16, 17), load j >= 18 token rows 8(j-18).. .
+  // Lane i carries row 8j + i/8, LDS piece i%8, global piece (i%8) ^ swizzle.
+  const int nld = (kRtLoads - w + 3) / 4;
+  uint32_t base_off[7];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int pc = tid + 256 * r;
-      const int row = pc >> 3, c8 = pc & 7;
-      wr[r] = bload16(r_w1, ok ? static_cast<uint32_t>((row * W1s + kc + 8 * c8) * 2) : kOOB);
+  for (int u = 0; u < 7; ++u) {
+    const int jj = w + 4 * u;
+    const int ri = lane >> 3, piece = lane & 7;
+    uint32_t off = kOOB;
+    if (jj < 16) {
+      const int r = 8 * jj + ri;
+      off = static_cast<uint32_t>((r * W1s + 8 * (piece ^ rt_swz(r))) * 2);
+    } else if (jj < 18) {
+      const int r = 8 * jj + ri, rr = r - Hr;
+      if (rr < C) off = static_cast<uint32_t>((rr * d + 8 * (piece ^ rt_swz(r))) * 2);
+    } else if (jj < kRtLoads) {
+      const int t = 8 * (jj - 18) + ri;
+      if (t < nvalid) off = static_cast<uint32_t>((t * d + 8 * (piece ^ rt_swz(t))) * 2);
     }
-    const int pc = tid + 1024;
-    const int row = (pc >> 3) - Hr, c8 = pc & 7;
-    wr[4] = bload16(r_wr, (ok && pc < kRtRows * 8 && row < C) ? static_cast<uint32_t>((row * d + kc + 8 * c8) * 2) : kOOB);
-  };
-  auto store_w = [&](const u32x4* wr, int buf) {
+    base_off[u] = off;
+  }
+  // Wave-loads u = 0..3 are always W1 rows (j <= 15); u = 4 is W_r rows for
+  // waves 0-1 and token rows for waves 2-3; u = 5, 6 are token rows. Each call
+  // site below uses one fixed buffer resource so it stays in scalar registers.
+  auto issue = [&](int c) {
+    const uint32_t sbase = ring_base + (c % kRtNB) * kRtStage;
+    const bool ok = c < nch;  // chunks past the end are all-out-of-range dummies
+    const uint32_t kb = static_cast<uint32_t>(c) * kRtKc * 2;
+    auto off = [&](int u) { return (ok && base_off[u] != kOOB) ? base_off[u] + kb : kOOB; };
+    auto dst = [&](int u) {
+      const int jj = w + 4 * u;
+      return sbase + (jj < 18 ? jj * 1024 : kRtWBytes + (jj - 18) * 1024);
+    };
 #pragma unroll
-    for (int r = 0; r < 5; ++r) {
-      const int pc = tid + 256 * r;
-      if (pc < kRtRows * 8) {
-        const int row = pc >> 3, c8 = pc & 7;
-        *reinterpret_cast<u32x4*>(&Ws[buf][row * kRtLd + 8 * c8]) = wr[r];
-      }
-    }
-  };
-  auto load_h = [&](u32x4* hr, int c) {
-    const bool ok = valid && c < nch;
-    hr[0] = bload16(r_h, ok ? hoff + 2u * c * kRtKc : kOOB);
-    hr[1] = bload16(r_h, ok ? hoff + 2u * c * kRtKc + 64u : kOOB);
+    for (int u = 0; u < 4; ++u) dma16(r_w1, off(u), dst(u));
+    if (w < 2) dma16(r_wr, off(4), dst(4));
+    else dma16(r_h, off(4), dst(4));
+    dma16(r_h, off(5), dst(5));
+    if (w < 2) dma16(r_h, off(6), dst(6));
   };
 
   f32x4 acc[9];
 #pragma unroll
   for (int m = 0; m < 9; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Register ring: hidden-state chunks (HBM) are requested kDh chunks ahead,
-  // weight chunks (L2) kDw chunks ahead; weights pass through a double
-  // buffer in LDS shared by the four waves. The inner loop is fully unrolled
-  // so every ring slot is a fixed set of registers.
-  constexpr int kDh = 8, kDw = 4;
-  u32x4 hreg[kDh][2];
-  u32x4 wreg[kDw][5];
 #pragma unroll
-  for (int u = 0; u < kDw; ++u) load_w(wreg[u], u);
+  for (int c = 0; c < kRtNB - 1; ++c) issue(c);
+  for (int c = 0; c < nch; ++c) {
+    // chunk c has landed once at most (kRtNB - 2) younger stages are pending
+    if (nld == 7) wait_vmcnt<7 * (kRtNB - 2)>();
+    else wait_vmcnt<6 * (kRtNB - 2)>();
+    __syncthreads();
+    const char* st = ring + (c % kRtNB) * kRtStage;
+    const int th = 16 * w + l16;
+    bf16x8 hb[2];
 #pragma unroll
-  for (int u = 0; u < kDh; ++u) load_h(hreg[u], u);
-  store_w(wreg[0], 0);
-  for (int c0 = 0; c0 < nch; c0 += kDh) {
+    for (int ks = 0; ks < 2; ++ks)
+      hb[ks] = *reinterpret_cast<const bf16x8*>(st + kRtWBytes + th * 128 + 16 * ((4 * ks + g4) ^ rt_swz(th)));
 #pragma unroll
-    for (int u = 0; u < kDh; ++u) {
-      const int c = c0 + u;
-      if (c < nch) {
-        __syncthreads();
-        const bf16* Wb = Ws[c & 1];
-        const bf16x8 h0 = __builtin_bit_cast(bf16x8, hreg[u][0]);
-        const bf16x8 h1 = __builtin_bit_cast(bf16x8, hreg[u][1]);
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int m = 0; m < 9; ++m) {
-          const bf16* ar = Wb + (16 * m + l16) * kRtLd + 8 * g4;
-          acc[m] = mfma_16x16x32(*reinterpret_cast<const bf16x8*>(ar), h0, acc[m]);
-          acc[m] = mfma_16x16x32(*reinterpret_cast<const bf16x8*>(ar + 32), h1, acc[m]);
-        }
-        if (c + 1 < nch) store_w(wreg[(u + 1) % kDw], (c + 1) & 1);
-        load_w(wreg[u % kDw], c + kDw);
-        load_h(hreg[u], c + kDh);
+      for (int m = 0; m < 9; ++m) {
+        const int r = 16 * m + l16;
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(st + r * 128 + 16 * ((4 * ks + g4) ^ rt_swz(r)));
+        acc[m] = mfma_16x16x32(a, hb[ks], acc[m]);
       }
-    }
+    issue(c + kRtNB - 1);  // refills the stage read in the previous iteration
   }
+  wait_vmcnt<0>();  // trailing dummy loads land before the LDS is released
 
   // ---- epilogue: lanes l16, l16+16, l16+32, l16+48 hold token `tok`
   const int b = valid ? tok / p.T : 0;
