@@ -107,8 +107,27 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// GELU(x) = x Phi(x) = x erfc(-x / sqrt 2) / 2, the exact (erf-based) form.
+// erfc is evaluated without branches with the Chebyshev-fitted approximation
+// of Numerical Recipes (erfcc; fractional error below 1.2e-7 for z >= 0),
+// erfc(z) = t exp(-z^2 + P(t)) with t = 1 / (1 + z/2), and erfc(-z) =
+// 2 - erfc(z). A branch-free form matters here: a divergent branch inside the
+// per-hidden-unit loop of the router epilogue serialises its LDS reads.
 __device__ __forceinline__ float gelu_exact(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+  const float z = fabsf(x) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(1.f + 0.5f * z);
+  float P = 0.17087277f;
+  P = fmaf(P, t, -0.82215223f);
+  P = fmaf(P, t, 1.48851587f);
+  P = fmaf(P, t, -1.13520398f);
+  P = fmaf(P, t, 0.27886807f);
+  P = fmaf(P, t, -0.18628806f);
+  P = fmaf(P, t, 0.09678418f);
+  P = fmaf(P, t, 0.37409196f);
+  P = fmaf(P, t, 1.00002368f);
+  P = fmaf(P, t, -1.26551223f);
+  const float ec = t * expf(fmaf(-z, z, P));
+  return 0.5f * x * (x >= 0.f ? 2.f - ec : ec);
 }
 
 // Workgroup-to-XCD placement: consecutive workgroup ids go round-robin to the

@@ -405,46 +405,59 @@ constexpr int kRtLoads = kRtRows / 8 + kRtTok / 8;  // 1 KB wave-loads per stage
 
 __device__ __forceinline__ int rt_swz(int r) { return (r >> 1) & 7; }
 
+// Epilogue operands, written into the (then idle) ring after the K loop:
+// F zero-padded to 16 role columns and W2 transposed to [Hr][GP], both with a
+// row stride of 4 extra floats so that the 4 rows read by one instruction
+// (lanes of one token quarter share a row) fall on distinct LDS banks.
+constexpr int kFsStride = 20;
+
+template <int GP>
 __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
+  constexpr int Hr = 128, kW2Stride = GP + 4;
+  static_assert(Hr * (kFsStride + kW2Stride) * 4 <= kRtNB * kRtStage, "epilogue tiles fit the ring");
   __shared__ __attribute__((aligned(16))) char ring[kRtNB * kRtStage];
-  __shared__ __attribute__((aligned(16))) float Fs[128 * 16];
-  __shared__ __attribute__((aligned(16))) bf16 W2s[32 * 128];
-  __shared__ float b2s[32], brs[16];
+  __shared__ float b2s[GP], brs[16];
   const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
   const int d = p.d, C = p.C, G = p.G;
-  constexpr int Hr = 128;
   const size_t W1s = 2 * static_cast<size_t>(d) + p.d_e;
-  {
-    // stage F (Hr x C f32) and W2 (G x Hr bf16): loads first, then LDS stores
-    const rsrc_t r_F = make_rsrc(p.F, static_cast<uint32_t>(Hr * C) * 4u);
-    const rsrc_t r_W2 = make_rsrc(p.W2, static_cast<uint32_t>(G * Hr) * 2u);
-    u32x4 f[2], w2[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int i = (u * 256 + tid) * 4;  // floats of F
-      f[u] = bload16(r_F, i < Hr * C ? 4u * i : kOOB);
-      const int j = (u * 256 + tid) * 8;  // bf16 of W2
-      w2[u] = bload16(r_W2, j < G * Hr ? 2u * j : kOOB);
-    }
-    const float b2v = tid < G ? tof(static_cast<const bf16*>(p.b2)[tid]) : 0.f;
-    const float brv = tid < C ? tof(static_cast<const bf16*>(p.b_r)[tid]) : 0.f;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int i = (u * 256 + tid) * 4;
-      if (i < Hr * C) *reinterpret_cast<u32x4*>(Fs + i) = f[u];
-      const int j = (u * 256 + tid) * 8;
-      if (j < G * Hr) *reinterpret_cast<u32x4*>(W2s + j) = w2[u];
-    }
-    if (tid < G) b2s[tid] = b2v;
-    if (tid < C) brs[tid] = brv;
-  }
 
   const int N = p.B * p.T;
   const int tok0 = blockIdx.x * kRtTok;
   const int tok = tok0 + 16 * w + l16;
   const bool valid = tok < N;
   const int nvalid = min(kRtTok, N - tok0);
+  const int b = valid ? tok / p.T : 0;
+  const int type = p.types[valid ? tok : 0];
+
+  // Epilogue operands are loaded now and held in registers through the K
+  // loop: F (entry e = j*16 + c), W2 transposed (entry e = s*Hr + j) and this
+  // lane's 32 per-sample language terms cb[b][16m + 4q + i].
+  float fv[8], w2v[GP / 2], cbv[32];
+  {
+    const rsrc_t r_F = make_rsrc(p.F, static_cast<uint32_t>(Hr * C) * 4u);
+    const rsrc_t r_W2 = make_rsrc(p.W2, static_cast<uint32_t>(G * Hr) * 2u);
+    const rsrc_t r_cb = make_rsrc(p.cb, static_cast<uint32_t>(p.B * Hr) * 4u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = u * 256 + tid, j = e >> 4, c = e & 15;
+      fv[u] = __uint_as_float(bload4(r_F, c < C ? 4u * (j * C + c) : kOOB));
+    }
+#pragma unroll
+    for (int u = 0; u < GP / 2; ++u) {
+      const int e = u * 256 + tid, sg = e >> 7, j = e & 127;
+      const uint32_t x = bload4(r_W2, sg < G ? 4u * ((sg * Hr + j) >> 1) : kOOB);
+      w2v[u] = __uint_as_float((j & 1) ? (x & 0xffff0000u) : (x << 16));
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        cbv[4 * m + i] = __uint_as_float(bload4(r_cb, 4u * (b * Hr + 16 * m + 4 * g4 + i)));
+    if (tid < GP) b2s[tid] = tid < G ? tof(static_cast<const bf16*>(p.b2)[tid]) : 0.f;
+    if (tid < 16) brs[tid] = tid < C ? tof(static_cast<const bf16*>(p.b_r)[tid]) : 0.f;
+  }
+
   const rsrc_t r_h = make_rsrc(static_cast<const bf16*>(p.h) + static_cast<size_t>(tok0) * d,
                                static_cast<uint32_t>(nvalid) * d * 2);
   const rsrc_t r_w1 = make_rsrc(p.W1, static_cast<uint32_t>(Hr * W1s * 2));
@@ -523,15 +536,30 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
     issue(c + kRtNB - 1);  // refills the stage read in the previous iteration
   }
   wait_vmcnt<0>();  // trailing dummy loads land before the LDS is released
+  __syncthreads();  // every wave is done with the ring
 
-  // ---- epilogue: lanes l16, l16+16, l16+32, l16+48 hold token `tok`
-  const int b = valid ? tok / p.T : 0;
-  const int type = valid ? p.types[tok] : 0;
+  float* Fs = reinterpret_cast<float*>(ring);
+  float* W2t = Fs + Hr * kFsStride;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int e = u * 256 + tid;
+    Fs[(e >> 4) * kFsStride + (e & 15)] = fv[u];
+  }
+#pragma unroll
+  for (int u = 0; u < GP / 2; ++u) {
+    const int e = u * 256 + tid;
+    W2t[(e & 127) * kW2Stride + (e >> 7)] = w2v[u];
+  }
+  __syncthreads();
+
+  // ---- epilogue: lanes l16, l16+16, l16+32, l16+48 hold token `tok`;
+  // lane quarter q = g4 owns hidden units 16m + 4q + i and role logits 4q + i.
   float ex[4], mx = -INFINITY;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int c = 4 * g4 + i;
-    ex[i] = c < C ? acc[8][i] + brs[c] : -INFINITY;
+    const float lg = acc[8][i] + brs[c];
+    ex[i] = c < C ? lg : -INFINITY;
     mx = fmaxf(mx, ex[i]);
   }
   mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
@@ -539,73 +567,97 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
   float sm = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    ex[i] = (4 * g4 + i < C) ? expf(ex[i] - mx) : 0.f;
+    const float e = expf(ex[i] - mx);
+    ex[i] = (4 * g4 + i < C) ? e : 0.f;
     sm += ex[i];
   }
   sm += __shfl_xor(sm, 16, kWave);
   sm += __shfl_xor(sm, 32, kWave);
   const float isum = 1.f / sm;
-  float a[16];
+  float a[16];  // role mixture weights; zero past C
 #pragma unroll
   for (int c = 0; c < 16; ++c) a[c] = __shfl(ex[c & 3], l16 + 16 * (c >> 2), kWave) * isum;
 
-  const float* cb = p.cb + static_cast<size_t>(b) * Hr;
-  float gam[32];
+  float gam[GP];
 #pragma unroll
-  for (int s = 0; s < 32; ++s) gam[s] = 0.f;
+  for (int s = 0; s < GP; ++s) gam[s] = 0.f;
 #pragma unroll
   for (int m = 0; m < 8; ++m) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = 16 * m + 4 * g4 + i;
-      float x = acc[m][i] + cb[j];
+      float x = acc[m][i] + cbv[4 * m + i];
+      const f32x4* fr = reinterpret_cast<const f32x4*>(Fs + j * kFsStride);
 #pragma unroll
-      for (int c = 0; c < 16; ++c)
-        if (c < C) x += Fs[j * C + c] * a[c];
+      for (int c4 = 0; c4 < 4; ++c4) {
+        const f32x4 f = fr[c4];
+        x += f[0] * a[4 * c4];
+        x += f[1] * a[4 * c4 + 1];
+        x += f[2] * a[4 * c4 + 2];
+        x += f[3] * a[4 * c4 + 3];
+      }
       const float gl = gelu_exact(x);
+      const f32x4* wr = reinterpret_cast<const f32x4*>(W2t + j * kW2Stride);
 #pragma unroll
-      for (int s = 0; s < 32; ++s)
-        if (s < G) gam[s] += tof(W2s[s * Hr + j]) * gl;
+      for (int s4 = 0; s4 < GP / 4; ++s4) {
+        const f32x4 w2 = wr[s4];
+        gam[4 * s4] += w2[0] * gl;
+        gam[4 * s4 + 1] += w2[1] * gl;
+        gam[4 * s4 + 2] += w2[2] * gl;
+        gam[4 * s4 + 3] += w2[3] * gl;
+      }
     }
   }
   int n_above = 0;
 #pragma unroll
-  for (int s = 0; s < 32; ++s) {
-    if (s < G) {
-      gam[s] += __shfl_xor(gam[s], 16, kWave);
-      gam[s] += __shfl_xor(gam[s], 32, kWave);
-      gam[s] += b2s[s];
-      n_above += gam[s] > p.tau;
-    }
+  for (int s = 0; s < GP; ++s) {
+    gam[s] += __shfl_xor(gam[s], 16, kWave);
+    gam[s] += __shfl_xor(gam[s], 32, kWave);
+    gam[s] += b2s[s];
+    n_above += static_cast<int>((s < G) & (gam[s] > p.tau));
   }
-  // the four lanes of a token now hold bitwise-identical scores
+  // the four lanes of a token now hold bitwise-identical scores; lane quarter
+  // q ranks groups s = 4u + q
+  // (a bitwise blend: a select chain on q gets turned into an indexed access,
+  // which would move gam to scratch memory)
+  float mine[GP / 4];
+  uint32_t qsel[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) qsel[q] = g4 == q ? ~0u : 0u;
+#pragma unroll
+  for (int u = 0; u < GP / 4; ++u) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v |= qsel[q] & __float_as_uint(gam[4 * u + q]);
+    mine[u] = __uint_as_float(v);
+  }
   const int K = budget_k(p.mode, p.k_by_type, type, p.tau, p.kmin, p.kmax, G, n_above);
-  uint32_t m = 0;
+  uint32_t msk = 0;
   if (p.mode == 1 && K == n_above) {
 #pragma unroll
-    for (int s = 0; s < 32; ++s)
-      if (s < G && gam[s] > p.tau) m |= 1u << s;
+    for (int s = 0; s < GP; ++s) msk |= static_cast<uint32_t>((s < G) & (gam[s] > p.tau)) << s;
   } else {
 #pragma unroll
-    for (int s = 0; s < 32; ++s) {
-      if (s < G && (s & 3) == g4) {
-        int rank = 0;
+    for (int u = 0; u < GP / 4; ++u) {
+      const int s = 4 * u + g4;
+      int rank = 0;
 #pragma unroll
-        for (int t = 0; t < 32; ++t)
-          if (t < G) rank += key_above(gam[t], gam[s]) || (t < s && key_equal(gam[t], gam[s]));
-        if (rank < K) m |= 1u << s;
-      }
+      for (int t = 0; t < GP; ++t)
+        rank += static_cast<int>((t < G) & (key_above(gam[t], mine[u]) | ((t < s) & key_equal(gam[t], mine[u]))));
+      msk |= static_cast<uint32_t>((s < G) & (rank < K)) << s;
     }
-    m |= __shfl_xor(m, 16, kWave);
-    m |= __shfl_xor(m, 32, kWave);
+    msk |= __shfl_xor(msk, 16, kWave);
+    msk |= __shfl_xor(msk, 32, kWave);
   }
   if (valid) {
     if (p.scores_out) {
 #pragma unroll
-      for (int s = 0; s < 32; ++s)
-        if (s < G && (s & 3) == g4) p.scores_out[static_cast<size_t>(tok) * G + s] = gam[s];
+      for (int u = 0; u < GP / 4; ++u) {
+        const int s = 4 * u + g4;
+        if (s < G) p.scores_out[static_cast<size_t>(tok) * G + s] = mine[u];
+      }
     }
-    if (g4 == 0) write_selection(p, tok, m);
+    if (g4 == 0) write_selection(p, tok, msk);
   }
 }
 
@@ -636,7 +688,9 @@ hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s) {
                        p.G <= 32 && p.d % kRtKc == 0 && ntok < (1u << 30);
   if (mfma_ok) {
     const unsigned nblk = static_cast<unsigned>((ntok + kRtTok - 1) / kRtTok);
-    hipLaunchKernelGGL(k_route_mlp2_bf16, dim3(nblk), dim3(256), 0, s, p);
+    if (p.G <= 8) hipLaunchKernelGGL(k_route_mlp2_bf16<8>, dim3(nblk), dim3(256), 0, s, p);
+    else if (p.G <= 16) hipLaunchKernelGGL(k_route_mlp2_bf16<16>, dim3(nblk), dim3(256), 0, s, p);
+    else hipLaunchKernelGGL(k_route_mlp2_bf16<32>, dim3(nblk), dim3(256), 0, s, p);
   } else {
     const int nmain = p.kind == 0 ? p.Hr : p.G;
     const size_t shm = sizeof(float) * (static_cast<size_t>(p.d) + nmain + p.C +
