@@ -56,6 +56,14 @@ __device__ __forceinline__ u32x2 bload8(rsrc_t r, uint32_t off) {
 __device__ __forceinline__ uint32_t bload4(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b32(r, static_cast<int>(off), 0, 0);
 }
+// Offset v for lanes with ok, else kOOB. The empty asm pins v as computed
+// unconditionally: otherwise the compiler may move an expensive operand (a
+// division, a 64-bit product) under a branch, and a branch around memory
+// operations makes later waits cover every outstanding one.
+__device__ __forceinline__ uint32_t oob_unless(bool ok, uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return ok ? v : kOOB;
+}
 __device__ __forceinline__ uint32_t clamp_bytes(size_t n) {
   return n < kOOB ? static_cast<uint32_t>(n) : kOOB;
 }

@@ -6,21 +6,46 @@ namespace rolesub {
 namespace {
 
 // bf16 matrix-core rotation. Each workgroup owns one head h and a contiguous
-// run of tokens (flattened over samples). The product is computed transposed,
-// Z^T = R_h^T V^T, so the streamed operand (the values, 16 B per lane straight
-// from HBM) is the MFMA B fragment and every lane ends up with 4 consecutive
-// outputs of its token. R_h^T lives in LDS (staged once per workgroup) and
-// its fragments are read from there per tile, which keeps the register count
-// low: occupancy, not software pipelining, hides the memory latency.
-// Workgroups of one head are placed on one XCD so R_h stays in its L2.
+// run of tokens (flattened over samples); each wave takes 16-token tiles. The
+// product is computed transposed, Z^T = R_h^T V^T, so the streamed operand
+// (the values, 16 B per lane straight from HBM) is the MFMA B fragment and
+// every lane ends up with 4 consecutive outputs of its token. R_h^T lives in
+// LDS (staged once per workgroup, 16-byte chunks XOR-swizzled by row so that
+// fragment reads are conflict-free) and its fragments are read per tile,
+// which keeps the register count low. Workgroups of one head are placed on
+// one XCD so R_h stays in its L2.
 //
-// PACK = false writes z. PACK = true writes only the kept groups into the
-// compact cache (the kept groups of M z, Sec. 3.2) at the slots given by the
-// offsets, so z never reaches memory.
-template <int DH, bool PACK>
+// A tile's results are not stored from the MFMA layout (8 bytes per lane,
+// scattered over 16 tokens): such partial-line writes run at about two thirds
+// of the bandwidth of contiguous ones. They are first written to a per-wave
+// LDS tile in output order and then copied out with consecutive lanes on
+// consecutive 16-byte units.
+//
+// OUT = kZ writes z (16 rows of dh values). The pack modes write only the
+// kept groups into the compact cache (the kept groups of M z, Sec. 3.2) at
+// the slots given by the offsets, so z never reaches memory; the tile then
+// holds the tile's slots in cache order and a slot -> token table. The copy
+// unit is 16 bytes (kPack16, ds >= 8), 8 bytes (kPack8, ds = 4) or 4 bytes
+// (kPack4, ds = 2), never wider than a slot.
+enum RotOut { kZ = 0, kPack16 = 1, kPack8 = 2, kPack4 = 3 };
+
+template <int DH>
+__device__ __forceinline__ int rt_chunk_swz(int j) {
+  // 16-byte chunk permutation of R^T row j: rows of 256 B (dh = 128) use j mod
+  // 16; rows of 128 B (dh = 64) share a bank line in pairs, so j/2 mod 8
+  return DH == 128 ? (j & 15) : ((j >> 1) & 7);
+}
+
+template <int DH, int OUT>
 __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
-  constexpr int MT = DH / 16, KS = DH / 32, LD = DH + 8;
-  __shared__ __attribute__((aligned(16))) bf16 Rt[DH * LD];  // Rt[j][k] = R[k][j]
+  constexpr bool PACK = OUT != kZ;
+  constexpr int MT = DH / 16, KS = DH / 32;
+  constexpr int U = OUT == kPack4 ? 4 : (OUT == kPack8 ? 8 : 16);  // copy-out unit, bytes
+  constexpr int NSLOT = PACK ? 16 * 32 : 1;  // slots of one tile: 16 tokens x G <= 32
+  __shared__ __attribute__((aligned(16))) bf16 Rt[DH * DH];  // Rt[j][k] = R[k][j], swizzled
+  __shared__ __attribute__((aligned(16))) bf16 Ost[4][16 * DH];  // per-wave output tile
+  __shared__ uint8_t Otok[4][NSLOT];                           // slot -> token of the tile
+  __shared__ int32_t Obase[4][PACK ? 16 : 1], Opre[4][PACK ? 16 : 1];
   const int H = p.H, ntok = p.ntok;
   int h, chunk;
   xcd_split(blockIdx.x, H, h, chunk);
@@ -30,7 +55,7 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
     // Transposed staging. An item is (row pair p, 8-column chunk jc): rows 2p
     // and 2p+1 of R_h are read 16 bytes each and written as 8 dwords
     // Rt[jc*8+e][2p..2p+1]; consecutive lanes take consecutive p, so each
-    // store instruction fills consecutive dwords of one LDS row.
+    // store instruction fills distinct dwords of one LDS row.
     constexpr int NPAIR = DH / 2, NCH = DH / 8, NI = NPAIR * NCH / 256;
     uint32_t* Rt32 = reinterpret_cast<uint32_t*>(Rt);
     u32x4 lo[NI], hi[NI];
@@ -47,8 +72,13 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       const int pr = it % NPAIR, jc = it / NPAIR;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        Rt32[(8 * jc + 2 * q) * (LD / 2) + pr] = (lo[r][q] & 0xFFFFu) | (hi[r][q] << 16);
-        Rt32[(8 * jc + 2 * q + 1) * (LD / 2) + pr] = (lo[r][q] >> 16) | (hi[r][q] & 0xFFFF0000u);
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int j = 8 * jc + 2 * q + e;  // row of R^T = column of R
+          const uint32_t d = e == 0 ? ((lo[r][q] & 0xFFFFu) | (hi[r][q] << 16))
+                                    : ((lo[r][q] >> 16) | (hi[r][q] & 0xFFFF0000u));
+          Rt32[j * (DH / 2) + (((pr >> 2) ^ rt_chunk_swz<DH>(j)) << 2) + (pr & 3)] = d;
+        }
       }
     }
   }
@@ -62,35 +92,41 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
                                static_cast<uint32_t>(t_end - t_begin - 1) * tstride + DH * 2);
   // PACK: group masks and cache offsets of the run's tokens
   const rsrc_t r_m = make_rsrc(p.mask + t_begin, static_cast<uint32_t>(t_end - t_begin) * 4u);
+  // rotate only: this run's rows of z
+  const rsrc_t r_z = make_rsrc(static_cast<bf16*>(p.z) + (static_cast<size_t>(t_begin) * H + h) * DH,
+                               PACK ? 0u : static_cast<uint32_t>(t_end - t_begin - 1) * tstride + DH * 2);
+  // offsets are [B][T+1]: token (b, t) sits at b*(T+1)+t
+  const rsrc_t r_o = make_rsrc(p.offsets, PACK ? static_cast<uint32_t>(ntok + ntok / max(p.T, 1)) * 4u : 0u);
   const uint32_t gm = p.G >= 32 ? 0xFFFFFFFFu : ((1u << p.G) - 1u);
   const int ds = DH / p.G;
+  // G divides dh (a power of two), so ds is one too: shifts, no divisions
+  const int lds = __builtin_ctz(ds);
+  const int cap32 = static_cast<int>(p.cap);  // < 2^31: the cache per (sample, head) is < 2 GiB
+  bf16* ost = Ost[w];
+  char* ostb = reinterpret_cast<char*>(ost);
 
-  bf16x8 nxt[KS];
-  uint32_t nmask = 0;
-  int32_t noff = 0;
-  auto load = [&](int tt) {
+  struct Tile {
+    bf16x8 v[KS];
+    uint32_t mask;
+    int32_t off;
+  };
+  // Loads are unconditional (rows past the run read as zeros through the
+  // buffer bounds): a branch around them makes later waits cover every
+  // outstanding memory operation.
+  auto load = [&](Tile& x, int tt) {
     const int tok = tt + l16;
     const bool ok = tok < t_end;
     const uint32_t o = static_cast<uint32_t>(tok - t_begin) * tstride + 16u * g4;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) nxt[ks] = __builtin_bit_cast(bf16x8, bload16(r_v, ok ? o + 64u * ks : kOOB));
+    for (int ks = 0; ks < KS; ++ks) x.v[ks] = __builtin_bit_cast(bf16x8, bload16(r_v, oob_unless(ok, o + 64u * ks)));
+    x.mask = 0;
+    x.off = 0;
     if constexpr (PACK) {
-      nmask = bload4(r_m, ok ? 4u * (tok - t_begin) : kOOB);
-      // offsets are [B][T+1]: token (b, t) sits at b*(T+1)+t
-      const int tk = ok ? tok : t_begin;
-      const int b = tk / p.T;
-      noff = p.offsets[static_cast<size_t>(tk) + b];
+      x.mask = bload4(r_m, oob_unless(ok, 4u * (tok - t_begin)));
+      x.off = static_cast<int32_t>(bload4(r_o, oob_unless(ok, 4u * (tok + tok / p.T))));
     }
   };
-  int t0 = t_begin + 16 * w;
-  if (t0 < t_end) load(t0);
-  for (; t0 < t_end; t0 += 64) {
-    bf16x8 cur[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) cur[ks] = nxt[ks];
-    const uint32_t cmask = nmask & gm;
-    const int32_t coff = noff;
-    if (t0 + 64 < t_end) load(t0 + 64);
+  auto process = [&](const Tile& x, int tt) {
     // keep the R^T fragments in LDS: without this the compiler hoists the
     // loop-invariant LDS reads into ~128 registers and occupancy collapses
     asm volatile("" ::: "memory");
@@ -98,55 +134,125 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int j = 16 * m + l16;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(Rt + (16 * m + l16) * LD + 32 * ks + 8 * g4);
-        acc[m] = mfma_16x16x32(a, cur[ks], acc[m]);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(Rt + j * DH + 8 * ((4 * ks + g4) ^ rt_chunk_swz<DH>(j)));
+        acc[m] = mfma_16x16x32(a, x.v[ks], acc[m]);
       }
     }
-    const int tok = t0 + l16;
-    if (tok < t_end) {
-      if constexpr (!PACK) {
-        bf16* zr = static_cast<bf16*>(p.z) + (static_cast<size_t>(tok) * H + h) * DH + 4 * g4;
+    if constexpr (!PACK) {
+      // tile row r = token tt + r; 16-byte chunk c of row r at c ^ (r mod NC)
+      constexpr int NC = DH / 8;
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-          bf16x4 o;
-          o[0] = static_cast<bf16>(acc[m][0]);
-          o[1] = static_cast<bf16>(acc[m][1]);
-          o[2] = static_cast<bf16>(acc[m][2]);
-          o[3] = static_cast<bf16>(acc[m][3]);
-          *reinterpret_cast<bf16x4*>(zr + 16 * m) = o;
-        }
-      } else {
-        const int b = tok / p.T;
-        bf16* vb = static_cast<bf16*>(p.Vp) + (static_cast<size_t>(b) * H + h) * p.cap * ds;
+      for (int m = 0; m < MT; ++m) {
+        bf16x4 o;
+        o[0] = static_cast<bf16>(acc[m][0]);
+        o[1] = static_cast<bf16>(acc[m][1]);
+        o[2] = static_cast<bf16>(acc[m][2]);
+        o[3] = static_cast<bf16>(acc[m][3]);
+        const int c = 2 * m + (g4 >> 1);
+        *reinterpret_cast<bf16x4*>(ost + l16 * DH + 8 * (c ^ (l16 % NC)) + 4 * (g4 & 1)) = o;
+      }
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-          const int dim = 16 * m + 4 * g4;  // this lane's 4 outputs: dims dim..dim+3
-          if (ds >= 4) {
-            const int g = dim / ds;
-            const int64_t slot = coff + __popc(cmask & ((1u << g) - 1u));
-            if (((cmask >> g) & 1u) && slot < p.cap) {
-              bf16x4 o;
-              o[0] = static_cast<bf16>(acc[m][0]);
-              o[1] = static_cast<bf16>(acc[m][1]);
-              o[2] = static_cast<bf16>(acc[m][2]);
-              o[3] = static_cast<bf16>(acc[m][3]);
-              *reinterpret_cast<bf16x4*>(vb + slot * ds + (dim - g * ds)) = o;
-            }
-          } else {
-            // 2-dim groups: the lane's outputs cover groups dim/2 and dim/2+1
+      for (int i = 0; i < 16 * NC / 64; ++i) {
+        const int u = 64 * i + lane, r = u / NC, c = u % NC;
+        const u32x4 d = *reinterpret_cast<const u32x4*>(ost + r * DH + 8 * (c ^ (r % NC)));
+        const uint32_t off = static_cast<uint32_t>(tt + r - t_begin) * tstride + 16u * c;
+        __builtin_amdgcn_raw_buffer_store_b128(d, r_z, oob_unless(tt + r < t_end, off), 0, 0);
+      }
+    } else {
+      const int tok = tt + l16;
+      const uint32_t cmask = x.mask & gm;  // zero for rows past the run
+      // groups of this token that fit the cache, and its first local slot
+      const int cnt = min(__popc(cmask), max(cap32 - x.off, 0));
+      int incl = cnt;
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              const int g = dim / 2 + u;
-              const int64_t slot = coff + __popc(cmask & ((1u << g) - 1u));
-              if (((cmask >> g) & 1u) && slot < p.cap)
-                *reinterpret_cast<uint32_t*>(vb + slot * 2) = pack_bf16x2(acc[m][2 * u], acc[m][2 * u + 1]);
+      for (int o = 1; o < 16; o <<= 1) {
+        const int y = __shfl_up(incl, o, 16);
+        if (l16 >= o) incl += y;
+      }
+      const int pre = incl - cnt;
+      const int nslot = __shfl(incl, 15, 16);
+      // the tile's tokens span samples b0.. ; slots are addressed relative to
+      // (b0, h) so that offsets stay small however large the cache is
+      const int b0 = __builtin_amdgcn_readfirstlane(tt / p.T);
+      const int b1 = __builtin_amdgcn_readfirstlane(min(tt + 15, t_end - 1) / p.T);
+      const size_t hstride = static_cast<size_t>(p.cap) * ds;  // elements per (sample, head)
+      const rsrc_t r_vp = make_rsrc(static_cast<bf16*>(p.Vp) + (static_cast<size_t>(b0) * H + h) * hstride,
+                                    clamp_bytes((static_cast<size_t>(b1 - b0) * H + 1) * hstride * 2));
+      if (g4 == 0) {
+        Obase[w][l16] = static_cast<int32_t>(static_cast<uint32_t>((tok / p.T - b0) * H) *
+                                                 static_cast<uint32_t>(hstride) +
+                                             (static_cast<uint32_t>(x.off) << lds));
+        Opre[w][l16] = pre;
+      }
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const int dim = 16 * m + 4 * g4;  // this lane's 4 outputs: dims dim..dim+3
+        if constexpr (OUT != kPack4) {
+          const int g = dim >> lds;
+          const int rank = __popc(cmask & ((1u << g) - 1u));
+          if (((cmask >> g) & 1u) && rank < cnt) {
+            bf16x4 o;
+            o[0] = static_cast<bf16>(acc[m][0]);
+            o[1] = static_cast<bf16>(acc[m][1]);
+            o[2] = static_cast<bf16>(acc[m][2]);
+            o[3] = static_cast<bf16>(acc[m][3]);
+            const int ls = pre + rank;
+            *reinterpret_cast<bf16x4*>(ost + (ls << lds) + (dim & (ds - 1))) = o;
+            if ((dim & (ds - 1)) == 0) Otok[w][ls] = static_cast<uint8_t>(l16);
+          }
+        } else {
+          // 2-dim groups: the lane's outputs cover groups dim/2 and dim/2+1
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int g = dim / 2 + u;
+            const int rank = __popc(cmask & ((1u << g) - 1u));
+            if (((cmask >> g) & 1u) && rank < cnt) {
+              const int ls = pre + rank;
+              *reinterpret_cast<uint32_t*>(ost + 2 * ls) = pack_bf16x2(acc[m][2 * u], acc[m][2 * u + 1]);
+              Otok[w][ls] = static_cast<uint8_t>(l16);
             }
           }
         }
       }
+      // copy-out: unit q covers bytes [q U, q U + U) of the tile's slots. A
+      // fixed number of store instructions (units past the tile's slots go
+      // out of range) keeps the count of outstanding stores known, so the
+      // next tile's wait does not also drain these stores.
+      constexpr int NQ = 16 * DH * 2 / U;  // units of a fully kept tile
+      const int lsu = lds + 1 - __builtin_ctz(U);  // log2(units per slot)
+      const int nunit = nslot << lsu;
+#pragma unroll
+      for (int q0 = 0; q0 < NQ; q0 += 64) {
+        const int q = q0 + lane;
+        const int ls = min(q >> lsu, NSLOT - 1);
+        const int t = Otok[w][ls] & 15;  // stale entries past the tile's slots stay in range
+        const uint32_t go = static_cast<uint32_t>(Obase[w][t]) +
+                            (static_cast<uint32_t>(ls - Opre[w][t]) << lds) +
+                            static_cast<uint32_t>((q & ((1 << lsu) - 1)) * (U / 2));
+        const uint32_t off = oob_unless(q < nunit, 2u * go);
+        if constexpr (U == 16)
+          __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4*>(ostb + 16 * q), r_vp, off, 0, 0);
+        else if constexpr (U == 8)
+          __builtin_amdgcn_raw_buffer_store_b64(*reinterpret_cast<const u32x2*>(ostb + 8 * q), r_vp, off, 0, 0);
+        else
+          __builtin_amdgcn_raw_buffer_store_b32(*reinterpret_cast<const uint32_t*>(ostb + 4 * q), r_vp, off, 0, 0);
+      }
     }
+  };
+  // one tile in flight ahead of the one being processed; A and B alternate
+  // roles so that no register copy forces an early wait
+  Tile A, B;
+  int t0 = t_begin + 16 * w;
+  load(A, t0);
+  for (; t0 < t_end; t0 += 128) {
+    load(B, t0 + 64);
+    process(A, t0);
+    if (t0 + 64 >= t_end) break;
+    load(A, t0 + 128);
+    process(B, t0 + 64);
   }
 }
 
@@ -195,10 +301,11 @@ __global__ __launch_bounds__(256) void k_rotate_pack_generic(RotateParams p, int
 
 namespace {
 int rotate_tokens_per_wg(int ntok, int H) {
-  // enough workgroups to fill 256 CUs several times over, but long enough
-  // token runs to amortise staging R_h
-  int tpw = 256;
-  while (tpw > 64 && static_cast<long>((ntok + tpw - 1) / tpw) * H < 4096) tpw >>= 1;
+  // Long token runs amortise staging R_h (32 KB at dh = 128, as much as 128
+  // tokens of values); shorten them only while there would be fewer than
+  // about 2.5 workgroups per CU (256 CUs) to spread the stream over.
+  int tpw = 512;
+  while (tpw > 64 && static_cast<long>((ntok + tpw - 1) / tpw) * H < 640) tpw >>= 1;
   return tpw;
 }
 }  // namespace
@@ -217,9 +324,9 @@ hipError_t launch_rotate(bool bf16, int ntok, int H, int dh, const void* v, cons
     p.tok_per_wg = rotate_tokens_per_wg(ntok, H);
     const dim3 grid(static_cast<unsigned>(((ntok + p.tok_per_wg - 1) / p.tok_per_wg) * H));
     if (dh == 128)
-      hipLaunchKernelGGL((k_rotate_bf16<128, false>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((k_rotate_bf16<128, kZ>), grid, dim3(256), 0, s, p);
     else
-      hipLaunchKernelGGL((k_rotate_bf16<64, false>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((k_rotate_bf16<64, kZ>), grid, dim3(256), 0, s, p);
   } else {
     const int per = 256 / dh;
     const size_t n = static_cast<size_t>(ntok) * H;
@@ -254,10 +361,18 @@ hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, con
   if (bf16 && (dh == 128 || dh == 64) && dh / G >= 2) {
     p.tok_per_wg = rotate_tokens_per_wg(ntok, H);
     const dim3 grid(static_cast<unsigned>(((ntok + p.tok_per_wg - 1) / p.tok_per_wg) * H));
-    if (dh == 128)
-      hipLaunchKernelGGL((k_rotate_bf16<128, true>), grid, dim3(256), 0, s, p);
+    // G <= 32, so 2-dim groups occur only at dh = 64
+    const int ds = dh / G;
+    if (dh == 128 && ds >= 8)
+      hipLaunchKernelGGL((k_rotate_bf16<128, kPack16>), grid, dim3(256), 0, s, p);
+    else if (dh == 128)
+      hipLaunchKernelGGL((k_rotate_bf16<128, kPack8>), grid, dim3(256), 0, s, p);
+    else if (ds >= 8)
+      hipLaunchKernelGGL((k_rotate_bf16<64, kPack16>), grid, dim3(256), 0, s, p);
+    else if (ds == 4)
+      hipLaunchKernelGGL((k_rotate_bf16<64, kPack8>), grid, dim3(256), 0, s, p);
     else
-      hipLaunchKernelGGL((k_rotate_bf16<64, true>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((k_rotate_bf16<64, kPack4>), grid, dim3(256), 0, s, p);
   } else {
     const int per = 256 / dh;
     const size_t n = static_cast<size_t>(ntok) * H;

@@ -139,7 +139,7 @@ rolesub_status rolesub_rotate_values(const rolesub_dims* dims, rolesub_dtype dty
   if (ntok > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
   const size_t bytes = ntok * dims->H * dims->dh * esize(dtype);
   if (ranges_overlap(v, bytes, z, bytes)) return fail(ROLESUB_ERR_INVALID_ARG, "%s: z overlaps v", fn);
-  if (static_cast<size_t>(256) * dims->H * dims->dh * esize(dtype) >= kMaxRegion)
+  if (static_cast<size_t>(512) * dims->H * dims->dh * esize(dtype) >= kMaxRegion)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: too many heads", fn);
   return from_hip(launch_rotate(dtype == ROLESUB_BF16, static_cast<int>(ntok), dims->H, dims->dh, v, R,
                                 z, static_cast<hipStream_t>(stream)),
@@ -288,8 +288,12 @@ rolesub_status rolesub_rotate_pack(const rolesub_dims* dims, rolesub_dtype dtype
     return fail(ROLESUB_ERR_INVALID_ARG, "%s: v, R, mask, offsets and Vp must be non-NULL", fn);
   if (static_cast<size_t>(dims->B) * dims->T > 0x7FFFFFFF)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
-  if (static_cast<size_t>(256) * dims->H * dims->dh * esize(dtype) >= kMaxRegion)
+  if (static_cast<size_t>(512) * dims->H * dims->dh * esize(dtype) >= kMaxRegion)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: too many heads", fn);
+  // a 16-token tile spans at most 15/T + 2 samples of the cache
+  if (static_cast<size_t>(15 / std::max(dims->T, 1) + 2) * dims->H * cap_groups * (dims->dh / dims->G) *
+          esize(dtype) >= kMaxRegion)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: packed cache too large", fn);
   hipStream_t s = static_cast<hipStream_t>(stream);
   rolesub_status r = from_hip(launch_pack_offsets(dims->B, dims->T, dims->G, mask, offsets, s), fn);
   if (r) return r;
