@@ -31,26 +31,32 @@ __device__ __forceinline__ uint32_t group_mask(int G) { return G >= 32 ? 0xFFFFF
 // and packed groups of tile i+1 are in flight into registers, and the group
 // masks and cache offsets of tile i+2 (which address tile i+2's packed groups)
 // are in flight too.
-// R_h is staged into LDS in the prologue (coalesced 16-byte rows, latency
-// hidden behind the first tiles). After the last tile, O^T = R_h U^T (one
-// more MFMA chain, U in bf16, R_h fragments from LDS) and each lane stores 4
-// consecutive outputs of its query.
+// After the last tile R_h is staged into LDS over the tile buffers
+// (coalesced 16-byte rows), O^T = R_h U^T is one more MFMA chain (U in bf16,
+// R_h fragments from LDS) and each lane stores 4 consecutive outputs of its
+// query.
 // VM: how the 8-dim chunks of the value tile map to packed groups:
 //   kWide  groups of >= 8 dims (one 16-byte load per token and chunk)
 //   kDs4   4-dim groups (two 8-byte loads), kDs2  2-dim groups (four 4-byte loads)
 constexpr int kWide = 0, kDs4 = 1, kDs2 = 2;
 
+// Three waves per SIMD (three workgroups per CU): the register budget is
+// capped at 168 so that occupancy, not just the pipeline, hides latency.
 template <int DH, int VM>
-__global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k_attend_bf16(AttendParams p) {
   constexpr int TK = 64, MT = DH / 16, KS = DH / 32, KLD = DH + 8, ZLD = TK / 2 + 4;
   constexpr int NKP = TK * DH / 8 / 256;          // 16-byte K pieces per thread per tile
   constexpr int NVI = (TK / 2) * (DH / 8) / 256;  // (token pair, 8-dim chunk) items per thread
-  __shared__ __attribute__((aligned(16))) bf16 Ks[TK * KLD];
-  __shared__ __attribute__((aligned(16))) uint32_t Zt[DH * ZLD];
+  constexpr int RLD = DH + 8;  // padded rows: conflict-free fragment reads per half-wave
+  // R_h is needed only after the key loop: it reuses the K / value tile space,
+  // which keeps the workgroup at about 36 KB of LDS
+  constexpr int KB = TK * KLD * 2, ZB = DH * ZLD * 4, RB = DH * RLD * 2;
+  __shared__ __attribute__((aligned(16))) char smem[KB + ZB > RB ? KB + ZB : RB];
+  bf16* Ks = reinterpret_cast<bf16*>(smem);
+  uint32_t* Zt = reinterpret_cast<uint32_t*>(smem + KB);
+  bf16* Rs = reinterpret_cast<bf16*>(smem);
   __shared__ uint32_t s_mask[2][TK];
   __shared__ int32_t s_off[2][TK];
-  constexpr int RLD = DH + 8;  // padded rows: conflict-free fragment reads per half-wave
-  __shared__ __attribute__((aligned(16))) bf16 Rs[DH * RLD];
   int h, b;
   xcd_split(blockIdx.x, p.H, h, b);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
@@ -159,19 +165,9 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
   // ---- prologue: R_h into LDS (coalesced rows, used by the final
   // back-rotation), metadata of tiles 0 and 1, operands of tile 0
   {
-    constexpr int NRP = DH * DH / 8 / 256;  // 16-byte pieces of R_h per thread
-    const rsrc_t r_R = make_rsrc(static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH, DH * DH * 2);
-    u32x4 rv[NRP];
-#pragma unroll
-    for (int r = 0; r < NRP; ++r) rv[r] = bload16(r_R, 16u * (tid + 256 * r));
     uint32_t m0;
     int32_t o0;
     load_meta(0, m0, o0);
-#pragma unroll
-    for (int r = 0; r < NRP; ++r) {
-      const int pc = tid + 256 * r;
-      *reinterpret_cast<u32x4*>(Rs + (pc / (DH / 8)) * RLD + 8 * (pc % (DH / 8))) = rv[r];
-    }
     if (tid < TK) {
       s_mask[0][tid] = m0 & gm;
       s_off[0][tid] = o0;
@@ -254,6 +250,20 @@ __global__ __launch_bounds__(256) void k_attend_bf16(AttendParams p) {
     __syncthreads();
   }
 
+  // ---- R_h into LDS over the (now idle) K / value tiles; the loop ended on a barrier
+  {
+    constexpr int NRP = DH * DH / 8 / 256;  // 16-byte pieces of R_h per thread
+    const rsrc_t r_R = make_rsrc(static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH, DH * DH * 2);
+    u32x4 rv[NRP];
+#pragma unroll
+    for (int r = 0; r < NRP; ++r) rv[r] = bload16(r_R, 16u * (tid + 256 * r));
+#pragma unroll
+    for (int r = 0; r < NRP; ++r) {
+      const int pc = tid + 256 * r;
+      *reinterpret_cast<u32x4*>(Rs + (pc / (DH / 8)) * RLD + 8 * (pc % (DH / 8))) = rv[r];
+    }
+  }
+  __syncthreads();
   // ---- normalise and rotate back: O^T = R_h U^T
   float lsum = l_run + __shfl_xor(l_run, 16, kWave);
   lsum += __shfl_xor(lsum, 32, kWave);
