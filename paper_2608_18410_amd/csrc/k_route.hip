@@ -491,21 +491,20 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
   // Wave-loads u = 0..3 are always W1 rows (j <= 15); u = 4 is W_r rows for
   // waves 0-1 and token rows for waves 2-3; u = 5, 6 are token rows. Each call
   // site below uses one fixed buffer resource so it stays in scalar registers.
-  auto issue = [&](int c) {
+  auto issue_one = [&](int c, int u) {
     const uint32_t sbase = ring_base + (c % kRtNB) * kRtStage;
     const bool ok = c < nch;  // chunks past the end are all-out-of-range dummies
     const uint32_t kb = static_cast<uint32_t>(c) * kRtKc * 2;
-    auto off = [&](int u) { return (ok && base_off[u] != kOOB) ? base_off[u] + kb : kOOB; };
-    auto dst = [&](int u) {
-      const int jj = w + 4 * u;
-      return sbase + (jj < 18 ? jj * 1024 : kRtWBytes + (jj - 18) * 1024);
-    };
+    const uint32_t off = (ok && base_off[u] != kOOB) ? base_off[u] + kb : kOOB;
+    const int jj = w + 4 * u;
+    const uint32_t dst = sbase + (jj < 18 ? jj * 1024 : kRtWBytes + (jj - 18) * 1024);
+    if (u < 4) dma16(r_w1, off, dst);
+    else if (u == 4 && w < 2) dma16(r_wr, off, dst);
+    else if (u == 4 || u == 5 || (u == 6 && w < 2)) dma16(r_h, off, dst);
+  };
+  auto issue = [&](int c) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) dma16(r_w1, off(u), dst(u));
-    if (w < 2) dma16(r_wr, off(4), dst(4));
-    else dma16(r_h, off(4), dst(4));
-    dma16(r_h, off(5), dst(5));
-    if (w < 2) dma16(r_h, off(6), dst(6));
+    for (int u = 0; u < 7; ++u) issue_one(c, u);
   };
 
   f32x4 acc[9];
@@ -519,21 +518,29 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
     if (nld == 7) wait_vmcnt<7 * (kRtNB - 2)>();
     else wait_vmcnt<6 * (kRtNB - 2)>();
     __syncthreads();
+    // All fragment reads first; then the 18 MFMAs with this wave's 7 refill
+    // DMAs of chunk c + kRtNB - 1 spread between them (the stage they fill was
+    // released at this barrier). Issued as one burst after the MFMAs, the
+    // DMAs of the four waves queued at the texture unit (about 64 B per
+    // clock) while the matrix cores idled, and the other way round.
     const char* st = ring + (c % kRtNB) * kRtStage;
     const int th = 16 * w + l16;
-    bf16x8 hb[2];
+    bf16x8 hb[2], af[2][9];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < 2; ++ks) {
       hb[ks] = *reinterpret_cast<const bf16x8*>(st + kRtWBytes + th * 128 + 16 * ((4 * ks + g4) ^ rt_swz(th)));
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int m = 0; m < 9; ++m) {
         const int r = 16 * m + l16;
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(st + r * 128 + 16 * ((4 * ks + g4) ^ rt_swz(r)));
-        acc[m] = mfma_16x16x32(a, hb[ks], acc[m]);
+        af[ks][m] = *reinterpret_cast<const bf16x8*>(st + r * 128 + 16 * ((4 * ks + g4) ^ rt_swz(r)));
       }
-    issue(c + kRtNB - 1);  // refills the stage read in the previous iteration
+    }
+#pragma unroll
+    for (int i = 0; i < 18; ++i) {
+      acc[i % 9] = mfma_16x16x32(af[i / 9][i % 9], hb[i / 9], acc[i % 9]);
+      if (i % 3 == 1) issue_one(c + kRtNB - 1, i / 3);
+    }
+    issue_one(c + kRtNB - 1, 6);
   }
   wait_vmcnt<0>();  // trailing dummy loads land before the LDS is released
   __syncthreads();  // every wave is done with the ring
