@@ -585,6 +585,28 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
 #pragma unroll
   for (int c = 0; c < 16; ++c) a[c] = __shfl(ex[c & 3], l16 + 16 * (c >> 2), kWave) * isum;
 
+  // F a on the f32 matrix cores: the accumulator layout is that of a 16x16x4
+  // MFMA with A = F (rows 16m + t, roles k0 + q) and B = a (role k0 + q of the
+  // lane's token), so x += F a costs ceil(C / 4) MFMAs per 16 hidden units.
+  // Lane quarter q takes a[k0 + q] by a bitwise blend (a select chain on q
+  // would be turned into an indexed access and move a[] to scratch memory).
+  float ab[4];
+#pragma unroll
+  for (int k4 = 0; k4 < 4; ++k4) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v |= (g4 == q ? ~0u : 0u) & __float_as_uint(a[4 * k4 + q]);
+    ab[k4] = __uint_as_float(v);
+  }
+#pragma unroll
+  for (int k4 = 0; k4 < 4; ++k4) {
+    if (4 * k4 < C) {
+#pragma unroll
+      for (int m = 0; m < 8; ++m)
+        acc[m] = __builtin_amdgcn_mfma_f32_16x16x4f32(Fs[(16 * m + l16) * kFsStride + 4 * k4 + g4], ab[k4],
+                                                      acc[m], 0, 0, 0);
+    }
+  }
   float gam[GP];
 #pragma unroll
   for (int s = 0; s < GP; ++s) gam[s] = 0.f;
@@ -593,17 +615,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = 16 * m + 4 * g4 + i;
-      float x = acc[m][i] + cbv[4 * m + i];
-      const f32x4* fr = reinterpret_cast<const f32x4*>(Fs + j * kFsStride);
-#pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) {
-        const f32x4 f = fr[c4];
-        x += f[0] * a[4 * c4];
-        x += f[1] * a[4 * c4 + 1];
-        x += f[2] * a[4 * c4 + 2];
-        x += f[3] * a[4 * c4 + 3];
-      }
-      const float gl = gelu_exact(x);
+      const float gl = gelu_exact(acc[m][i] + cbv[4 * m + i]);
       const f32x4* wr = reinterpret_cast<const f32x4*>(W2t + j * kW2Stride);
 #pragma unroll
       for (int s4 = 0; s4 < GP / 4; ++s4) {
