@@ -94,8 +94,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   auto load_meta = [&](int t0, uint32_t& m, int32_t& o) {
     const int t = t0 + tid;
     const bool ok = tid < TK && t < T;
-    m = bload4(r_mask, ok ? 4u * t : kOOB);  // masked to G bits when stored (no wait here)
-    o = static_cast<int32_t>(bload4(r_off, ok ? 4u * t : kOOB));
+    m = bload4(r_mask, oob_unless(ok, 4u * t));  // masked to G bits when stored (no wait here)
+    o = static_cast<int32_t>(bload4(r_off, oob_unless(ok, 4u * t)));
   };
   u32x4 kreg[NKP];
   auto load_k = [&](int t0) {
@@ -104,16 +104,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       const int pc = tid + 256 * r;
       const int row = pc / (DH / 8), c8 = pc % (DH / 8);
       const int t = t0 + row;
-      kreg[r] = bload16(r_k, t < T ? t * kstride + 16u * c8 : kOOB);
+      kreg[r] = bload16(r_k, oob_unless(t < T, t * kstride + 16u * c8));
     }
   };
   // packed groups of 2 tokens x 8 dims for each item, addressed through the LDS masks/offsets
   u32x4 vreg[NVI][2];
   const int64_t cap = p.cap;
+  // slots are < 2^31 (the cache per (sample, head) is < 2 GiB); the select is
+  // pinned so that no load ends up behind a branch
+  const int cap32 = static_cast<int>(cap);
   auto slot_off = [&](uint32_t m, int o, int g, bool tok_ok, int elem) -> uint32_t {
-    const int64_t sl = o + __popc(m & ((1u << g) - 1u));
-    const bool ok = tok_ok && ((m >> g) & 1u) && sl < cap;
-    return ok ? static_cast<uint32_t>((sl * ds + elem) * 2) : kOOB;
+    const int sl = o + __popc(m & ((1u << g) - 1u));
+    const bool ok = tok_ok & (((m >> g) & 1u) != 0u) & (sl < cap32);
+    return oob_unless(ok, static_cast<uint32_t>((sl * ds + elem) * 2));
   };
   auto load_v = [&](int t0, int slot) {
 #pragma unroll
@@ -189,11 +192,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       s_off[nslot][tid] = oreg;
     }
     __syncthreads();
-    if (t0 + TK < T) {
-      load_k(t0 + TK);
-      load_v(t0 + TK, nslot);
-      load_meta(t0 + 2 * TK, mreg, oreg);
-    }
+    // next tile's operands; past the end every load is out of range (no
+    // memory access), so there is no branch here: a branch around the loads
+    // makes the compiler wait on every outstanding load at its join
+    load_k(t0 + TK);
+    load_v(t0 + TK, nslot);
+    load_meta(t0 + 2 * TK, mreg, oreg);
 
     // ---- S^T = K Q^T (rows: tile tokens 16*m2 + 4*g4 + i; column: this lane's query)
     f32x4 s[4];
@@ -276,29 +280,58 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       ub[ks][i] = static_cast<bf16>(acc[2 * ks][i] * inv);
       ub[ks][4 + i] = static_cast<bf16>(acc[2 * ks + 1][i] * inv);
     }
-  const size_t obase = ((static_cast<size_t>(b) * p.Tq + (qvalid ? qq : 0)) * H + h) * DH + 4 * g4;
+  f32x4 o[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
-    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    o[m] = f32x4{0.f, 0.f, 0.f, 0.f};
     const bf16* rr = Rs + (16 * m + l16) * RLD + 4 * g4;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const u32x2 lo = *reinterpret_cast<const u32x2*>(rr + 32 * ks);
       const u32x2 hi = *reinterpret_cast<const u32x2*>(rr + 32 * ks + 16);
       const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
-      o = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), ub[ks], o);
+      o[m] = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), ub[ks], o[m]);
     }
-    if (qvalid) {
-      if (p.out_f32) {
-        *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + obase + 16 * m) = o;
-      } else {
-        bf16x4 ov;
-        ov[0] = static_cast<bf16>(o[0]);
-        ov[1] = static_cast<bf16>(o[1]);
-        ov[2] = static_cast<bf16>(o[2]);
-        ov[3] = static_cast<bf16>(o[3]);
-        *reinterpret_cast<bf16x4*>(static_cast<bf16*>(p.out) + obase + 16 * m) = ov;
-      }
+  }
+  // ---- output: each wave stages its 16 query rows in LDS (over R_h, once
+  // every wave is done with it) in row order, 16-byte chunks XOR-swizzled by
+  // row, and writes them with consecutive lanes on consecutive 16-byte units
+  // (scattered 8-byte stores from the MFMA layout waste write bandwidth).
+  // Rows past Tq fall outside the output resource and are dropped.
+  __syncthreads();
+  const int q0 = blockIdx.y * 64 + 16 * w;  // this wave's first query
+  const uint32_t esz = p.out_f32 ? 4u : 2u;
+  const uint32_t ostride = static_cast<uint32_t>(H) * DH * esz;  // bytes between queries
+  const rsrc_t r_o = make_rsrc(static_cast<char*>(p.out) + ((static_cast<size_t>(b) * p.Tq) * H + h) * DH * esz,
+                               clamp_bytes((static_cast<size_t>(p.Tq - 1) * H + 1) * DH * esz));
+  char* stg = smem + w * (16 * DH * 4);  // 16 rows of up to 4-byte elements
+  if (p.out_f32) {
+    constexpr int NC = DH / 4;  // 16-byte chunks per f32 row
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+      *reinterpret_cast<f32x4*>(stg + l16 * (DH * 4) + 16 * ((4 * m + g4) ^ l16)) = o[m];
+#pragma unroll
+    for (int i = 0; i < 16 * NC / 64; ++i) {
+      const int u = 64 * i + lane, r = u / NC, c = u % NC;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r * (DH * 4) + 16 * (c ^ r));
+      __builtin_amdgcn_raw_buffer_store_b128(v, r_o, oob_unless(q0 + r < p.Tq, (q0 + r) * ostride + 16u * c), 0, 0);
+    }
+  } else {
+    constexpr int NC = DH / 8;  // 16-byte chunks per bf16 row
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      bf16x4 ov;
+      ov[0] = static_cast<bf16>(o[m][0]);
+      ov[1] = static_cast<bf16>(o[m][1]);
+      ov[2] = static_cast<bf16>(o[m][2]);
+      ov[3] = static_cast<bf16>(o[m][3]);
+      *reinterpret_cast<bf16x4*>(stg + l16 * (DH * 2) + 16 * ((2 * m + (g4 >> 1)) ^ (l16 % NC)) + 8 * (g4 & 1)) = ov;
+    }
+#pragma unroll
+    for (int i = 0; i < 16 * NC / 64; ++i) {
+      const int u = 64 * i + lane, r = u / NC, c = u % NC;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r * (DH * 2) + 16 * (c ^ (r % NC)));
+      __builtin_amdgcn_raw_buffer_store_b128(v, r_o, oob_unless(q0 + r < p.Tq, (q0 + r) * ostride + 16u * c), 0, 0);
     }
   }
 }
