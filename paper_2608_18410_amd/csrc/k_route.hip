@@ -24,18 +24,72 @@ constexpr int kLang = 1;
 // owns 64*VEC columns of one sample; its language rows are listed in LDS in
 // ascending order, the four waves take every fourth listed row, and the wave
 // partial sums are added in wave order (deterministic).
-template <class T>
+//
+// With PCB (bf16 MLP2 router, d a multiple of 512, Hr 64 or 128) the
+// block also forms its columns' share of the language term,
+//   pcb[cblk][b][j] = W1[j, d+d_e + cols] . hbar[b][cols],
+// while the pooled columns are still in registers, and blocks past B*ncb fold
+// the role term F = W1_e E^T (one thread per entry). cb is then the sum of the
+// ncb shares plus b1, added by the MFMA router itself or by k_route_cbsum.
+template <class T, bool PCB>
 __global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int TCH = 1024;  // tokens listed per pass
+  constexpr int RU = 16;     // row loads in flight per wave
   __shared__ int s_rows[TCH];
   __shared__ int s_wcnt[4];
   __shared__ float s_part[4][64 * VEC];
   const int ncb = (p.d + 64 * VEC - 1) / (64 * VEC);
-  const int b = blockIdx.x / ncb, cb = blockIdx.x % ncb;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if (PCB && blockIdx.x >= static_cast<unsigned>(p.B * ncb)) {
+    // F[j][c] = W1[j, d : d+d_e] . E[c]; d_e a multiple of 8, rows 16-byte aligned
+    const int e = (blockIdx.x - p.B * ncb) * 256 + tid;
+    const int j = e / p.C, c = e - j * p.C;
+    const bool ok = j < p.Hr;
+    const uint32_t W1s = 2u * p.d + p.d_e;
+    const rsrc_t r_w = make_rsrc(p.W1, static_cast<uint32_t>(p.Hr) * W1s * sizeof(T));
+    const rsrc_t r_e = make_rsrc(p.E, static_cast<uint32_t>(p.C * p.d_e) * sizeof(T));
+    const uint32_t ow = (static_cast<uint32_t>(j) * W1s + p.d) * sizeof(T);
+    const uint32_t oe = static_cast<uint32_t>(c * p.d_e) * sizeof(T);
+    float acc = 0.f;
+    for (int m0 = 0; m0 < p.d_e; m0 += 8 * VEC) {
+      u32x4 wv[8], ev[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const bool in = ok && m0 + u * VEC < p.d_e;
+        const uint32_t m = static_cast<uint32_t>(m0 + u * VEC) * sizeof(T);
+        wv[u] = bload16(r_w, oob_unless(in, ow + m));
+        ev[u] = bload16(r_e, oob_unless(in, oe + m));
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const T* a = reinterpret_cast<const T*>(&wv[u]);
+        const T* x = reinterpret_cast<const T*>(&ev[u]);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc = fmaf(tof(a[i]), tof(x[i]), acc);
+      }
+    }
+    if (ok) p.F[j * p.C + c] = acc;
+    return;
+  }
+  const int b = blockIdx.x / ncb, cb = blockIdx.x % ncb;
   const uint8_t* ty = p.types + static_cast<size_t>(b) * p.T;
   const int col = cb * 64 * VEC + lane * VEC;
+  // PCB: the language-term weights this block needs (Hr <= 128 rows of its
+  // 64*VEC columns) are requested first, so they arrive during the pooling
+  u32x4 wraw[PCB ? 2 : 1][16];
+  if constexpr (PCB) {
+    const uint32_t W1s = 2u * p.d + p.d_e;
+    const rsrc_t r_w = make_rsrc(p.W1, static_cast<uint32_t>(p.Hr) * W1s * sizeof(T));
+    const uint32_t ol = static_cast<uint32_t>(p.d + p.d_e + col) * sizeof(T);
+#pragma unroll
+    for (int jb = 0; jb < 2; ++jb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int j = 64 * jb + 16 * w + i;
+        wraw[jb][i] = bload16(r_w, oob_unless(j < p.Hr, static_cast<uint32_t>(j) * W1s * sizeof(T) + ol));
+      }
+  }
   const bool vec = (p.d % VEC) == 0;
   const T* hsample = static_cast<const T*>(p.h) + static_cast<size_t>(b) * p.T * p.d;
   const rsrc_t r_h = make_rsrc(hsample, static_cast<uint32_t>(p.T) * p.d * sizeof(T));
@@ -62,16 +116,16 @@ __global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
     }
     n_total += base;
     if (vec && col < p.d) {
-      // wave w sums listed rows w, w+4, ...; 4 loads in flight per step
-      for (int i0 = w; i0 < base; i0 += 16) {
-        u32x4 raw[4];
+      // wave w sums listed rows w, w+4, ...; RU loads in flight per step
+      for (int i0 = w; i0 < base; i0 += 4 * RU) {
+        u32x4 raw[RU];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < RU; ++u) {
           const int i = i0 + 4 * u;
           raw[u] = bload16(r_h, i < base ? static_cast<uint32_t>((static_cast<size_t>(s_rows[i]) * p.d + col) * sizeof(T)) : kOOB);
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < RU; ++u) {
           const T* v = reinterpret_cast<const T*>(&raw[u]);
 #pragma unroll
           for (int e = 0; e < VEC; ++e) acc[e] += tof(v[e]);
@@ -93,6 +147,60 @@ __global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
     if (c < p.d)
       p.hbar[static_cast<size_t>(b) * p.d + c] = (((s_part[0][i] + s_part[1][i]) + s_part[2][i]) + s_part[3][i]) * inv;
   }
+  if constexpr (PCB) {
+    // lane holds pooled columns col..col+VEC-1; wave w takes rows jb+16*w+i
+    __shared__ float s_red[4][16][65];
+    float hv[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const int i = lane * VEC + e;
+      hv[e] = (((s_part[0][i] + s_part[1][i]) + s_part[2][i]) + s_part[3][i]) * inv;
+    }
+    float* dst = p.pcb + (static_cast<size_t>(cb) * p.B + b) * p.Hr;
+#pragma unroll
+    for (int jh = 0; jh < 2; ++jh) {
+      const int jb = 64 * jh;
+      if (jb >= p.Hr) break;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const T* v = reinterpret_cast<const T*>(&wraw[jh][i]);
+        float pd = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) pd = fmaf(tof(v[e]), hv[e], pd);
+        s_red[w][i][lane] = pd;
+      }
+      __syncthreads();
+      // lane (r = lane/4, q = lane%4) adds lanes 16q..16q+15 of row r, then the
+      // four quarters are combined as (q0+q1)+(q2+q3)
+      const int r = lane >> 2, q = lane & 3;
+      float sum = 0.f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) sum += s_red[w][r][16 * q + k];
+      sum += __shfl_xor(sum, 1);
+      sum += __shfl_xor(sum, 2);
+      if (q == 0) dst[jb + 16 * w + r] = sum;
+      __syncthreads();
+    }
+  }
+}
+
+// cb[b][j] = b1[j] + sum over column blocks s (in order) of pcb[s][b][j].
+// One thread per (b, j).
+__global__ __launch_bounds__(256) void k_route_cbsum(RouteParams p, int ncb) {
+  const int n = p.B * p.Hr;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  const bool ok = i < n;
+  const rsrc_t r_p = make_rsrc(p.pcb, static_cast<uint32_t>(ncb) * n * 4u);
+  float acc = 0.f;
+  for (int s0 = 0; s0 < ncb; s0 += 8) {
+    uint32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = bload4(r_p, oob_unless(ok && s0 + u < ncb, static_cast<uint32_t>((s0 + u) * n + i) * 4u));
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += __uint_as_float(v[u]);
+  }
+  if (ok) p.cb[i] = acc + tof(static_cast<const bf16*>(p.b1)[i % p.Hr]);
 }
 
 // Per-sample language term and folded role term. 1D grid:
@@ -411,12 +519,13 @@ __device__ __forceinline__ int rt_swz(int r) { return (r >> 1) & 7; }
 // (lanes of one token quarter share a row) fall on distinct LDS banks.
 constexpr int kFsStride = 20;
 
-template <int GP>
-__global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
+template <int GP, bool PS>
+__global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb) {
   constexpr int Hr = 128, kW2Stride = GP + 4;
   static_assert(Hr * (kFsStride + kW2Stride) * 4 <= kRtNB * kRtStage, "epilogue tiles fit the ring");
   __shared__ __attribute__((aligned(16))) char ring[kRtNB * kRtStage];
   __shared__ float b2s[GP], brs[16];
+  __shared__ __attribute__((aligned(16))) float cbs[PS ? 2 : 1][Hr];
   const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
   const int d = p.d, C = p.C, G = p.G;
@@ -431,9 +540,13 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
   const int type = p.types[valid ? tok : 0];
 
   // Epilogue operands are loaded now and held in registers through the K
-  // loop: F (entry e = j*16 + c), W2 transposed (entry e = s*Hr + j) and this
-  // lane's 32 per-sample language terms cb[b][16m + 4q + i].
-  float fv[8], w2v[GP / 2], cbv[32];
+  // loop: F (entry e = j*16 + c), W2 transposed (entry e = s*Hr + j) and
+  // either this lane's 32 per-sample language terms cb[b][16m + 4q + i] or,
+  // with PS, this thread's share of the block's language terms: the npcb
+  // (at most 8) column-block partials of unit j = tid % 128 for sample
+  // tok0 / T + tid / 128 (a block spans at most two samples when T >= 64).
+  float fv[8], w2v[GP / 2], cbv[PS ? 1 : 32], ps[PS ? 8 : 1], b1v = 0.f;
+  const int b0 = tok0 / p.T;
   {
     const rsrc_t r_F = make_rsrc(p.F, static_cast<uint32_t>(Hr * C) * 4u);
     const rsrc_t r_W2 = make_rsrc(p.W2, static_cast<uint32_t>(G * Hr) * 2u);
@@ -449,11 +562,20 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
       const uint32_t x = bload4(r_W2, sg < G ? 4u * ((sg * Hr + j) >> 1) : kOOB);
       w2v[u] = __uint_as_float((j & 1) ? (x & 0xffff0000u) : (x << 16));
     }
+    if constexpr (PS) {
+      const int bs = b0 + (tid >> 7), jj = tid & 127;
+      const rsrc_t r_p = make_rsrc(p.pcb, static_cast<uint32_t>(npcb * p.B * Hr) * 4u);
 #pragma unroll
-    for (int m = 0; m < 8; ++m)
+      for (int u = 0; u < 8; ++u)
+        ps[u] = __uint_as_float(bload4(r_p, oob_unless(bs < p.B && u < npcb, 4u * ((u * p.B + bs) * Hr + jj))));
+      b1v = tof(static_cast<const bf16*>(p.b1)[jj]);
+    } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        cbv[4 * m + i] = __uint_as_float(bload4(r_cb, 4u * (b * Hr + 16 * m + 4 * g4 + i)));
+      for (int m = 0; m < 8; ++m)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          cbv[4 * m + i] = __uint_as_float(bload4(r_cb, 4u * (b * Hr + 16 * m + 4 * g4 + i)));
+    }
     if (tid < GP) b2s[tid] = tid < G ? tof(static_cast<const bf16*>(p.b2)[tid]) : 0.f;
     if (tid < 16) brs[tid] = tid < C ? tof(static_cast<const bf16*>(p.b_r)[tid]) : 0.f;
   }
@@ -557,7 +679,27 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
     const int e = u * 256 + tid;
     W2t[(e & 127) * kW2Stride + (e >> 7)] = w2v[u];
   }
+  if constexpr (PS) {
+    // partials added in block order; out-of-range ones read as zero
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) sum += ps[u];
+    cbs[tid >> 7][tid & 127] = sum + b1v;
+  }
   __syncthreads();
+  float cbl[32];
+  if constexpr (PS) {
+    const float* src = cbs[valid ? b - b0 : 0];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(src + 16 * m + 4 * g4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cbl[4 * m + i] = v[i];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 32; ++i) cbl[i] = cbv[i];
+  }
 
   // ---- epilogue: lanes l16, l16+16, l16+32, l16+48 hold token `tok`;
   // lane quarter q = g4 owns hidden units 16m + 4q + i and role logits 4q + i.
@@ -615,7 +757,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = 16 * m + 4 * g4 + i;
-      const float gl = gelu_exact(acc[m][i] + cbv[4 * m + i]);
+      const float gl = gelu_exact(acc[m][i] + cbl[4 * m + i]);
       const f32x4* wr = reinterpret_cast<const f32x4*>(W2t + j * kW2Stride);
 #pragma unroll
       for (int s4 = 0; s4 < GP / 4; ++s4) {
@@ -685,31 +827,51 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p) {
 hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s) {
   const size_t ntok = static_cast<size_t>(p.B) * p.T;
   if (ntok == 0) return hipSuccess;
+  const bool mfma_ok = bf16 && p.kind == 0 && p.Hr == 128 && p.C >= 1 && p.C <= 16 &&
+                       p.G <= 32 && p.d % kRtKc == 0 && ntok < (1u << 30);
+  const int vec = bf16 ? 8 : 4;
+  const int ncb = (p.d + 64 * vec - 1) / (64 * vec);
+  const bool pcb_ok = bf16 && p.kind == 0 && p.pcb && p.d % (64 * vec) == 0 && p.d_e % 8 == 0 &&
+                      p.Hr % 64 == 0 && p.Hr <= 128 && p.C >= 1 &&
+                      static_cast<size_t>(p.Hr) * (2 * static_cast<size_t>(p.d) + p.d_e) * 2 < (1ull << 31) &&
+                      static_cast<size_t>(ncb) * p.B * p.Hr * 4 < (1ull << 31) &&
+                      ((reinterpret_cast<uintptr_t>(p.W1) | reinterpret_cast<uintptr_t>(p.E)) & 15) == 0;
+  // the MFMA router adds the partial language terms itself when a block of
+  // its tokens spans at most two samples and there are at most 8 partials
+  const bool ps = mfma_ok && pcb_ok && p.T >= kRtTok && ncb <= 8;
   {
-    const int vec = bf16 ? 8 : 4;
-    const int ncb = (p.d + 64 * vec - 1) / (64 * vec);
     const dim3 gpool(static_cast<unsigned>(p.B * ncb));
     const int nout = p.kind == 0 ? p.Hr : p.G;
     const int nF = ((p.kind == 0 ? p.Hr : p.G) + 3) / 4;
     const dim3 gproj(static_cast<unsigned>(p.B * ((nout + 7) / 8) + nF));
     const size_t shm = static_cast<size_t>(p.d) * sizeof(float);
-    if (bf16) {
-      hipLaunchKernelGGL(k_route_pool<rolesub::bf16>, gpool, dim3(256), 0, s, p);
+    if (pcb_ok) {
+      const unsigned nfb = static_cast<unsigned>((p.Hr * p.C + 255) / 256);
+      hipLaunchKernelGGL((k_route_pool<rolesub::bf16, true>), dim3(gpool.x + nfb), dim3(256), 0, s, p);
+      if (!ps)
+        hipLaunchKernelGGL(k_route_cbsum, dim3(static_cast<unsigned>((p.B * p.Hr + 255) / 256)), dim3(256), 0,
+                           s, p, ncb);
+    } else if (bf16) {
+      hipLaunchKernelGGL((k_route_pool<rolesub::bf16, false>), gpool, dim3(256), 0, s, p);
       hipLaunchKernelGGL(k_route_proj<rolesub::bf16>, gproj, dim3(256), shm, s, p);
     } else {
-      hipLaunchKernelGGL(k_route_pool<float>, gpool, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((k_route_pool<float, false>), gpool, dim3(256), 0, s, p);
       hipLaunchKernelGGL(k_route_proj<float>, gproj, dim3(256), shm, s, p);
     }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const bool mfma_ok = bf16 && p.kind == 0 && p.Hr == 128 && p.C >= 1 && p.C <= 16 &&
-                       p.G <= 32 && p.d % kRtKc == 0 && ntok < (1u << 30);
   if (mfma_ok) {
-    const unsigned nblk = static_cast<unsigned>((ntok + kRtTok - 1) / kRtTok);
-    if (p.G <= 8) hipLaunchKernelGGL(k_route_mlp2_bf16<8>, dim3(nblk), dim3(256), 0, s, p);
-    else if (p.G <= 16) hipLaunchKernelGGL(k_route_mlp2_bf16<16>, dim3(nblk), dim3(256), 0, s, p);
-    else hipLaunchKernelGGL(k_route_mlp2_bf16<32>, dim3(nblk), dim3(256), 0, s, p);
+    const dim3 grid(static_cast<unsigned>((ntok + kRtTok - 1) / kRtTok));
+    if (ps) {
+      if (p.G <= 8) hipLaunchKernelGGL((k_route_mlp2_bf16<8, true>), grid, dim3(256), 0, s, p, ncb);
+      else if (p.G <= 16) hipLaunchKernelGGL((k_route_mlp2_bf16<16, true>), grid, dim3(256), 0, s, p, ncb);
+      else hipLaunchKernelGGL((k_route_mlp2_bf16<32, true>), grid, dim3(256), 0, s, p, ncb);
+    } else {
+      if (p.G <= 8) hipLaunchKernelGGL((k_route_mlp2_bf16<8, false>), grid, dim3(256), 0, s, p, 0);
+      else if (p.G <= 16) hipLaunchKernelGGL((k_route_mlp2_bf16<16, false>), grid, dim3(256), 0, s, p, 0);
+      else hipLaunchKernelGGL((k_route_mlp2_bf16<32, false>), grid, dim3(256), 0, s, p, 0);
+    }
   } else {
     const int nmain = p.kind == 0 ? p.Hr : p.G;
     const size_t shm = sizeof(float) * (static_cast<size_t>(p.d) + nmain + p.C +

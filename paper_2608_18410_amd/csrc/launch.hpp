@@ -15,6 +15,7 @@ struct RouteParams {
   float* cb;  // [B][Hr or G] per-sample language term (workspace)
   float* F;   // [Hr or G][C] folded role term (workspace)
   float* hbar;  // [B][d] pooled language state (workspace)
+  float* pcb;   // [ncb][B][Hr] partial language terms per column block (bf16 MLP2; workspace)
   int mode;
   int k_by_type[4];
   float tau;
@@ -34,6 +35,11 @@ inline size_t route_F_floats(int Hr, int G, int C, int kind) {
   return static_cast<size_t>(kind == 0 ? Hr : G) * C;
 }
 inline size_t route_hbar_floats(int B, int d) { return static_cast<size_t>(B) * d; }
+// column blocks of 256 (the smallest block the pool kernel uses, f32) bound
+// the number of partial language terms for any dtype
+inline size_t route_pcb_floats(int B, int d, int Hr, int kind) {
+  return kind == 0 ? static_cast<size_t>((d + 255) / 256) * B * Hr : 0;
+}
 
 hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s);
 // LDS bytes the generic (one token per workgroup) router needs.

@@ -105,7 +105,8 @@ size_t route_ws_bytes(const rolesub_dims* d, const rolesub_router* r) {
   if (!d || !r || d->B <= 0) return 0;
   return align256(route_cb_floats(d->B, r->Hr, d->G, r->kind) * sizeof(float)) +
          align256(route_F_floats(r->Hr, d->G, r->C, r->kind) * sizeof(float)) +
-         align256(route_hbar_floats(d->B, d->d > 0 ? d->d : 0) * sizeof(float));
+         align256(route_hbar_floats(d->B, d->d > 0 ? d->d : 0) * sizeof(float)) +
+         align256(route_pcb_floats(d->B, d->d > 0 ? d->d : 0, r->Hr, r->kind) * sizeof(float));
 }
 
 }  // namespace
@@ -241,8 +242,10 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype, cons
   p.cb = reinterpret_cast<float*>(ws);
   const size_t off_F = align256(route_cb_floats(p.B, p.Hr, p.G, p.kind) * sizeof(float));
   const size_t off_h = off_F + align256(route_F_floats(p.Hr, p.G, p.C, p.kind) * sizeof(float));
+  const size_t off_p = off_h + align256(route_hbar_floats(p.B, p.d) * sizeof(float));
   p.F = reinterpret_cast<float*>(ws + off_F);
   p.hbar = reinterpret_cast<float*>(ws + off_h);
+  p.pcb = reinterpret_cast<float*>(ws + off_p);
   return from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
 }
 

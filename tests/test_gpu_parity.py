@@ -286,6 +286,22 @@ def test_route_mlp2(cid, B):
     _route_check(w, h, types, router_tensors(wt, tdtype(w)), ref, f"mlp2 workload {cid} B={B}")
 
 
+# bf16 MLP2 shapes that take the other launch paths: partial language terms
+# summed by their own kernel (short prefix: a router block spans more than two
+# samples; more than 8 column blocks; Hr = 64 on the generic router) and the
+# per-row projection (d not a multiple of 512).
+@pytest.mark.parametrize("B,d,Hr,n_vis,n_lang", [(3, 1024, 128, 30, 9), (2, 4608, 128, 60, 9),
+                                                 (2, 1024, 64, 80, 9), (2, 1088, 128, 80, 9)])
+def test_route_mlp2_launch_paths(B, d, Hr, n_vis, n_lang):
+    w = synth.workload(2).replace(B=B, d=d, Hr=Hr, n_vis=n_vis, n_lang=n_lang, n_prop=1)
+    wt = synth.layer_weights(w, 0)
+    h = np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(B)])
+    types = stack_types(w, B)
+    ref = lambda hh, tt: O.router_mlp2(hh, tt, wt["W_r"], wt["b_r"], wt["E"], wt["W1"], wt["b1"],
+                                       wt["W2"], wt["b2"])
+    _route_check(w, h, types, router_tensors(wt, torch.bfloat16), ref, f"mlp2 B={B} d={d} Hr={Hr} T={w.T}")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_route_additive(dtype):
     w = synth.workload(2).replace(B=2, dtype=dtype, d=512, G=16, C=6, n_vis=40, n_lang=9, n_prop=1,
