@@ -215,6 +215,8 @@ def _attend_case(w, B, T, Tq, H, dh, G, counts=None, out_dtype=None, seed=0):
     (3, 2, 97, 20, 8, 64, 8),          # head dim 64 on matrix cores
     (3, 2, 65, 16, 8, 64, 32),         # 2-dim groups
     (1, 2, 33, 3, 4, 128, 4),          # f32, head dim 128
+    (3, 301, 70, 20, 4, 128, 8),       # runs of 3 samples per workgroup, last run shorter
+    (3, 150, 40, 9, 8, 64, 16),        # one tile per sample: every tile starts and ends one
 ])
 def test_attend(cid, B, T, Tq, H, dh, G):
     w = synth.workload(cid)
@@ -225,11 +227,12 @@ def test_attend(cid, B, T, Tq, H, dh, G):
     assert err <= TOL[w.dtype]
 
 
-def test_attend_f32_output_from_bf16():
+@pytest.mark.parametrize("B,H", [(2, 16), (70, 8)])
+def test_attend_f32_output_from_bf16(B, H):
     w = synth.workload(2)
-    got, ref, _ = _attend_case(w, 2, 150, 56, 16, 128, 8, out_dtype=torch.float32)
+    got, ref, _ = _attend_case(w, B, 150, 56, H, 128, 8, out_dtype=torch.float32)
     err = max_rel(got, ref)
-    _say(f"attend bf16 in, f32 out: max rel err {err:.2e}")
+    _say(f"attend bf16 in, f32 out B={B} H={H}: max rel err {err:.2e}")
     assert err <= 2e-2
 
 
