@@ -17,7 +17,8 @@ __device__ __forceinline__ uint32_t group_mask(int G) { return G >= 32 ? 0xFFFFF
 
 // ---------------------------------------------------------------------------
 // bf16 matrix-core kernel. One workgroup = one (sample, head) and up to 64
-// queries; wave w owns queries 16w..16w+15. KV tokens stream in tiles of 64:
+// queries; wave w owns queries 16w..16w+15. KV tokens stream in tiles of TK
+// (32 at head dim 128, 64 at head dim 64):
 //   * K tile (64 x DH) -> LDS, shared by the four waves;
 //   * the tile's packed groups -> a zero-filled, transposed LDS tile
 //     Zt[dim][token] (token pairs packed in one dword);
@@ -44,14 +45,19 @@ constexpr int kWide = 0, kDs4 = 1, kDs2 = 2;
 // capped at 168 so that occupancy, not just the pipeline, hides latency.
 template <int DH, int VM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k_attend_bf16(AttendParams p) {
-  constexpr int TK = 64, MT = DH / 16, KS = DH / 32, KLD = DH + 8, ZLD = TK / 2 + 4;
+  // 32-token tiles at DH = 128 (shorter per-tile chains, 140 registers); 64 at
+  // DH = 64 so that every thread has a value item per tile
+  constexpr int TK = DH == 128 ? 32 : 64, MT = DH / 16, KS = DH / 32, KLD = DH + 8, ZLD = TK / 2 + 4;
+  constexpr int NM2 = TK / 16, NHF = TK / 32;  // 16-token score blocks, 32-token P.V steps
   constexpr int NKP = TK * DH / 8 / 256;          // 16-byte K pieces per thread per tile
   constexpr int NVI = (TK / 2) * (DH / 8) / 256;  // (token pair, 8-dim chunk) items per thread
   constexpr int RLD = DH + 8;  // padded rows: conflict-free fragment reads per half-wave
-  // R_h is needed only after the key loop: it reuses the K / value tile space,
-  // which keeps the workgroup at about 36 KB of LDS
-  constexpr int KB = TK * KLD * 2, ZB = DH * ZLD * 4, RB = DH * RLD * 2;
-  __shared__ __attribute__((aligned(16))) char smem[KB + ZB > RB ? KB + ZB : RB];
+  // R_h is needed only after the key loop and the output staging only after
+  // R_h: both reuse the K / value tile space (about 35 KB of LDS at DH = 128)
+  constexpr int KB = TK * KLD * 2, ZB = DH * ZLD * 4, RB = DH * RLD * 2, SB = 4 * 16 * DH * 4;
+  constexpr int SMEM = KB + ZB > RB ? (KB + ZB > SB ? KB + ZB : SB) : (RB > SB ? RB : SB);
+  static_assert(NKP >= 1 && NVI >= 1 && NHF >= 1, "tile shape");
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
   bf16* Ks = reinterpret_cast<bf16*>(smem);
   uint32_t* Zt = reinterpret_cast<uint32_t*>(smem + KB);
   bf16* Rs = reinterpret_cast<bf16*>(smem);
@@ -200,9 +206,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     load_meta(t0 + 2 * TK, mreg, oreg);
 
     // ---- S^T = K Q^T (rows: tile tokens 16*m2 + 4*g4 + i; column: this lane's query)
-    f32x4 s[4];
+    f32x4 s[NM2];
 #pragma unroll
-    for (int m2 = 0; m2 < 4; ++m2) {
+    for (int m2 = 0; m2 < NM2; ++m2) {
       s[m2] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -213,7 +219,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     // ---- online softmax (base 2)
     float mx = -INFINITY;
 #pragma unroll
-    for (int m2 = 0; m2 < 4; ++m2)
+    for (int m2 = 0; m2 < NM2; ++m2)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int t = t0 + 16 * m2 + 4 * g4 + i;
@@ -226,9 +232,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     const float m_new = fmaxf(m_run, mx);
     const float alpha = exp2f(m_run - m_new);
     float psum = 0.f;
-    bf16x8 pb[2];
+    bf16x8 pb[NHF];
 #pragma unroll
-    for (int m2 = 0; m2 < 4; ++m2)
+    for (int m2 = 0; m2 < NM2; ++m2)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float pr = exp2f(s[m2][i] - m_new);
@@ -237,13 +243,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       }
     l_run = l_run * alpha + psum;
     m_run = m_new;
-    // ---- O^T += Z~^T P^T, two 32-token halves
+    // ---- O^T += Z~^T P^T, one MFMA per 32 tokens
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       const uint32_t* zr = Zt + (16 * m + l16) * ZLD + 2 * g4;
       f32x4 a = acc[m] * alpha;
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
+      for (int hf = 0; hf < NHF; ++hf) {
         const u32x2 lo = *reinterpret_cast<const u32x2*>(zr + 16 * hf);
         const u32x2 hi = *reinterpret_cast<const u32x2*>(zr + 16 * hf + 8);
         const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
