@@ -51,16 +51,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   constexpr int NM2 = TK / 16, NHF = TK / 32;  // 16-token score blocks, 32-token P.V steps
   constexpr int NKP = TK * DH / 8 / 256;          // 16-byte K pieces per thread per tile
   constexpr int NVI = (TK / 2) * (DH / 8) / 256;  // (token pair, 8-dim chunk) items per thread
-  constexpr int RLD = DH + 8;  // padded rows: conflict-free fragment reads per half-wave
-  // R_h is needed only after the key loop and the output staging only after
-  // R_h: both reuse the K / value tile space (about 35 KB of LDS at DH = 128)
-  constexpr int KB = TK * KLD * 2, ZB = DH * ZLD * 4, RB = DH * RLD * 2, SB = 4 * 16 * DH * 4;
-  constexpr int SMEM = KB + ZB > RB ? (KB + ZB > SB ? KB + ZB : SB) : (RB > SB ? RB : SB);
+  // R_h has its own LDS region, filled by buffer->LDS DMA at the start so its
+  // load overlaps the key loop; rows are unpadded with 16-byte chunks
+  // XOR-swizzled by row (conflict-free fragment reads). The output staging
+  // reuses R_h and the tile buffers after the back-rotation. About 51 KB of
+  // LDS at DH = 128: three workgroups per CU.
+  constexpr int RBY = DH * 2, RCH = RBY / 16;  // bytes and 16-byte chunks per R_h row
+  constexpr int RB = DH * RBY, KB = TK * KLD * 2, ZB = DH * ZLD * 4, SB = 4 * 16 * DH * 4;
+  constexpr int SMEM = RB + KB + ZB > SB ? RB + KB + ZB : SB;
   static_assert(NKP >= 1 && NVI >= 1 && NHF >= 1, "tile shape");
+  static_assert(RB % (4 * 1024) == 0, "R_h splits into whole 1 KB DMA blocks per wave");
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  bf16* Ks = reinterpret_cast<bf16*>(smem);
-  uint32_t* Zt = reinterpret_cast<uint32_t*>(smem + KB);
-  bf16* Rs = reinterpret_cast<bf16*>(smem);
+  char* Rs = smem;
+  bf16* Ks = reinterpret_cast<bf16*>(smem + RB);
+  uint32_t* Zt = reinterpret_cast<uint32_t*>(smem + RB + KB);
   __shared__ uint32_t s_mask[2][TK];
   __shared__ int32_t s_off[2][TK];
   int h, b;
@@ -71,6 +75,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   const int qq = blockIdx.y * 64 + 16 * w + l16;
   const bool qvalid = qq < p.Tq;
 
+  // R_h: wave w brings 1 KB blocks w*NRD .. w*NRD+NRD-1; lane i of a block
+  // lands at byte 16i, which holds global chunk (16i % RBY)/16 ^ (row % RCH)
+  {
+    constexpr int NRD = RB / 1024 / 4;
+    const rsrc_t r_R = make_rsrc(static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH, RB);
+    const uint32_t rbase = lds_addr(Rs);
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+#pragma unroll
+    for (int u = 0; u < NRD; ++u) {
+      const int j = wu * NRD + u;
+      const int byte = 1024 * j + 16 * lane, row = byte / RBY, cp = (byte % RBY) / 16;
+      dma16(r_R, static_cast<uint32_t>(row * RBY + 16 * (cp ^ (row % RCH))), rbase + 1024u * j);
+    }
+  }
   bf16x8 qf[KS];
   {
     const rsrc_t r_q = make_rsrc(static_cast<const bf16*>(p.q) + (static_cast<size_t>(b) * p.Tq * H + h) * DH,
@@ -171,8 +189,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     }
   };
 
-  // ---- prologue: R_h into LDS (coalesced rows, used by the final
-  // back-rotation), metadata of tiles 0 and 1, operands of tile 0
+  // ---- prologue: metadata of tiles 0 and 1, operands of tile 0
   {
     uint32_t m0;
     int32_t o0;
@@ -260,19 +277,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     __syncthreads();
   }
 
-  // ---- R_h into LDS over the (now idle) K / value tiles; the loop ended on a barrier
-  {
-    constexpr int NRP = DH * DH / 8 / 256;  // 16-byte pieces of R_h per thread
-    const rsrc_t r_R = make_rsrc(static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH, DH * DH * 2);
-    u32x4 rv[NRP];
-#pragma unroll
-    for (int r = 0; r < NRP; ++r) rv[r] = bload16(r_R, 16u * (tid + 256 * r));
-#pragma unroll
-    for (int r = 0; r < NRP; ++r) {
-      const int pc = tid + 256 * r;
-      *reinterpret_cast<u32x4*>(Rs + (pc / (DH / 8)) * RLD + 8 * (pc % (DH / 8))) = rv[r];
-    }
-  }
+  // ---- R_h has landed (its DMA was issued before every other load; the loop
+  // ended on a barrier, and this wait plus one more barrier covers all waves)
+  wait_vmcnt<0>();
   __syncthreads();
   // ---- normalise and rotate back: O^T = R_h U^T
   float lsum = l_run + __shfl_xor(l_run, 16, kWave);
@@ -290,11 +297,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     o[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const bf16* rr = Rs + (16 * m + l16) * RLD + 4 * g4;
+    // row 16m + l16, elements 32ks + 4g4 .. +3 and 32ks + 16 + 4g4 .. +3:
+    // byte 8*(g4 & 1) of chunks 4ks + g4/2 and 4ks + 2 + g4/2
+    const int row = 16 * m + l16;
+    const char* rr = Rs + row * RBY + 8 * (g4 & 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const u32x2 lo = *reinterpret_cast<const u32x2*>(rr + 32 * ks);
-      const u32x2 hi = *reinterpret_cast<const u32x2*>(rr + 32 * ks + 16);
+      const u32x2 lo = *reinterpret_cast<const u32x2*>(rr + 16 * ((4 * ks + (g4 >> 1)) ^ (row % RCH)));
+      const u32x2 hi = *reinterpret_cast<const u32x2*>(rr + 16 * ((4 * ks + 2 + (g4 >> 1)) ^ (row % RCH)));
       const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
       o[m] = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), ub[ks], o[m]);
     }
