@@ -121,8 +121,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     m = bload4(r_mask, oob_unless(ok, 4u * t));  // masked to G bits when stored (no wait here)
     o = static_cast<int32_t>(bload4(r_off, oob_unless(ok, 4u * t)));
   };
-  u32x4 kreg[NKP];
-  auto load_k = [&](int t0) {
+  // two register sets (A, B) for tile operands in flight
+  u32x4 kA[NKP], kB[NKP];
+  auto load_k = [&](u32x4 (&kreg)[NKP], int t0) {
 #pragma unroll
     for (int r = 0; r < NKP; ++r) {
       const int pc = tid + 256 * r;
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     }
   };
   // packed groups of 2 tokens x 8 dims for each item, addressed through the LDS masks/offsets
-  u32x4 vreg[NVI][2];
+  u32x4 vA[NVI][2], vB[NVI][2];
   const int64_t cap = p.cap;
   // slots are < 2^31 (the cache per (sample, head) is < 2 GiB); the select is
   // pinned so that no load ends up behind a branch
@@ -142,7 +143,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     const bool ok = tok_ok & (((m >> g) & 1u) != 0u) & (sl < cap32);
     return oob_unless(ok, static_cast<uint32_t>((sl * ds + elem) * 2));
   };
-  auto load_v = [&](int t0, int slot) {
+  auto load_v = [&](u32x4 (&vreg)[NVI][2], int t0, int slot) {
 #pragma unroll
     for (int r = 0; r < NVI; ++r) {
       const int it = tid + 256 * r;
@@ -169,7 +170,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       }
     }
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](const u32x4 (&kreg)[NKP], const u32x4 (&vreg)[NVI][2]) {
 #pragma unroll
     for (int r = 0; r < NKP; ++r) {
       const int pc = tid + 256 * r;
@@ -189,38 +190,51 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     }
   };
 
-  // ---- prologue: metadata of tiles 0 and 1, operands of tile 0
+  // ---- pipeline: the operands of tiles i+1 and i+2 are in flight while
+  // tile i is computed. Tile i+2's packed groups are addressed through its
+  // masks and offsets, which were requested together with tile i's operands,
+  // so each iteration waits only for what was issued two iterations earlier.
+  // Register sets alternate A, B, A, ... (the loop body runs twice per pass;
+  // a second half past the last tile computes a fully masked tile).
+  // Prologue: tile 0's keys (they need no metadata), the metadata of tiles 0
+  // and 1 into LDS, then the rest of tiles 0 and 1 and the metadata of tiles
+  // 2 and 3: the loop is entered with the loads of its back edge outstanding,
+  // in the same order.
+  uint32_t mA, mB;
+  int32_t oA, oB;
+  load_k(kA, 0);
   {
-    uint32_t m0;
-    int32_t o0;
+    uint32_t m0, m1;
+    int32_t o0, o1;
     load_meta(0, m0, o0);
+    load_meta(TK, m1, o1);
     if (tid < TK) {
       s_mask[0][tid] = m0 & gm;
       s_off[0][tid] = o0;
+      s_mask[1][tid] = m1 & gm;
+      s_off[1][tid] = o1;
     }
   }
-  uint32_t mreg;
-  int32_t oreg;
-  load_meta(TK, mreg, oreg);
   __syncthreads();
-  load_k(0);
-  load_v(0, 0);
+  load_v(vA, 0, 0);
+  load_meta(2 * TK, mA, oA);
+  load_k(kB, TK);
+  load_v(vB, TK, 1);
+  load_meta(3 * TK, mB, oB);
 
-  int it = 0;
-  for (int t0 = 0; t0 < T; t0 += TK, ++it) {
-    const int nslot = (it + 1) & 1;
-    store_tile();
-    if (tid < TK) {
-      s_mask[nslot][tid] = mreg & gm;
-      s_off[nslot][tid] = oreg;
+  auto step = [&](int t0, int slot, u32x4 (&kreg)[NKP], u32x4 (&vreg)[NVI][2], uint32_t& mreg, int32_t& oreg) {
+    store_tile(kreg, vreg);
+    if (tid < TK) {  // masks/offsets of tile t0 + 2*TK into this tile's slot
+      s_mask[slot][tid] = mreg & gm;
+      s_off[slot][tid] = oreg;
     }
     __syncthreads();
-    // next tile's operands; past the end every load is out of range (no
+    // operands two tiles ahead; past the end every load is out of range (no
     // memory access), so there is no branch here: a branch around the loads
     // makes the compiler wait on every outstanding load at its join
-    load_k(t0 + TK);
-    load_v(t0 + TK, nslot);
-    load_meta(t0 + 2 * TK, mreg, oreg);
+    load_k(kreg, t0 + 2 * TK);
+    load_v(vreg, t0 + 2 * TK, slot);
+    load_meta(t0 + 4 * TK, mreg, oreg);
 
     // ---- S^T = K Q^T (rows: tile tokens 16*m2 + 4*g4 + i; column: this lane's query)
     f32x4 s[NM2];
@@ -275,6 +289,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       acc[m] = a;
     }
     __syncthreads();
+  };
+  for (int t0 = 0; t0 < T; t0 += 2 * TK) {
+    step(t0, 0, kA, vA, mA, oA);
+    step(t0 + TK, 1, kB, vB, mB, oB);
   }
 
   // ---- R_h has landed (its DMA was issued before every other load; the loop
