@@ -17,25 +17,26 @@ __device__ __forceinline__ uint32_t group_mask(int G) { return G >= 32 ? 0xFFFFF
 
 // ---------------------------------------------------------------------------
 // bf16 matrix-core kernel. One workgroup = one (sample, head) and up to 64
-// queries; wave w owns queries 16w..16w+15. KV tokens stream in tiles of TK
-// (32 at head dim 128, 64 at head dim 64):
-//   * K tile (64 x DH) -> LDS, shared by the four waves;
+// queries; wave w owns queries 16w..16w+15. R_h is brought into LDS by DMA at
+// the start. KV tokens stream in tiles of TK (32 at head dim 128, 64 at head
+// dim 64):
+//   * K tile (TK x DH) -> LDS, shared by the four waves;
 //   * the tile's packed groups -> a zero-filled, transposed LDS tile
 //     Zt[dim][token] (token pairs packed in one dword);
 //   * S^T = K Q^T on MFMA (queries are the B operand held in registers), so
-//     each lane owns one query column and 16 token rows;
-//   * online softmax per query: 16 values in-lane, then 2 cross-lane steps;
+//     each lane owns one query column and TK/4 token rows;
+//   * online softmax per query: in-lane, then 2 cross-lane steps, against a
+//     reference that lags the running maximum by at most kSlack;
 //   * O^T += Z~^T P^T on MFMA. The lane's own softmax values form the P^T
 //     fragment directly once the A fragment lists its tokens in the same
-//     order (tokens 4q..4q+3 and 16+4q..16+4q+3 of each 32-token half).
-// Loads are software-pipelined: while tile i is computed from LDS, the K rows
-// and packed groups of tile i+1 are in flight into registers, and the group
-// masks and cache offsets of tile i+2 (which address tile i+2's packed groups)
-// are in flight too.
-// After the last tile R_h is staged into LDS over the tile buffers
-// (coalesced 16-byte rows), O^T = R_h U^T is one more MFMA chain (U in bf16,
-// R_h fragments from LDS) and each lane stores 4 consecutive outputs of its
-// query.
+//     order (tokens 4q..4q+3 and 16+4q..16+4q+3 of each 32 tokens).
+// Loads are software-pipelined two tiles deep: while tile i is computed from
+// LDS, the K rows and packed groups of tiles i+1 and i+2 are in flight into
+// registers, and the masks and cache offsets that address tile i+2's packed
+// groups arrived with tile i's operands.
+// After the last tile, O^T = R_h U^T is one more MFMA chain (U in bf16, R_h
+// fragments from LDS), and each wave stages its 16 output rows in LDS and
+// writes them as whole 16-byte units.
 // VM: how the 8-dim chunks of the value tile map to packed groups:
 //   kWide  groups of >= 8 dims (one 16-byte load per token and chunk)
 //   kDs4   4-dim groups (two 8-byte loads), kDs2  2-dim groups (four 4-byte loads)
@@ -102,7 +103,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
 #pragma unroll
   for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
-  const float sl2 = p.scale * 1.4426950408889634f;  // softmax in base 2
+  // softmax in base 2 with a positive factor: a negative scale is applied by
+  // negating the queries (exact in bf16), once they have arrived
+  const float sl2 = fabsf(p.scale) * 1.4426950408889634f;
+  constexpr float kSlack = 8.f;  // the softmax reference lags the running maximum by at most this (log2)
 
   // Buffer resources: a masked or out-of-range element loads as zero with no
   // memory access, so every load below is unconditional.
@@ -216,11 +220,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     }
   }
   __syncthreads();
+  if (p.scale < 0.f) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[ks] = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, qf[ks]) ^ u32x4{0x80008000u, 0x80008000u,
+                                                                                   0x80008000u, 0x80008000u});
+  }
   load_v(vA, 0, 0);
   load_meta(2 * TK, mA, oA);
   load_k(kB, TK);
   load_v(vB, TK, 1);
   load_meta(3 * TK, mB, oB);
+  // every wave has read slots 0 and 1 (tiles 0 and 1) before the first step
+  // overwrites slot 0 with tile 2's metadata
+  __syncthreads();
 
   auto step = [&](int t0, int slot, u32x4 (&kreg)[NKP], u32x4 (&vreg)[NVI][2], uint32_t& mreg, int32_t& oreg) {
     store_tile(kreg, vreg);
@@ -247,38 +260,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
         s[m2] = mfma_16x16x32(a, qf[ks], s[m2]);
       }
     }
-    // ---- online softmax (base 2)
+    // ---- online softmax (base 2) with a lazily moved reference: scores are
+    // taken relative to m_run, which moves only when a tile's maximum exceeds
+    // it by more than kSlack (then acc and l_run are rescaled, for the whole
+    // wave at once). Softmax does not depend on the reference, P stays below
+    // 2^kSlack, and most tiles skip the rescale. Scores past T (only in the
+    // last tile) are masked to -inf.
     float mx = -INFINITY;
+    if (t0 + TK <= T) {
 #pragma unroll
-    for (int m2 = 0; m2 < NM2; ++m2)
+      for (int m2 = 0; m2 < NM2; ++m2)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int t = t0 + 16 * m2 + 4 * g4 + i;
-        const float x = t < T ? s[m2][i] * sl2 : -INFINITY;
-        s[m2][i] = x;
-        mx = fmaxf(mx, x);
-      }
+        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[m2][i]);
+    } else {
+#pragma unroll
+      for (int m2 = 0; m2 < NM2; ++m2)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = t0 + 16 * m2 + 4 * g4 + i;
+          s[m2][i] = t < T ? s[m2][i] : -INFINITY;
+          mx = fmaxf(mx, s[m2][i]);
+        }
+    }
     mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
     mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
+    const float m_cand = fmaxf(m_run, mx * sl2);  // sl2 >= 0
+    if (__builtin_amdgcn_ballot_w64(m_cand > m_run + kSlack) != 0) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_cand);  // 0 on the first tile
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m] *= alpha;
+      l_run *= alpha;
+      m_run = m_cand;
+    }
     float psum = 0.f;
     bf16x8 pb[NHF];
 #pragma unroll
     for (int m2 = 0; m2 < NM2; ++m2)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float pr = exp2f(s[m2][i] - m_new);
+        const float pr = __builtin_amdgcn_exp2f(fmaf(s[m2][i], sl2, -m_run));
         psum += pr;
         pb[m2 >> 1][4 * (m2 & 1) + i] = static_cast<bf16>(pr);
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+    l_run += psum;
     // ---- O^T += Z~^T P^T, one MFMA per 32 tokens
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       const uint32_t* zr = Zt + (16 * m + l16) * ZLD + 2 * g4;
-      f32x4 a = acc[m] * alpha;
+      f32x4 a = acc[m];
 #pragma unroll
       for (int hf = 0; hf < NHF; ++hf) {
         const u32x2 lo = *reinterpret_cast<const u32x2*>(zr + 16 * hf);

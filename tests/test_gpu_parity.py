@@ -227,6 +227,17 @@ def test_attend(cid, B, T, Tq, H, dh, G):
     assert err <= TOL[w.dtype]
 
 
+def test_attend_stack_layer_shape():
+    # the 7B-stack layer shape with its per-type kept counts (4 of 8 groups for
+    # 128 visual tokens, 6 for 48 language tokens, all 8 for the proprio token)
+    w = synth.workload(4)
+    counts = np.array([4] * 128 + [6] * 48 + [8])
+    got, ref, _ = _attend_case(w, 4, 177, 56, 32, 128, 8, counts=counts)
+    err = max_rel(got, ref)
+    _say(f"attend 7B-stack layer shape, B=4: max rel err {err:.2e}")
+    assert err <= TOL[w.dtype]
+
+
 @pytest.mark.parametrize("B,H", [(2, 16), (70, 8)])
 def test_attend_f32_output_from_bf16(B, H):
     w = synth.workload(2)
@@ -401,6 +412,14 @@ def test_pipeline_stack_full_batch_sampled(layer):
     cnt = host(bufs.count)
     assert np.all(cnt[:, :w.n_vis] == w.k_vis) and np.all(cnt[:, w.n_vis:w.n_vis + w.n_lang] == w.k_lang)
     assert np.all(host(bufs.offsets)[:, -1] == cap)
+    if layer == 0:
+        # attention at full size is bitwise repeatable (no workgroup may read
+        # metadata or tiles that another wave is still replacing)
+        R = put(wt["R"], tdtype(w))
+        for rep in range(24):
+            again = rs.attend(acts["q"], acts["k"], bufs.mask, bufs.offsets, bufs.Vp, R, w.G)
+            torch.cuda.synchronize()
+            assert torch.equal(again, bufs.out), f"attend repeat {rep} differs"
 
 
 def test_pipeline_stress_full_batch_sampled():
