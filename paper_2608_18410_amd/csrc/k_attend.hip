@@ -15,6 +15,21 @@ namespace {
 
 __device__ __forceinline__ uint32_t group_mask(int G) { return G >= 32 ? 0xFFFFFFFFu : ((1u << G) - 1u); }
 
+// Scheduling of N LDS fragment reads feeding N MFMAs: the reads run two MFMAs
+// ahead (left to itself the compiler reuses one register set and waits on
+// every read).
+template <int N>
+__device__ __forceinline__ void sched_reads_ahead() {
+  constexpr int kDsRead = 0x100, kMfma = 0x008;
+  __builtin_amdgcn_sched_group_barrier(kDsRead, N < 2 ? N : 2, 0);
+#pragma unroll
+  for (int i = 0; i + 2 < N; ++i) {
+    __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(kMfma, N < 2 ? N : 2, 0);
+}
+
 // ---------------------------------------------------------------------------
 // bf16 matrix-core kernel. One workgroup = one (sample, head) and up to 64
 // queries; wave w owns queries 16w..16w+15. R_h is brought into LDS by DMA at
@@ -251,14 +266,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
 
     // ---- S^T = K Q^T (rows: tile tokens 16*m2 + 4*g4 + i; column: this lane's query)
     f32x4 s[NM2];
+    {
+      // fragment i = (ks, m2) with m2 fastest: the NM2 accumulation chains alternate
+      bf16x8 kf[NM2 * KS];
 #pragma unroll
-    for (int m2 = 0; m2 < NM2; ++m2) {
-      s[m2] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int i = 0; i < NM2 * KS; ++i)
+        kf[i] = *reinterpret_cast<const bf16x8*>(Ks + (16 * (i % NM2) + l16) * KLD + 32 * (i / NM2) + 8 * g4);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(Ks + (16 * m2 + l16) * KLD + 32 * ks + 8 * g4);
-        s[m2] = mfma_16x16x32(a, qf[ks], s[m2]);
-      }
+      for (int m2 = 0; m2 < NM2; ++m2) s[m2] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < NM2 * KS; ++i) s[i % NM2] = mfma_16x16x32(kf[i], qf[i / NM2], s[i % NM2]);
+      sched_reads_ahead<NM2 * KS>();
     }
     // ---- online softmax (base 2) with a lazily moved reference: scores are
     // taken relative to m_run, which moves only when a tile's maximum exceeds
@@ -304,18 +322,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       }
     l_run += psum;
     // ---- O^T += Z~^T P^T, one MFMA per 32 tokens
+    {
+      u32x4 zf[MT * NHF];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      const uint32_t* zr = Zt + (16 * m + l16) * ZLD + 2 * g4;
-      f32x4 a = acc[m];
-#pragma unroll
-      for (int hf = 0; hf < NHF; ++hf) {
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(zr + 16 * hf);
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(zr + 16 * hf + 8);
-        const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
-        a = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), pb[hf], a);
+      for (int i = 0; i < MT * NHF; ++i) {
+        const uint32_t* zr = Zt + (16 * (i / NHF) + l16) * ZLD + 2 * g4 + 16 * (i % NHF);
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(zr);
+        const u32x2 hi = *reinterpret_cast<const u32x2*>(zr + 8);
+        zf[i] = u32x4{lo[0], lo[1], hi[0], hi[1]};
       }
-      acc[m] = a;
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int hf = 0; hf < NHF; ++hf)
+          acc[m] = mfma_16x16x32(__builtin_bit_cast(bf16x8, zf[m * NHF + hf]), pb[hf], acc[m]);
+      sched_reads_ahead<MT * NHF>();
     }
     __syncthreads();
   };
