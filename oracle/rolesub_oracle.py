@@ -20,7 +20,9 @@ notes of the repository):
   * router "additive": the paper's routing-score equation with linear heads;
   * top-K ties go to the lower group index, -0 equals +0, NaN ranks lowest;
   * threshold budgets keep count(gamma > tau) groups clamped to [kmin, kmax];
-  * attention: scale 1/sqrt(dh), no mask, keys unchanged, routed values.
+  * attention: scale 1/sqrt(dh), no mask, keys unchanged, routed values;
+  * prefix self-attention: the prefix tokens are the queries, query t sees
+    keys 0..t (causal), keys unchanged, routed values.
 
 Parity: every function here is pinned by CPU tests against closed forms, the
 paper's printed KV fractions, brute-force enumeration and textbook special
@@ -38,6 +40,7 @@ __all__ = [
     "VIS", "LANG", "PROP", "ACT", "TOPK", "THRESHOLD",
     "rotate", "back_rotate", "latent_role", "language_pool", "gelu",
     "router_mlp2", "router_additive", "group_budget", "select_groups",
+    "attend_packed_causal", "attend_plain_causal",
     "mask_to_idx", "popcount", "pack", "unpack", "expand_mask", "routed_values",
     "attend_packed", "attend_plain", "softmax", "pipeline",
     "kv_fraction", "packed_groups",
@@ -314,6 +317,37 @@ def attend_packed(q, k, mask, offsets, Vp, R, G, scale=None):
     p = softmax(s, axis=-1)
     u = np.einsum("bhqt,bthd->bqhd", p, zt)
     return back_rotate(u, R)
+
+
+def _causal_scores(q, k, scale):
+    q, k = _f64(q), _f64(k)
+    B, T, H, dh = q.shape
+    s = np.einsum("bqhd,bthd->bhqt", q, k) * _scale(dh, scale)
+    future = np.triu(np.ones((T, T), dtype=bool), k=1)            # key index > query index
+    s[:, :, future] = -np.inf
+    return s
+
+
+def attend_packed_causal(q, k, mask, offsets, Vp, R, G, scale=None):
+    """Prefix self-attention over the routed cache (Sec. 3, Sec. 3.2): the T prefix
+    tokens are the queries and query t attends keys 0..t; softmax over those
+    keys, P.V in the rotated space over each token's kept groups, o = R_h u.
+
+    q, k [B,T,H,dh], mask [B,T], offsets [B,T+1], Vp [B,H,cap,ds], R [H,dh,dh].
+    Returns [B,T,H,dh] float64."""
+    T = _f64(k).shape[1]
+    zt = unpack(offsets, Vp, mask, G, T)
+    p = softmax(_causal_scores(q, k, scale), axis=-1)
+    u = np.einsum("bhqt,bthd->bqhd", p, zt)
+    return back_rotate(u, R)
+
+
+def attend_plain_causal(q, k, v, mask, R, G, scale=None):
+    """Plain form of the prefix self-attention: causal textbook attention whose
+    values are the explicit routed values v~_i = R M_i R^T v_i (Sec. 3.2)."""
+    vt = routed_values(v, mask, R, G)
+    p = softmax(_causal_scores(q, k, scale), axis=-1)
+    return np.einsum("bhqt,bthd->bqhd", p, vt)
 
 
 def attend_plain(q, k, v, mask, R, G, scale=None):

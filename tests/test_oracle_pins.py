@@ -422,6 +422,59 @@ def test_attend_method_form_equals_plain_form():
     assert np.max(np.abs(a - b)) < 1e-12
 
 
+# ----------------------------------------------------------------------------
+# Prefix self-attention (causal) over the routed values
+# ----------------------------------------------------------------------------
+
+def _causal_case(seed=11, B=2, T=9, H=2, dh=64, G=8):
+    q, k, v, R = _attn_case(B=B, T=T, Tq=T, H=H, dh=dh, G=G, seed=seed)
+    m = np.random.default_rng(seed).integers(0, 1 << G, size=(B, T)).astype(np.uint32)
+    off, Vp = O.pack(O.rotate(v, R), m, G, T * G)
+    return q, k, v, R, m, off, Vp
+
+
+def test_attend_causal_row_t_is_attention_over_the_first_t_plus_1_tokens():
+    q, k, v, R, m, off, Vp = _causal_case()
+    G, T = 8, 9
+    out = O.attend_packed_causal(q, k, m, off, Vp, R, G)
+    for t in range(T):
+        # the prefix 0..t packs to the same slots (offsets are prefix sums)
+        ref = O.attend_packed(q[:, t:t + 1], k[:, :t + 1], m[:, :t + 1], off[:, :t + 2], Vp, R, G)
+        assert np.max(np.abs(out[:, t:t + 1] - ref)) < 1e-12
+
+
+def test_attend_causal_first_query_returns_its_routed_value():
+    q, k, v, R, m, off, Vp = _causal_case(seed=12)
+    G, dh = 8, 64
+    out = O.attend_packed_causal(q, k, m, off, Vp, R, G)
+    for b in range(2):
+        M = np.diag(np.repeat([(int(m[b, 0]) >> s) & 1 for s in range(G)], dh // G).astype(float))
+        for h in range(2):
+            assert np.allclose(out[b, 0, h], R[h] @ M @ R[h].T @ v[b, 0, h], atol=1e-12)
+
+
+def test_attend_causal_all_groups_is_textbook_causal_attention():
+    q, k, v, R = _attn_case(B=2, T=10, Tq=10, H=2, dh=64, seed=13)
+    G = 8
+    m = np.full((2, 10), (1 << G) - 1, dtype=np.uint32)
+    off, Vp = O.pack(O.rotate(v, R), m, G, 10 * G)
+    out = O.attend_packed_causal(q, k, m, off, Vp, R, G)
+    for b in range(2):
+        for h in range(2):
+            for t in range(10):
+                s = k[b, :t + 1, h] @ q[b, t, h] / math.sqrt(64)
+                p = np.exp(s - s.max())
+                p /= p.sum()
+                assert np.allclose(out[b, t, h], p @ v[b, :t + 1, h], atol=1e-12)
+
+
+def test_attend_causal_method_form_equals_plain_form():
+    q, k, v, R, m, off, Vp = _causal_case(seed=14, T=12)
+    a = O.attend_packed_causal(q, k, m, off, Vp, R, 8)
+    b = O.attend_plain_causal(q, k, v, m, R, 8)
+    assert np.max(np.abs(a - b)) < 1e-12
+
+
 def test_routed_value_is_a_projection():
     _, _, v, R = _attn_case(T=20, seed=9)
     G = 8
