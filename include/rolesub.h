@@ -201,6 +201,25 @@ rolesub_status rolesub_attend(const rolesub_dims* dims, rolesub_dtype dtype, int
                               const void* R, float scale, void* out, rolesub_dtype out_dtype,
                               void* workspace, size_t ws_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * rolesub_attend_causal: prefix self-attention over the routed values. In the
+ * single forward pass the T prefix tokens are also queries (Sec. 3: queries
+ * and keys unchanged; Sec. 3.2: routed values); query t sees keys 0..t:
+ *   s[t,i] = scale * <q_t, k_i> for i <= t
+ *   P      = softmax_{i <= t}(s)
+ *   u_t    = sum_{i <= t} P[t,i] * (M_i z_i)
+ *   out_t  = R_h u_t
+ *   q, k [B,T,H,dh] (dtype; q holds the prefix tokens' queries); mask,
+ *   offsets, Vp, cap_groups, R, scale, workspace and errors as for
+ *   rolesub_attend; out [B,T,H,dh] in out_dtype (f32 or the call's dtype).
+ * T = 0 or B = 0 does nothing and returns OK.
+ * ------------------------------------------------------------------------ */
+rolesub_status rolesub_attend_causal(const rolesub_dims* dims, rolesub_dtype dtype, const void* q,
+                                     const void* k, const uint32_t* mask, const int32_t* offsets,
+                                     const void* Vp, int64_t cap_groups, const void* R, float scale,
+                                     void* out, rolesub_dtype out_dtype, void* workspace,
+                                     size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -89,6 +89,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   const int T = p.T, H = p.H, G = p.G, ds = DH / G;
   const uint32_t gm = group_mask(G);
   const int qq = blockIdx.y * 64 + 16 * w + l16;
+  const int q_first = blockIdx.y * 64 + 16 * __builtin_amdgcn_readfirstlane(w);  // this wave's first query
   const bool qvalid = qq < p.Tq;
 
   // R_h: wave w brings 1 KB blocks w*NRD .. w*NRD+NRD-1; lane i of a block
@@ -285,7 +286,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     // 2^kSlack, and most tiles skip the rescale. Scores past T (only in the
     // last tile) are masked to -inf.
     float mx = -INFINITY;
-    if (t0 + TK <= T) {
+    // full tile: inside T and, for prefix self-attention, entirely before this
+    // wave's first query
+    if (t0 + TK <= T && (!p.causal || t0 + TK - 1 <= q_first)) {
 #pragma unroll
       for (int m2 = 0; m2 < NM2; ++m2)
 #pragma unroll
@@ -296,7 +299,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int t = t0 + 16 * m2 + 4 * g4 + i;
-          s[m2][i] = t < T ? s[m2][i] : -INFINITY;
+          s[m2][i] = (t < T) & (!p.causal | (t <= qq)) ? s[m2][i] : -INFINITY;
           mx = fmaxf(mx, s[m2][i]);
         }
     }
@@ -340,7 +343,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     }
     __syncthreads();
   };
-  for (int t0 = 0; t0 < T; t0 += 2 * TK) {
+  // prefix self-attention: keys past this block's last query are all masked
+  const int t_stop = p.causal ? min(T, static_cast<int>(blockIdx.y) * 64 + 64) : T;
+  for (int t0 = 0; t0 < t_stop; t0 += 2 * TK) {
     step(t0, 0, kA, vA, mA, oA);
     step(t0 + TK, 1, kB, vB, mB, oB);
   }
@@ -441,7 +446,8 @@ __global__ __launch_bounds__(128) void k_attend_generic(AttendParams p) {
   const float qj = tof(qv[j]);
   float m = -INFINITY, l = 0.f, u = 0.f;
   const int nw = (dh + 63) / 64;
-  for (int t = 0; t < T; ++t) {
+  const int t_stop = p.causal ? min(T, qi + 1) : T;
+  for (int t = 0; t < t_stop; ++t) {
     float part = qj * tof(kv[((static_cast<size_t>(b) * T + t) * H + h) * dh + j]);
     part = wave_sum(part);
     if (nw > 1) {

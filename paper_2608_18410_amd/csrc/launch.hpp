@@ -80,6 +80,7 @@ struct AttendParams {
   float scale;
   void* out;
   int out_f32;
+  int causal;  // prefix self-attention: Tq == T and query t sees keys 0..t
 };
 hipError_t launch_attend(const AttendParams& p, bool bf16, hipStream_t s);
 

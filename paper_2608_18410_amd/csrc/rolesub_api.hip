@@ -312,11 +312,11 @@ size_t rolesub_attend_workspace_size(const rolesub_dims* dims, int32_t Tq) {
   return 0;
 }
 
-rolesub_status rolesub_attend(const rolesub_dims* dims, rolesub_dtype dtype, int32_t Tq, const void* q,
-                              const void* k, const uint32_t* mask, const int32_t* offsets, const void* Vp,
-                              int64_t cap_groups, const void* R, float scale, void* out,
-                              rolesub_dtype out_dtype, void* workspace, size_t ws_bytes, void* stream) {
-  const char* fn = "rolesub_attend";
+static rolesub_status attend_call(const char* fn, bool causal, const rolesub_dims* dims, rolesub_dtype dtype,
+                                  int32_t Tq, const void* q, const void* k, const uint32_t* mask,
+                                  const int32_t* offsets, const void* Vp, int64_t cap_groups, const void* R,
+                                  float scale, void* out, rolesub_dtype out_dtype, void* workspace,
+                                  size_t ws_bytes, void* stream) {
   (void)workspace;
   (void)ws_bytes;
   rolesub_status st = check_value_dims(dims, fn);
@@ -356,7 +356,28 @@ rolesub_status rolesub_attend(const rolesub_dims* dims, rolesub_dtype dtype, int
   p.scale = scale == 0.f ? 1.f / std::sqrt(static_cast<float>(dims->dh)) : scale;
   p.out = out;
   p.out_f32 = out_dtype == ROLESUB_F32;
+  p.causal = causal ? 1 : 0;
   return from_hip(launch_attend(p, dtype == ROLESUB_BF16, static_cast<hipStream_t>(stream)), fn);
+}
+
+rolesub_status rolesub_attend(const rolesub_dims* dims, rolesub_dtype dtype, int32_t Tq, const void* q,
+                              const void* k, const uint32_t* mask, const int32_t* offsets, const void* Vp,
+                              int64_t cap_groups, const void* R, float scale, void* out,
+                              rolesub_dtype out_dtype, void* workspace, size_t ws_bytes, void* stream) {
+  return attend_call("rolesub_attend", false, dims, dtype, Tq, q, k, mask, offsets, Vp, cap_groups, R, scale, out,
+                     out_dtype, workspace, ws_bytes, stream);
+}
+
+rolesub_status rolesub_attend_causal(const rolesub_dims* dims, rolesub_dtype dtype, const void* q,
+                                     const void* k, const uint32_t* mask, const int32_t* offsets,
+                                     const void* Vp, int64_t cap_groups, const void* R, float scale,
+                                     void* out, rolesub_dtype out_dtype, void* workspace, size_t ws_bytes,
+                                     void* stream) {
+  const char* fn = "rolesub_attend_causal";
+  if (!dims) return fail(ROLESUB_ERR_INVALID_ARG, "%s: dims is NULL", fn);
+  if (dims->T == 0) return ROLESUB_OK;  // no prefix tokens, no queries
+  return attend_call(fn, true, dims, dtype, dims->T, q, k, mask, offsets, Vp, cap_groups, R, scale, out,
+                     out_dtype, workspace, ws_bytes, stream);
 }
 
 }  // extern "C"

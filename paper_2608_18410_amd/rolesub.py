@@ -24,6 +24,7 @@ EXPORTS = (
     "rolesub_status_str", "rolesub_last_error", "rolesub_version",
     "rolesub_rotate_values", "rolesub_route_workspace_size", "rolesub_route",
     "rolesub_pack_kv", "rolesub_rotate_pack", "rolesub_attend_workspace_size", "rolesub_attend",
+    "rolesub_attend_causal",
 )
 
 
@@ -78,6 +79,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rolesub_attend_workspace_size.restype = SZ
     lib.rolesub_attend.argtypes = [P, ctypes.c_int, I32, P, P, P, P, P, I64, P, ctypes.c_float, P,
                                    ctypes.c_int, P, SZ, P]
+    lib.rolesub_attend_causal.argtypes = [P, ctypes.c_int, P, P, P, P, P, I64, P, ctypes.c_float, P,
+                                          ctypes.c_int, P, SZ, P]
     for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_rotate_pack",
                "rolesub_attend"):
         getattr(lib, fn).restype = ctypes.c_int
@@ -257,6 +260,21 @@ def attend(q, k, mask, offsets, Vp, R, G: int, scale: float = 0.0, out_dtype=Non
     dims = Dims(B, T, H, dh, G, 0)
     _check("rolesub_attend", load().rolesub_attend(
         ctypes.byref(dims), _code(q), Tq, _ptr(q), _ptr(k, q.dtype), _ptr(mask), _ptr(offsets, torch.int32),
+        _ptr(Vp, q.dtype), int(cap), _ptr(R, q.dtype), float(scale), _ptr(o), _code(o), None, 0,
+        _stream(stream)))
+    return o
+
+
+def attend_causal(q, k, mask, offsets, Vp, R, G: int, scale: float = 0.0, out_dtype=None, out=None, stream=None):
+    """Prefix self-attention over the packed routed values (query t sees keys
+    0..t); q and k are [B,T,H,dh]; returns [B,T,H,dh]."""
+    B, T, H, dh = q.shape
+    cap = Vp.shape[2]
+    odt = q.dtype if out_dtype is None else out_dtype
+    o = torch.empty((B, T, H, dh), dtype=odt, device=q.device) if out is None else out
+    dims = Dims(B, T, H, dh, G, 0)
+    _check("rolesub_attend_causal", load().rolesub_attend_causal(
+        ctypes.byref(dims), _code(q), _ptr(q), _ptr(k, q.dtype), _ptr(mask), _ptr(offsets, torch.int32),
         _ptr(Vp, q.dtype), int(cap), _ptr(R, q.dtype), float(scale), _ptr(o), _code(o), None, 0,
         _stream(stream)))
     return o

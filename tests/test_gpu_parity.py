@@ -227,6 +227,57 @@ def test_attend(cid, B, T, Tq, H, dh, G):
     assert err <= TOL[w.dtype]
 
 
+def _attend_causal_case(w, B, T, H, dh, G, counts=None, out_dtype=None, seed=0):
+    w = w.replace(B=B, n_vis=T, n_lang=0, n_prop=0, Tq=T, H=H, dh=dh, G=G)
+    dt = tdtype(w)
+    acts = [synth.sample_activations(w, seed, b, ("q", "k")) for b in range(B)]
+    q = np.stack([a["q"] for a in acts])
+    k = np.stack([a["k"] for a in acts])
+    z = np.stack([synth.synthetic_z(w, seed, b) for b in range(B)])
+    m = np.stack([synth.synthetic_masks(w, seed, b, counts=counts) for b in range(B)])
+    R = synth.layer_weights(w, seed)["R"]
+    cap = T * G
+    off, Vp = rs.pack_kv(put(z, dt), put_mask(m), G, cap)
+    out = rs.attend_causal(put(q, dt), put(k, dt), put_mask(m), off, Vp, put(R, dt), G, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    o_ref, Vp_ref = O.pack(z, m, G, cap)
+    ref = O.attend_packed_causal(q, k, m, o_ref, Vp_ref, R, G)
+    return host(out), ref
+
+
+@pytest.mark.parametrize("cid,B,T,H,dh,G", [
+    (1, 1, 80, 4, 64, 8),              # tiny f32 (vector kernel)
+    (1, 2, 33, 4, 128, 4),             # f32, head dim 128
+    (2, 1, 305, 32, 128, 8),           # 7B layer shape: 5 query blocks, ragged T
+    (3, 3, 113, 8, 128, 8),
+    (5, 2, 150, 8, 128, 32),           # 4-dim groups
+    (3, 2, 97, 8, 64, 8),              # head dim 64
+    (3, 2, 65, 4, 64, 32),             # 2-dim groups
+    (3, 2, 32, 4, 128, 8),             # one full tile
+    (3, 2, 33, 4, 128, 8),             # a tile plus one token
+    (3, 3, 1, 4, 128, 8),              # one token: its own routed value
+])
+def test_attend_causal(cid, B, T, H, dh, G):
+    w = synth.workload(cid)
+    counts = np.random.default_rng(T + 7).integers(0, G + 1, size=T)
+    counts[0] = max(int(counts[0]), 1)
+    got, ref = _attend_causal_case(w, B, T, H, dh, G, counts=counts)
+    err = max_rel(got, ref)
+    _say(f"attend_causal {w.dtype} B={B} T={T} H={H} dh={dh} G={G}: max rel err {err:.2e}")
+    assert err <= TOL[w.dtype]
+
+
+def test_attend_causal_stack_shape_and_f32_output():
+    w = synth.workload(4)
+    counts = np.array([4] * 128 + [6] * 48 + [8])
+    got, ref = _attend_causal_case(w, 2, 177, 32, 128, 8, counts=counts)
+    err = max_rel(got, ref)
+    _say(f"attend_causal 7B-stack shape B=2: max rel err {err:.2e}")
+    assert err <= TOL[w.dtype]
+    got, ref = _attend_causal_case(w, 2, 177, 8, 128, 8, counts=counts, out_dtype=torch.float32)
+    assert max_rel(got, ref) <= TOL[w.dtype]
+
+
 def test_attend_stack_layer_shape():
     # the 7B-stack layer shape with its per-type kept counts (4 of 8 groups for
     # 128 visual tokens, 6 for 48 language tokens, all 8 for the proprio token)
