@@ -84,12 +84,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   __shared__ uint32_t s_mask[2][TK];
   __shared__ int32_t s_off[2][TK];
   int h, b;
-  xcd_split(blockIdx.x, p.H, h, b);
+  // 1D grid of (sample, head) items x query blocks. When B*H is a multiple of
+  // 8 the query blocks of one item are consecutive workgroups of one XCD, so
+  // the blocks after the first find the item's keys and values in that L2.
+  int qb;
+  {
+    const int nqb = (p.Tq + 63) / 64, lin = blockIdx.x;
+    int item;
+    if ((p.B * p.H) % 8 == 0) {
+      const int xcd = lin & 7, slot = lin >> 3;
+      item = (slot / nqb) * 8 + xcd;
+      qb = slot % nqb;
+    } else {
+      item = lin / nqb;
+      qb = lin % nqb;
+    }
+    xcd_split(item, p.H, h, b);
+  }
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
   const int T = p.T, H = p.H, G = p.G, ds = DH / G;
   const uint32_t gm = group_mask(G);
-  const int qq = blockIdx.y * 64 + 16 * w + l16;
-  const int q_first = blockIdx.y * 64 + 16 * __builtin_amdgcn_readfirstlane(w);  // this wave's first query
+  const int qq = qb * 64 + 16 * w + l16;
+  const int q_first = qb * 64 + 16 * __builtin_amdgcn_readfirstlane(w);  // this wave's first query
   const bool qvalid = qq < p.Tq;
 
   // R_h: wave w brings 1 KB blocks w*NRD .. w*NRD+NRD-1; lane i of a block
@@ -344,7 +360,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     __syncthreads();
   };
   // prefix self-attention: keys past this block's last query are all masked
-  const int t_stop = p.causal ? min(T, static_cast<int>(blockIdx.y) * 64 + 64) : T;
+  const int t_stop = p.causal ? min(T, qb * 64 + 64) : T;
   for (int t0 = 0; t0 < t_stop; t0 += 2 * TK) {
     step(t0, 0, kA, vA, mA, oA);
     step(t0 + TK, 1, kB, vB, mB, oB);
@@ -388,7 +404,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   // (scattered 8-byte stores from the MFMA layout waste write bandwidth).
   // Rows past Tq fall outside the output resource and are dropped.
   __syncthreads();
-  const int q0 = blockIdx.y * 64 + 16 * w;  // this wave's first query
+  const int q0 = qb * 64 + 16 * w;  // this wave's first query
   const uint32_t esz = p.out_f32 ? 4u : 2u;
   const uint32_t ostride = static_cast<uint32_t>(H) * DH * esz;  // bytes between queries
   const rsrc_t r_o = make_rsrc(static_cast<char*>(p.out) + ((static_cast<size_t>(b) * p.Tq) * H + h) * DH * esz,
@@ -486,7 +502,7 @@ __global__ __launch_bounds__(128) void k_attend_generic(AttendParams p) {
 hipError_t launch_attend(const AttendParams& p, bool bf16, hipStream_t s) {
   if (p.B == 0 || p.Tq == 0 || p.H == 0) return hipSuccess;
   if (bf16 && (p.dh == 128 || p.dh == 64)) {
-    const dim3 grid(static_cast<unsigned>(p.B * p.H), static_cast<unsigned>((p.Tq + 63) / 64));
+    const dim3 grid(static_cast<unsigned>(p.B * p.H * ((p.Tq + 63) / 64)));
     const int ds = p.dh / p.G;
     const int vm = ds >= 8 ? kWide : (ds == 4 ? kDs4 : kDs2);
     auto k = p.dh == 128 ? (vm == kWide ? k_attend_bf16<128, kWide> : vm == kDs4 ? k_attend_bf16<128, kDs4>
