@@ -30,7 +30,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "compressed-KV attention query-tokens/sec at 7B shape; achieved HBM GB/s vs peak"
+PREFIX_METRIC = "prefix self-attention (causal) over the compressed cache, query-tokens/sec at 7B shape"
 HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_hbm_traffic.json")
 
 
@@ -96,6 +98,129 @@ def cpu_baseline(w, budget_s: float = 12.0) -> dict:
                       f"({spent:.1f} s); BLAS pool {threads} threads, Python loops on one core"}
 
 
+def causal_flops(w) -> float:
+    """Matrix-core work of one prefix self-attention call: q.k over the causal
+    triangle, P.Z over the same pairs (dense head width in the rotated space),
+    and the back-rotation of every query."""
+    pairs = w.T * (w.T + 1) / 2
+    return w.B * w.H * (2 * pairs * 2 * w.dh + 2 * w.T * w.dh * w.dh)
+
+
+def cpu_baseline_causal(w, masks, budget_s: float = 12.0) -> dict:
+    """The float64 oracle's prefix self-attention on whole prefixes of layer 0."""
+    import oracle as O
+    import synth
+    from threadpoolctl import threadpool_info
+
+    wt = synth.layer_weights(w, 0)
+    done, spent = 0, 0.0
+    while spent < budget_s and done < w.B:
+        a = synth.sample_activations(w, 0, done, ("q", "k", "v"))
+        m = masks[done][None]
+        z = O.rotate(a["v"][None], wt["R"])
+        off, Vp = O.pack(z, m, w.G, w.T * w.G)
+        t0 = time.perf_counter()
+        O.attend_packed_causal(a["q"][None], a["k"][None], m, off, Vp, wt["R"], w.G)
+        spent += time.perf_counter() - t0
+        done += 1
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": done * w.T / spent, "unit": "query-tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"layer 0, prefixes 0..{done - 1} of {w.B}: causal attention over the packed cache in "
+                      f"float64 ({spent:.1f} s, pack excluded); BLAS pool {threads} threads"}
+
+
+def prefix_attention(args, w):
+    """Prefix self-attention (rolesub_attend_causal) at the 7B-stack layer shape:
+    every prefix token is a query and sees the keys before it; masks carry the
+    workload's per-type budgets, values are packed by the fused rotate+pack."""
+    import torch
+
+    import paper_2608_18410_amd as rs
+    import synth
+    from paper_2608_18410_amd.pipeline import pack_capacity
+
+    dev = torch.device("cuda:0")
+    w = w.replace(Tq=w.T)
+    dt = torch.bfloat16
+    cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
+    put = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+    masks0 = None
+    layers = []
+    t_gen = time.time()
+    for l in range(w.L):
+        wt = synth.layer_weights(w, l)
+        acts = {n: torch.empty((w.B, w.T, w.H, w.dh), dtype=dt, device=dev) for n in ("q", "k", "v")}
+        import concurrent.futures as cf
+        with cf.ThreadPoolExecutor(16) as ex:
+            for b0 in range(0, w.B, 16):
+                parts = list(ex.map(lambda b: synth.sample_activations(w, l, b, ("q", "k", "v")),
+                                    range(b0, min(w.B, b0 + 16))))
+                for i, p in enumerate(parts):
+                    for n in acts:
+                        acts[n][b0 + i].copy_(torch.from_numpy(p[n]))
+        m = np.stack([synth.synthetic_masks(w, l, b) for b in range(w.B)])
+        if l == 0:
+            masks0 = m
+        mask = torch.from_numpy(m.view(np.int32)).to(dev)
+        R = put(wt["R"])
+        offsets = torch.empty((w.B, w.T + 1), dtype=torch.int32, device=dev)
+        Vp = torch.empty((w.B, w.H, cap, w.ds), dtype=dt, device=dev)
+        rs.rotate_pack(acts["v"], R, mask, w.G, cap, out=(offsets, Vp))
+        del acts["v"]
+        out = torch.empty((w.B, w.T, w.H, w.dh), dtype=dt, device=dev)
+        layers.append(dict(q=acts["q"], k=acts["k"], mask=mask, offsets=offsets, Vp=Vp, R=R, out=out))
+        print(f"# layer {l} inputs resident ({time.time() - t_gen:.1f} s)", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+
+    def att(L):
+        rs.attend_causal(L["q"], L["k"], L["mask"], L["offsets"], L["Vp"], L["R"], w.G, out=L["out"])
+
+    for L in layers:
+        att(L)
+    torch.cuda.synchronize()
+    eager_out = layers[-1]["out"].clone()
+    stream = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for L in layers:
+            att(L)
+    for _ in range(args.warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    if not torch.equal(layers[-1]["out"], eager_out):
+        raise RuntimeError("graph replay output differs from the eager pass")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    call_us = ms_step * 1e3 / w.L
+    sum_k = int(layers[0]["offsets"][:, -1].sum().item()) // w.B
+    a_bytes = attend_bytes(w, sum_k, 2)
+    gbs = a_bytes / (call_us * 1e-6) / 1e9
+    tflops = causal_flops(w) / (call_us * 1e-6) / 1e12
+    line = {
+        "metric": PREFIX_METRIC, "value": w.B * w.T * w.L / (ms_step * 1e-3), "unit": "query-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded Gaussian activations, Haar rotations, per-type group budgets)",
+        "config": {"workload": w.name + "-prefix-self-attention", "layers": w.L, "prefixes": w.B,
+                   "kv_tokens": w.T, "queries": w.T, "heads": w.H, "head_dim": w.dh, "groups": w.G,
+                   "keep": {"vis": w.k_vis, "lang": w.k_lang, "prop": w.k_prop},
+                   "value_counts": "prefix query tokens x layers per second", "graphs": True},
+        "roofline": {"kernel": "rolesub_attend_causal (k_attend_bf16, causal)", "bound": "hbm",
+                     "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": call_us,
+                     "mfma": {"achieved": tflops, "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                              "frac": tflops / BF16_MFMA_PEAK_TFLOPS, "flops_per_launch": causal_flops(w)}},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_causal(w, masks0)
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -105,6 +230,8 @@ def main():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="issue the calls directly, no HIP graphs")
+    ap.add_argument("--prefix-attention", action="store_true",
+                    help="time prefix self-attention (rolesub_attend_causal) at the same shape instead")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 4 times (counter calibration) and exit")
     args = ap.parse_args()
@@ -136,6 +263,9 @@ def main():
     w = synth.workload(args.workload)
     if args.layers:
         w = w.replace(L=args.layers)
+    if args.prefix_attention:
+        prefix_attention(args, w)
+        return
     dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
     budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
     cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
