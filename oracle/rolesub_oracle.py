@@ -22,13 +22,19 @@ notes of the repository):
   * threshold budgets keep count(gamma > tau) groups clamped to [kmin, kmax];
   * attention: scale 1/sqrt(dh), no mask, keys unchanged, routed values;
   * prefix self-attention: the prefix tokens are the queries, query t sees
-    keys 0..t (causal), keys unchanged, routed values.
+    keys 0..t (causal), keys unchanged, routed values;
+  * token retention: per view (a run of consecutive tokens) the highest
+    token scores are kept with the same order as group selection; a budget
+    that does not divide evenly gives the first views one more token.
 
 Parity: every function here is pinned by CPU tests against closed forms, the
 paper's printed KV fractions, brute-force enumeration and textbook special
 cases; none is "parity unpinned".
 """
 from __future__ import annotations
+
+from fractions import Fraction
+import math
 
 import numpy as np
 from scipy.special import erf as _erf
@@ -41,6 +47,7 @@ __all__ = [
     "rotate", "back_rotate", "latent_role", "language_pool", "gelu",
     "router_mlp2", "router_additive", "group_budget", "select_groups",
     "attend_packed_causal", "attend_plain_causal",
+    "retained_count", "split_evenly", "retain_tokens", "gather_tokens",
     "mask_to_idx", "popcount", "pack", "unpack", "expand_mask", "routed_values",
     "attend_packed", "attend_plain", "softmax", "pipeline",
     "kv_fraction", "packed_groups",
@@ -386,3 +393,48 @@ def pipeline(h, q, k, v, types, weights, mode, k_by_type, G, tau=0.0, kmin=0, km
     return {"scores": scores, "K": K, "mask": mask, "z": z, "offsets": offsets,
             "Vp": Vp, "out": out}
 
+
+# ----------------------------------------------------------------------------
+# Token-level retention ahead of the routed path (Sec. 3.1; Sec. 4.1)
+# ----------------------------------------------------------------------------
+
+def retained_count(r, n):
+    """ceil(r * n): tokens of a type kept at retention ratio r (Sec. 3.1),
+    exact for the float r as given."""
+    return int(math.ceil(Fraction(r) * int(n)))
+
+
+def split_evenly(total, n_parts):
+    """The retained budget divided evenly between views (Sec. 4.1); when it does
+    not divide, the first views take one more token."""
+    q, rem = divmod(int(total), int(n_parts))
+    return [q + (1 if v < rem else 0) for v in range(int(n_parts))]
+
+
+def retain_tokens(scores, seg_len, seg_keep):
+    """Per sample and per segment (a run of consecutive tokens, e.g. one camera
+    view), keep the seg_keep highest-scoring tokens (Sec. 3.1): a larger score
+    first, equal scores (-0 equal to +0) by lower index, NaN after every
+    number. scores [B, N] with N = sum(seg_len). Returns [B, sum(seg_keep)]
+    int64 token indices, ascending within each segment, segments in order."""
+    scores = np.asarray(scores)
+    B, N = scores.shape
+    assert sum(seg_len) == N and all(0 <= k <= n for n, k in zip(seg_len, seg_keep))
+    out = np.zeros((B, sum(seg_keep)), dtype=np.int64)
+    for b in range(B):
+        pos = o = 0
+        for n, k in zip(seg_len, seg_keep):
+            sc = scores[b, pos:pos + n]
+            isnan = np.isnan(sc)
+            val = np.where(isnan, 0.0, sc.astype(np.float64))
+            order = np.lexsort((np.arange(n), -val, isnan))
+            out[b, o:o + k] = pos + np.sort(order[:k])
+            pos += n
+            o += k
+    return out
+
+
+def gather_tokens(x, idx):
+    """Rows of the retained tokens, x[b, idx[b, j]] for x [B, N, ...]."""
+    x = np.asarray(x)
+    return np.stack([x[b, idx[b]] for b in range(x.shape[0])])

@@ -475,6 +475,72 @@ def test_attend_causal_method_form_equals_plain_form():
     assert np.max(np.abs(a - b)) < 1e-12
 
 
+# ----------------------------------------------------------------------------
+# Token-level retention
+# ----------------------------------------------------------------------------
+
+def test_retained_counts_are_the_printed_ones():
+    g = json.load(open(os.path.join(GOLDEN, "retention_counts.json")))
+    for r, kept in g["rows"]:
+        assert O.retained_count(r, g["dense_visual_tokens"]) == kept
+        per_view = O.split_evenly(kept, g["views"])
+        assert per_view == [kept // 2, kept // 2] and sum(per_view) == kept
+    assert O.retained_count(1.0, 177) == 177 and O.retained_count(0.5, 3) == 2   # ceiling
+    assert O.split_evenly(7, 3) == [3, 2, 2]
+
+
+def _scores_with_ties(rng, B, N):
+    sc = rng.standard_normal((B, N)).astype(np.float32)
+    sc[:, ::5] = np.round(sc[:, ::5])               # exact ties
+    sc[:, 1::7] = 0.0
+    sc[:, 3::7] = -0.0                              # -0 equals +0
+    sc[:, 2::11] = np.nan                           # NaN ranks after every number
+    return sc
+
+
+def test_retention_equals_group_selection_on_short_segments():
+    # a segment of <= 32 tokens is exactly a group-selection problem, whose
+    # oracle is pinned by brute force above
+    rng = np.random.default_rng(21)
+    seg_len, seg_keep = [7, 32, 1, 20], [3, 12, 1, 0]
+    sc = _scores_with_ties(rng, 5, sum(seg_len))
+    got = O.retain_tokens(sc, seg_len, seg_keep)
+    for b in range(5):
+        pos = o = 0
+        for n, k in zip(seg_len, seg_keep):
+            m = int(O.select_groups(sc[b, pos:pos + n][None], np.array([k]))[0])
+            want = [pos + s for s in range(n) if (m >> s) & 1]
+            assert list(got[b, o:o + k]) == want
+            pos += n
+            o += k
+
+
+def test_retention_keeps_the_highest_scores():
+    rng = np.random.default_rng(22)
+    seg_len, seg_keep = [256, 256], [16, 16]
+    sc = _scores_with_ties(rng, 3, 512)
+    got = O.retain_tokens(sc, seg_len, seg_keep)
+    for b in range(3):
+        for v in range(2):
+            kept = got[b, 16 * v:16 * v + 16]
+            assert np.all(np.diff(kept) > 0) and np.all((kept >= 256 * v) & (kept < 256 * (v + 1)))
+            seg = sc[b, 256 * v:256 * (v + 1)]
+            key = lambda i: (np.isnan(seg[i]), -np.nan_to_num(seg[i], nan=0.0), i)
+            kept_keys = [key(i - 256 * v) for i in kept]
+            dropped = [key(i) for i in range(256) if 256 * v + i not in set(kept.tolist())]
+            assert max(kept_keys) < min(dropped)
+
+
+def test_gather_tokens_takes_the_listed_rows():
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal((2, 9, 3, 4))
+    idx = np.array([[0, 4, 8], [1, 2, 3]])
+    g = O.gather_tokens(x, idx)
+    for b in range(2):
+        for j in range(3):
+            assert np.array_equal(g[b, j], x[b, idx[b, j]])
+
+
 def test_routed_value_is_a_projection():
     _, _, v, R = _attn_case(T=20, seed=9)
     G = 8
