@@ -220,6 +220,36 @@ rolesub_status rolesub_attend_causal(const rolesub_dims* dims, rolesub_dtype dty
                                      void* out, rolesub_dtype out_dtype, void* workspace,
                                      size_t ws_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * rolesub_retain_tokens: token-level retention ahead of the routed path
+ * (Sec. 3.1: the ceil(r_m |I_m|) highest-scoring tokens of a type are kept;
+ * Sec. 4.1: the visual budget is divided evenly between the camera views).
+ * Each sample's N tokens form n_seg segments of consecutive tokens (e.g. one
+ * per view); segment s has seg_len[s] tokens, of which the seg_keep[s] with
+ * the highest scores are kept: a larger score first, equal scores (-0 equal
+ * to +0) by lower index, NaN after every number.
+ *   scores   [B,N] f32 (device)
+ *   keep_idx [B,K] int32 (device), K = sum(seg_keep): the kept token indices,
+ *            ascending within each segment, segments in order
+ *   seg_len, seg_keep: n_seg host integers; sum(seg_len) == N;
+ *            1 <= n_seg <= 16, seg_len[s] <= 8192
+ * B = 0 or K = 0 does nothing and returns OK.
+ * ------------------------------------------------------------------------ */
+rolesub_status rolesub_retain_tokens(int32_t B, int32_t N, int32_t n_seg, const int32_t* seg_len,
+                                     const int32_t* seg_keep, const float* scores, int32_t* keep_idx,
+                                     void* stream);
+
+/* ---------------------------------------------------------------------------
+ * rolesub_gather_tokens: rows of the retained tokens (the compact prefix the
+ * routed path runs on): dst[b,j,:] = src[b, keep_idx[b,j], :].
+ *   src [B,N,row_bytes], dst [B,K,row_bytes] (device, any element type);
+ *   keep_idx [B,K] int32 (device); row_bytes a multiple of 4 (16 is fastest).
+ * An index outside [0, N) gives a zero row. One sample's rows must be
+ * below 2 GiB. B, K or row_bytes = 0 does nothing and returns OK.
+ * ------------------------------------------------------------------------ */
+rolesub_status rolesub_gather_tokens(int32_t B, int32_t N, int32_t K, int64_t row_bytes, const int32_t* keep_idx,
+                                     const void* src, void* dst, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

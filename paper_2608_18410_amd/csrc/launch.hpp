@@ -84,4 +84,25 @@ struct AttendParams {
 };
 hipError_t launch_attend(const AttendParams& p, bool bf16, hipStream_t s);
 
+// Token retention (Sec. 3.1): per sample, per segment of consecutive tokens,
+// the seg_keep highest scores. Segments are at most kRetainMaxSeg tokens.
+constexpr int kRetainMaxSegments = 16, kRetainMaxSeg = 8192;
+struct RetainParams {
+  int B, N, K, n_seg;
+  int seg_start[kRetainMaxSegments], seg_len[kRetainMaxSegments], seg_keep[kRetainMaxSegments],
+      seg_out[kRetainMaxSegments];
+  const float* scores;  // [B][N]
+  int32_t* keep_idx;    // [B][K]
+};
+hipError_t launch_retain(const RetainParams& p, hipStream_t s);
+
+struct GatherParams {
+  int B, N, K;
+  int64_t row_bytes;
+  const int32_t* idx;  // [B][K]
+  const void* src;     // [B][N][row_bytes]
+  void* dst;           // [B][K][row_bytes]
+};
+hipError_t launch_gather_rows(const GatherParams& p, hipStream_t s);
+
 }  // namespace rolesub

@@ -380,4 +380,64 @@ rolesub_status rolesub_attend_causal(const rolesub_dims* dims, rolesub_dtype dty
                      out_dtype, workspace, ws_bytes, stream);
 }
 
+rolesub_status rolesub_retain_tokens(int32_t B, int32_t N, int32_t n_seg, const int32_t* seg_len,
+                                     const int32_t* seg_keep, const float* scores, int32_t* keep_idx,
+                                     void* stream) {
+  const char* fn = "rolesub_retain_tokens";
+  if (B < 0 || N < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: B and N must be >= 0", fn);
+  if (n_seg < 1 || n_seg > kRetainMaxSegments)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: n_seg=%d outside [1, %d]", fn, n_seg, kRetainMaxSegments);
+  if (!seg_len || !seg_keep) return fail(ROLESUB_ERR_INVALID_ARG, "%s: seg_len or seg_keep is NULL", fn);
+  RetainParams p = {};
+  p.B = B;
+  p.N = N;
+  p.n_seg = n_seg;
+  int64_t start = 0, out = 0;
+  for (int s_ = 0; s_ < n_seg; ++s_) {
+    if (seg_len[s_] < 0 || seg_keep[s_] < 0 || seg_keep[s_] > seg_len[s_])
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: segment %d: need 0 <= keep (%d) <= length (%d)", fn, s_,
+                  seg_keep[s_], seg_len[s_]);
+    if (seg_len[s_] > kRetainMaxSeg)
+      return fail(ROLESUB_ERR_UNSUPPORTED, "%s: segment %d has %d tokens (at most %d)", fn, s_, seg_len[s_],
+                  kRetainMaxSeg);
+    p.seg_start[s_] = static_cast<int>(start);
+    p.seg_len[s_] = seg_len[s_];
+    p.seg_keep[s_] = seg_keep[s_];
+    p.seg_out[s_] = static_cast<int>(out);
+    start += seg_len[s_];
+    out += seg_keep[s_];
+  }
+  if (start != N) return fail(ROLESUB_ERR_INVALID_ARG, "%s: segment lengths sum to %lld, not N=%d", fn,
+                              static_cast<long long>(start), N);
+  p.K = static_cast<int>(out);
+  if (B == 0 || p.K == 0) return ROLESUB_OK;
+  if (!scores || !keep_idx) return fail(ROLESUB_ERR_INVALID_ARG, "%s: a tensor pointer is NULL", fn);
+  if (static_cast<size_t>(B) * n_seg > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: grid too large", fn);
+  p.scores = scores;
+  p.keep_idx = keep_idx;
+  return from_hip(launch_retain(p, static_cast<hipStream_t>(stream)), fn);
+}
+
+rolesub_status rolesub_gather_tokens(int32_t B, int32_t N, int32_t K, int64_t row_bytes, const int32_t* keep_idx,
+                                     const void* src, void* dst, void* stream) {
+  const char* fn = "rolesub_gather_tokens";
+  if (B < 0 || N < 0 || K < 0 || row_bytes < 0)
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: sizes must be >= 0", fn);
+  if (row_bytes % 4 != 0) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: row_bytes must be a multiple of 4", fn);
+  if (B == 0 || K == 0 || row_bytes == 0) return ROLESUB_OK;
+  if (!keep_idx || !src || !dst) return fail(ROLESUB_ERR_INVALID_ARG, "%s: a tensor pointer is NULL", fn);
+  if (static_cast<size_t>(N) * row_bytes >= kMaxRegion || row_bytes >= static_cast<int64_t>(kMaxRegion))
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: one sample's rows exceed 2 GiB", fn);
+  if (static_cast<size_t>(B) * K > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: grid too large", fn);
+  GatherParams p = {};
+  p.B = B;
+  p.N = N;
+  p.K = K;
+  p.row_bytes = row_bytes;
+  p.idx = keep_idx;
+  p.src = src;
+  p.dst = dst;
+  return from_hip(launch_gather_rows(p, static_cast<hipStream_t>(stream)), fn);
+}
+
 }  // extern "C"

@@ -24,7 +24,7 @@ EXPORTS = (
     "rolesub_status_str", "rolesub_last_error", "rolesub_version",
     "rolesub_rotate_values", "rolesub_route_workspace_size", "rolesub_route",
     "rolesub_pack_kv", "rolesub_rotate_pack", "rolesub_attend_workspace_size", "rolesub_attend",
-    "rolesub_attend_causal",
+    "rolesub_attend_causal", "rolesub_retain_tokens", "rolesub_gather_tokens",
 )
 
 
@@ -81,6 +81,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                    ctypes.c_int, P, SZ, P]
     lib.rolesub_attend_causal.argtypes = [P, ctypes.c_int, P, P, P, P, P, I64, P, ctypes.c_float, P,
                                           ctypes.c_int, P, SZ, P]
+    lib.rolesub_retain_tokens.argtypes = [I32, I32, I32, P, P, P, P, P]
+    lib.rolesub_gather_tokens.argtypes = [I32, I32, I32, I64, P, P, P, P]
     for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_rotate_pack",
                "rolesub_attend"):
         getattr(lib, fn).restype = ctypes.c_int
@@ -277,4 +279,29 @@ def attend_causal(q, k, mask, offsets, Vp, R, G: int, scale: float = 0.0, out_dt
         ctypes.byref(dims), _code(q), _ptr(q), _ptr(k, q.dtype), _ptr(mask), _ptr(offsets, torch.int32),
         _ptr(Vp, q.dtype), int(cap), _ptr(R, q.dtype), float(scale), _ptr(o), _code(o), None, 0,
         _stream(stream)))
+    return o
+
+
+def retain_tokens(scores, seg_len, seg_keep, out=None, stream=None):
+    """Per sample and per segment of consecutive tokens, the indices of the
+    seg_keep highest-scoring tokens (int32 [B, sum(seg_keep)])."""
+    B, N = scores.shape
+    n = len(seg_len)
+    lens = (ctypes.c_int32 * n)(*[int(x) for x in seg_len])
+    keeps = (ctypes.c_int32 * n)(*[int(x) for x in seg_keep])
+    K = int(sum(seg_keep))
+    o = torch.empty((B, K), dtype=torch.int32, device=scores.device) if out is None else out
+    _check("rolesub_retain_tokens", load().rolesub_retain_tokens(
+        B, N, n, lens, keeps, _ptr(scores, torch.float32), _ptr(o, torch.int32), _stream(stream)))
+    return o
+
+
+def gather_tokens(x, idx, out=None, stream=None):
+    """Rows x[b, idx[b, j]] of a [B, N, ...] tensor (the retained prefix)."""
+    B, N = x.shape[:2]
+    K = idx.shape[1]
+    o = torch.empty((B, K) + tuple(x.shape[2:]), dtype=x.dtype, device=x.device) if out is None else out
+    row_bytes = x[0, 0].numel() * x.element_size() if N else 0
+    _check("rolesub_gather_tokens", load().rolesub_gather_tokens(
+        B, N, K, row_bytes, _ptr(idx, torch.int32), _ptr(x), _ptr(o), _stream(stream)))
     return o

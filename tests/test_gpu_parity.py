@@ -278,6 +278,54 @@ def test_attend_causal_stack_shape_and_f32_output():
     assert max_rel(got, ref) <= TOL[w.dtype]
 
 
+# ----------------------------------------------------------------------------
+# Token retention and the retained prefix
+# ----------------------------------------------------------------------------
+
+def _retention_scores(seed, B, N):
+    r = np.random.default_rng(seed)
+    sc = r.standard_normal((B, N)).astype(np.float32)
+    sc[:, ::5] = np.round(sc[:, ::5])               # exact ties
+    sc[:, 1::7] = 0.0
+    sc[:, 3::7] = -0.0                              # -0 equals +0
+    sc[:, 2::11] = np.nan                           # NaN ranks after every number
+    return sc
+
+
+@pytest.mark.parametrize("B,seg_len,seg_keep", [
+    (64, [256, 256], [64, 64]),                     # 7B stack: 128 of 512 visual tokens, two views
+    (16, [256, 256], [4, 4]),                       # the paper's 8 of 512
+    (3, [256] * 7 + [256], [16] * 7 + [256]),       # seven views, language kept whole
+    (2, [5, 0, 300, 1], [0, 0, 300, 1]),            # keep none / all / empty segment
+    (2, [1] * 16, [1, 0] * 8),                      # sixteen segments
+    (2, [8192], [1000]),                            # the longest segment
+])
+def test_retain_tokens_bit_exact(B, seg_len, seg_keep):
+    sc = _retention_scores(sum(seg_len) + B, B, sum(seg_len))
+    got = host(rs.retain_tokens(torch.from_numpy(sc).to(DEV), seg_len, seg_keep))
+    want = O.retain_tokens(sc, seg_len, seg_keep)
+    _say(f"retain_tokens B={B} segments={len(seg_len)} kept={sum(seg_keep)}: "
+         f"{int(np.sum(got != want))} mismatches")
+    assert np.array_equal(got, want)
+
+
+def test_gather_tokens_rows():
+    r = np.random.default_rng(31)
+    B, N, d = 4, 512, 4096
+    x = synth.round_to(r.standard_normal((B, N, d)), "bf16")
+    idx = O.retain_tokens(_retention_scores(32, B, N), [256, 256], [64, 64]).astype(np.int32)
+    got = host(rs.gather_tokens(put(x, torch.bfloat16), torch.from_numpy(idx).to(DEV)))
+    assert np.array_equal(got, O.gather_tokens(x, idx))
+    # 12-byte rows (no 16-byte pieces) and indices outside [0, N) (zero rows)
+    y = r.standard_normal((2, 9, 3)).astype(np.float32)
+    idx2 = np.array([[0, 8, -1, 4], [9, 3, 3, 100]], dtype=np.int32)
+    got2 = host(rs.gather_tokens(torch.from_numpy(y).to(DEV), torch.from_numpy(idx2).to(DEV)))
+    for b in range(2):
+        for j in range(4):
+            t = idx2[b, j]
+            assert np.array_equal(got2[b, j], y[b, t] if 0 <= t < 9 else np.zeros(3, np.float32))
+
+
 def test_attend_stack_layer_shape():
     # the 7B-stack layer shape with its per-type kept counts (4 of 8 groups for
     # 128 visual tokens, 6 for 48 language tokens, all 8 for the proprio token)
