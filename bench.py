@@ -31,6 +31,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "compressed-KV attention query-tokens/sec at 7B shape; achieved HBM GB/s vs peak"
 PREFIX_METRIC = "prefix self-attention (causal) over the compressed cache, query-tokens/sec at 7B shape"
+RETAIN_METRIC = "token retention (top scores per view) + gather of the retained hidden states, tokens/sec"
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_hbm_traffic.json")
@@ -221,6 +222,90 @@ def prefix_attention(args, w):
     print(json.dumps(line), flush=True)
 
 
+def retention(args, w):
+    """Token retention at the 7B-stack shape: 64 prefixes whose 512 visual
+    tokens come from two 256-patch views; per view the 64 highest-scoring
+    tokens are kept (128 retained, the workload's visual count) and their
+    hidden states (d = 4096, bf16) are gathered into the compact prefix."""
+    import torch
+
+    import paper_2608_18410_amd as rs
+
+    dev = torch.device("cuda:0")
+    B, views, per_view, d = w.B, 2, 256, w.d
+    keep = [w.n_vis // views] * views
+    N, K = views * per_view, sum(keep)
+    rng = np.random.default_rng(w.seed)
+    n_sets = 6  # distinct inputs cycled so no call finds its data in the memory-side cache
+    sets = []
+    for _ in range(n_sets):
+        sc = torch.from_numpy(rng.standard_normal((B, N)).astype(np.float32)).to(dev)
+        h = torch.randn(B, N, d, device=dev, dtype=torch.float32).to(torch.bfloat16)
+        sets.append(dict(scores=sc, h=h, idx=torch.empty((B, K), dtype=torch.int32, device=dev),
+                         out=torch.empty((B, K, d), dtype=torch.bfloat16, device=dev)))
+    torch.cuda.synchronize()
+
+    def call(S):
+        rs.retain_tokens(S["scores"], [per_view] * views, keep, out=S["idx"])
+        rs.gather_tokens(S["h"], S["idx"], out=S["out"])
+
+    stream = torch.cuda.Stream()
+    for S in sets:
+        call(S)
+    torch.cuda.synchronize()
+    ref = sets[0]["out"].clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for S in sets:
+            call(S)
+    for _ in range(args.warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    if not torch.equal(sets[0]["out"], ref):
+        raise RuntimeError("graph replay output differs from the eager pass")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    call_us = e0.elapsed_time(e1) * 1e3 / (args.steps * n_sets)
+    row = d * 2
+    moved = B * N * 4 + B * K * 4 * 2 + 2 * B * K * row  # scores, indices (written, read), rows read + written
+    gbs = moved / (call_us * 1e-6) / 1e9
+    line = {
+        "metric": RETAIN_METRIC, "value": B * K / (call_us * 1e-6), "unit": "retained tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": call_us * n_sets / 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32 scores, bf16 rows",
+        "data": "synthetic (seeded Gaussian scores and hidden states)",
+        "config": {"workload": w.name + "-token-retention", "prefixes": B, "views": views,
+                   "tokens_per_view": per_view, "kept_per_view": keep[0], "row": f"hidden {d} x bf16",
+                   "value_counts": "retained tokens per second (selection + gather per call)", "graphs": True},
+        "roofline": {"kernel": "rolesub_retain_tokens + rolesub_gather_tokens", "bound": "hbm", "achieved": gbs,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": moved, "avg_launch_us": call_us},
+    }
+    if not args.no_cpu_baseline:
+        import oracle as O
+        from threadpoolctl import threadpool_info
+        nb = 8  # prefixes per oracle call
+        sc = sets[0]["scores"][:nb].cpu().numpy()
+        hh = sets[0]["h"][:nb].float().cpu().numpy()
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 10.0:
+            idx = O.retain_tokens(sc, [per_view] * views, keep)
+            O.gather_tokens(hh, idx)
+            reps += 1
+        spent = time.perf_counter() - t0
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+        line["cpu_baseline"] = {"value": reps * nb * K / spent, "unit": "retained tokens/s", "cores": 1,
+                                "kind": "oracle",
+                                "sample": f"{reps} oracle calls on {nb} of the {B} prefixes (selection + gather, "
+                                          f"{spent:.1f} s); Python loops on one core (BLAS pool {threads} unused)"}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -232,6 +317,8 @@ def main():
     ap.add_argument("--eager", action="store_true", help="issue the calls directly, no HIP graphs")
     ap.add_argument("--prefix-attention", action="store_true",
                     help="time prefix self-attention (rolesub_attend_causal) at the same shape instead")
+    ap.add_argument("--retention", action="store_true",
+                    help="time token retention + gather of the retained hidden states instead")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 4 times (counter calibration) and exit")
     args = ap.parse_args()
@@ -265,6 +352,9 @@ def main():
         w = w.replace(L=args.layers)
     if args.prefix_attention:
         prefix_attention(args, w)
+        return
+    if args.retention:
+        retention(args, w)
         return
     dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
     budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)

@@ -20,13 +20,16 @@ __device__ __forceinline__ uint32_t score_key(float x) {
 // lower index. Kept tokens are written in index order (block-wide scan of the
 // keep flags).
 __global__ __launch_bounds__(256) void k_retain(RetainParams p) {
-  __shared__ uint32_t keys[kRetainMaxSeg];
+  __shared__ __attribute__((aligned(16))) uint32_t keys[kRetainMaxSeg + 4];
   __shared__ int wsum[4];
   const int b = blockIdx.x / p.n_seg, sg = blockIdx.x % p.n_seg;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n = p.seg_len[sg], start = p.seg_start[sg], keep = p.seg_keep[sg];
   const float* sc = p.scores + static_cast<size_t>(b) * p.N + start;
   for (int i = tid; i < n; i += 256) keys[i] = score_key(sc[i]);
+  // padding up to a multiple of 4: key 0 at an index past every token never
+  // ranks before one (0 is not above any key, and equal keys need j < i)
+  if (tid < 4) keys[n + tid] = 0u;
   __syncthreads();
   int32_t* out = p.keep_idx + static_cast<size_t>(b) * p.K + p.seg_out[sg];
   int base = 0;  // kept tokens before this chunk
@@ -36,9 +39,12 @@ __global__ __launch_bounds__(256) void k_retain(RetainParams p) {
     if (i < n && keep > 0) {
       const uint32_t ki = keys[i];
       int rank = 0;
-      for (int j = 0; j < n; ++j) {
-        const uint32_t kj = keys[j];  // the same address in every lane: a broadcast read
-        rank += (kj > ki) | ((kj == ki) & (j < i));
+      // four keys per 16-byte read; the same address in every lane is a broadcast
+#pragma unroll 4
+      for (int j = 0; j < n; j += 4) {
+        const u32x4 kj = *reinterpret_cast<const u32x4*>(keys + j);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rank += (kj[e] > ki) | ((kj[e] == ki) & (j + e < i));
       }
       kept = rank < keep;
     }
@@ -69,9 +75,19 @@ __global__ __launch_bounds__(256) void k_gather_rows(GatherParams p) {
   const bool in = (t >= 0) & (t < p.N);
   const uint32_t so = in ? static_cast<uint32_t>(t) * rb : kOOB;
   if ((rb & 15u) == 0) {
-    for (uint32_t o = 16u * threadIdx.x; o < rb; o += 16u * 256u) {
-      const u32x4 v = bload16(r_src, so == kOOB ? kOOB : so + o);
-      __builtin_amdgcn_raw_buffer_store_b128(v, r_dst, o, 0, 0);
+    // four 16-byte loads in flight per thread before their stores
+    for (uint32_t o0 = 16u * threadIdx.x; o0 < rb; o0 += 4u * 16u * 256u) {
+      u32x4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t o = o0 + u * 16u * 256u;
+        v[u] = bload16(r_src, (so == kOOB) | (o >= rb) ? kOOB : so + o);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t o = o0 + u * 16u * 256u;
+        __builtin_amdgcn_raw_buffer_store_b128(v[u], r_dst, o < rb ? o : kOOB, 0, 0);
+      }
     }
   } else {
     for (uint32_t o = 4u * threadIdx.x; o < rb; o += 4u * 256u) {
