@@ -25,7 +25,10 @@ notes of the repository):
     keys 0..t (causal), keys unchanged, routed values;
   * token retention: per view (a run of consecutive tokens) the highest
     token scores are kept with the same order as group selection; a budget
-    that does not divide evenly gives the first views one more token.
+    that does not divide evenly gives the first views one more token;
+  * role-driven budget allocation: priorities are an input, quantised to
+    integers, and each type's budget is apportioned by largest remainders
+    with a cap of G groups per token (details at allocate_groups).
 
 Parity: every function here is pinned by CPU tests against closed forms, the
 paper's printed KV fractions, brute-force enumeration and textbook special
@@ -48,6 +51,7 @@ __all__ = [
     "router_mlp2", "router_additive", "group_budget", "select_groups",
     "attend_packed_causal", "attend_plain_causal",
     "retained_count", "split_evenly", "retain_tokens", "gather_tokens",
+    "role_priority", "quantize_priority", "allocate_groups",
     "mask_to_idx", "popcount", "pack", "unpack", "expand_mask", "routed_values",
     "attend_packed", "attend_plain", "softmax", "pipeline",
     "kv_fraction", "packed_groups",
@@ -438,3 +442,81 @@ def gather_tokens(x, idx):
     """Rows of the retained tokens, x[b, idx[b, j]] for x [B, N, ...]."""
     x = np.asarray(x)
     return np.stack([x[b, idx[b]] for b in range(x.shape[0])])
+
+
+# ----------------------------------------------------------------------------
+# Role-driven within-type budget allocation (Sec. 3.5, the allocator B)
+# ----------------------------------------------------------------------------
+
+def role_priority(h, W_r, b_r, w_pri):
+    """Token-level priority from the latent role representation (Sec. 3.5):
+    p_i = w^T a_i with a_i = softmax(W_r h_i + b_r) (Eq. latentrole) and one
+    priority weight per latent role. Returns [B,T] float64."""
+    return latent_role(h, W_r, b_r) @ _f64(w_pri)
+
+
+def quantize_priority(p):
+    """Integer priority weights: floor(min(max(p, 0), 256) * 2^16) for float32
+    priorities p (NaN counts as 0). Exact: scaling by a power of two and the
+    floor introduce no rounding, so any implementation gets the same integers."""
+    p = np.asarray(p, dtype=np.float32).astype(np.float64)
+    p = np.where(np.isnan(p), 0.0, np.clip(p, 0.0, 256.0))
+    return np.floor(p * 65536.0).astype(np.int64)
+
+
+def _apportion(q, budget, G):
+    """Largest-remainder apportionment of `budget` units over weights q (int64,
+    tokens in index order) with at most G units each. A token whose quota
+    budget*q_i/Q exceeds G is capped at G and the rest is apportioned again
+    among the others; all-zero weights count as equal. Leftover units go to
+    the largest remainders, lower index first on ties."""
+    n = len(q)
+    K = np.zeros(n, dtype=np.int64)
+    active = list(range(n))
+    while active:
+        w = np.array([q[i] for i in active], dtype=object)
+        if sum(w) == 0:
+            w = np.ones(len(active), dtype=object)
+        Q = int(sum(w))
+        over = [a for a, wi in zip(active, w) if budget * int(wi) > G * Q]
+        if over:
+            for a in over:
+                K[a] = G
+            budget -= G * len(over)
+            active = [a for a in active if a not in over]
+            continue
+        floors = [budget * int(wi) // Q for wi in w]
+        rems = [budget * int(wi) % Q for wi in w]
+        left = budget - sum(floors)
+        order = sorted(range(len(active)), key=lambda j: (-rems[j], active[j]))
+        for j, a in enumerate(active):
+            K[a] = floors[j]
+        for j in order[:left]:
+            K[active[j]] += 1
+        break
+    return K
+
+
+def allocate_groups(priority, types, k_by_type, G):
+    """Per-token group budgets K_i (Sec. 3.5): within each sample and token type
+    m the B_m = K_m * |I_m| groups are distributed by role-derived priority,
+    with 0 <= K_i <= G and sum K_i = B_m. Types with K_m >= G keep all G
+    groups (no allocation), K_m = 0 keeps none; a token whose type is not one
+    of the four keeps all G groups (as with fixed budgets). priority [B, T]
+    float32, types [T] or [B, T], k_by_type[4]. Returns K [B, T] int64."""
+    priority = np.asarray(priority)
+    B, T = priority.shape
+    types = np.broadcast_to(np.asarray(types), (B, T))
+    q = quantize_priority(priority)
+    K = np.where(types > ACT, G, 0).astype(np.int64)
+    for b in range(B):
+        for m in range(4):
+            toks = np.nonzero(types[b] == m)[0]
+            if len(toks) == 0:
+                continue
+            km = min(int(k_by_type[m]), G)
+            if km >= G or km == 0:
+                K[b, toks] = km
+                continue
+            K[b, toks] = _apportion([int(x) for x in q[b, toks]], km * len(toks), G)
+    return K

@@ -567,3 +567,183 @@ def test_pipeline_tiny_invariants():
     assert r["out"].shape == (1, w.Tq, w.H, w.dh) and np.all(np.isfinite(r["out"]))
     plain = O.attend_plain(a["q"], a["k"], a["v"], r["mask"], wt["R"], w.G)
     assert np.max(np.abs(plain - r["out"])) < 1e-12
+
+
+# ----------------------------------------------------------------------------
+# Role-driven within-type budget allocation (Sec. 3.5)
+# ----------------------------------------------------------------------------
+
+def test_role_priority_special_cases():
+    rng = np.random.default_rng(30)
+    h = rng.standard_normal((2, 5, 8))
+    w = np.array([0.5, 2.0, -1.0])
+    # one role: a = 1, the priority is its weight
+    p1 = O.role_priority(h, np.zeros((1, 8)), np.zeros(1), w[:1])
+    assert np.allclose(p1, 0.5, rtol=0, atol=1e-15)
+    # equal logits: a is uniform, the priority is the mean weight
+    pu = O.role_priority(h, np.zeros((3, 8)), np.zeros(3), w)
+    assert np.allclose(pu, w.mean(), rtol=0, atol=1e-15)
+    # one dominant logit: the priority is that role's weight
+    pd = O.role_priority(h, np.zeros((3, 8)), np.array([0.0, 800.0, 0.0]), w)
+    assert np.allclose(pd, 2.0, rtol=0, atol=1e-12)
+
+
+def test_quantize_priority_exact_values():
+    x = np.array([1.0, 2.0 ** -16, 1.5 * 2.0 ** -16, 0.0, -0.0, -3.0, np.nan, 256.0, 1e9, np.inf,
+                  0.1, 3.75], dtype=np.float32)
+    want = [65536, 1, 1, 0, 0, 0, 0, 1 << 24, 1 << 24, 1 << 24,
+            int(np.floor(float(np.float32(0.1)) * 65536)), 245760]
+    assert O.quantize_priority(x).tolist() == want
+    assert want[10] == 6553
+
+
+def _alloc_case(rng, B, T, G):
+    pr = rng.standard_normal((B, T)).astype(np.float32) * 2 + 1
+    pr[rng.random((B, T)) < 0.15] = 0.0
+    pr[rng.random((B, T)) < 0.05] = np.nan
+    pr[:, 1::7] = pr[:, 0:1]                     # ties
+    types = rng.integers(0, 4, size=(B, T)).astype(np.uint8)
+    return pr, types
+
+
+@pytest.mark.parametrize("G", [4, 8, 16])
+def test_allocation_meets_the_stated_constraints(G):
+    rng = np.random.default_rng(31 + G)
+    pr, types = _alloc_case(rng, 3, 40, G)
+    for kby in ([1, 2, 3, 0], [G // 2, G, 1, G - 1], [0, 0, 0, 0]):
+        K = O.allocate_groups(pr, types, kby, G)
+        assert np.all((K >= 0) & (K <= G))
+        for b in range(3):
+            for m in range(4):
+                sel = types[b] == m
+                assert K[b][sel].sum() == min(kby[m], G) * sel.sum()
+
+
+def test_allocation_uniform_priorities_give_the_fixed_budget():
+    types = np.array([0] * 7 + [1] * 5 + [2, 3])
+    kby = [3, 5, 8, 2]
+    for val in (0.0, 1.25, 300.0):
+        K = O.allocate_groups(np.full((2, 14), val, np.float32), types, kby, 8)
+        assert np.array_equal(K, np.broadcast_to(np.array(kby)[types], (2, 14)))
+
+
+def test_allocation_is_monotone_in_priority():
+    rng = np.random.default_rng(32)
+    pr, types = _alloc_case(rng, 4, 60, 8)
+    K = O.allocate_groups(pr, types, [2, 3, 5, 1], 8)
+    q = O.quantize_priority(pr)
+    for b in range(4):
+        for m in range(4):
+            i = np.nonzero(types[b] == m)[0]
+            qi, ki = q[b, i], K[b, i]
+            hi = qi[:, None] > qi[None, :]
+            assert np.all((ki[:, None] >= ki[None, :]) | ~hi)
+
+
+def test_allocation_worked_examples():
+    # one dominant token: 16 groups over weights 100:1:1:1 give it 15.5 > G = 8,
+    # so it keeps 8 and the other 8 go 8/3 each: floors 2, 2, 2, then the equal
+    # remainders go to the lower indices
+    assert O.allocate_groups(np.array([[100.0, 1, 1, 1]], np.float32), [0] * 4, [4, 0, 0, 0], 8).tolist() == \
+        [[8, 3, 3, 2]]
+    # a cap that only appears after the first one: 24 groups over 100:60:10:10:10:10
+    # cap token 0 (12 > 8); 16 over 60:10:10:10:10 caps token 1 (9.6 > 8);
+    # 8 over four equal weights gives 2 each
+    assert O.allocate_groups(np.array([[100.0, 60, 10, 10, 10, 10]], np.float32), [1] * 6, [0, 4, 0, 0],
+                             8).tolist() == [[8, 8, 2, 2, 2, 2]]
+    # zero priorities share what the capped token leaves, equally
+    assert O.allocate_groups(np.array([[1.0, 0, 0]], np.float32), [0] * 3, [4, 0, 0, 0], 8).tolist() == \
+        [[8, 2, 2]]
+    # proportional with remainders: 10 groups over 3:2:1 -> quotas 5, 3.33, 1.67
+    assert O.allocate_groups(np.array([[3.0, 2.0, 1.0, 7.0]], np.float32), [2, 2, 2, 0], [8, 8, 10 // 3, 8],
+                             8).tolist() == [[5, 3, 1, 8]]
+
+
+def _water_filled_quotas(q, budget, G):
+    """Continuous allocation x_i = min(G, lam * q_i) with sum x = budget (a
+    water level lam found by trying every capped prefix), equal shares when the
+    uncapped weights are all zero. Exact rationals."""
+    n = len(q)
+    order = sorted(range(n), key=lambda i: -q[i])
+    for c in range(n + 1):
+        capped, rest = order[:c], order[c:]
+        left = budget - G * c
+        if left < 0:
+            break
+        Qr = sum(q[i] for i in rest)
+        x = [Fraction(0)] * n
+        for i in capped:
+            x[i] = Fraction(G)
+        if Qr == 0:
+            if not rest:
+                if left == 0:
+                    return x
+                continue
+            share = Fraction(left, len(rest))
+            if share <= G:
+                for i in rest:
+                    x[i] = share
+                return x
+            continue
+        lam = Fraction(left, Qr)
+        if all(lam * q[i] <= G for i in rest) and all(lam * q[i] >= G for i in capped):
+            for i in rest:
+                x[i] = lam * q[i]
+            return x
+    raise AssertionError("no water level")
+
+
+def test_allocation_is_the_nearest_integer_split_of_the_water_filled_quotas():
+    """Brute force: among all integer K with 0 <= K_i <= G and sum = B_m, the
+    allocation minimises sum (K_i - x_i)^2 for the continuous capped quotas x,
+    and among equal minimisers gives the extra groups to the lower indices."""
+    import itertools
+    rng = np.random.default_rng(33)
+    cases = 0
+    for _ in range(300):
+        n = int(rng.integers(1, 6))
+        G = int(rng.integers(2, 5))
+        km = int(rng.integers(1, G))
+        kind = rng.integers(0, 3)
+        if kind == 0:
+            pr = rng.integers(0, 6, size=n).astype(np.float32)       # small integers: ties, zeros
+        elif kind == 1:
+            pr = (rng.random(n) * 5).astype(np.float32)
+        else:
+            pr = np.where(rng.random(n) < 0.5, 0.0, rng.integers(1, 50, size=n)).astype(np.float32)
+        q = [int(x) for x in O.quantize_priority(pr)]
+        budget = km * n
+        try:
+            x = _water_filled_quotas(q, budget, G)
+        except AssertionError:
+            continue
+        best, arg = None, []
+        for K in itertools.product(range(G + 1), repeat=n):
+            if sum(K) != budget:
+                continue
+            dev = sum((Fraction(k) - xi) ** 2 for k, xi in zip(K, x))
+            if best is None or dev < best:
+                best, arg = dev, [K]
+            elif dev == best:
+                arg.append(K)
+        want = max(arg)       # lexicographically largest: lower index first
+        got = O.allocate_groups(pr[None, :], [0] * n, [km, 0, 0, 0], G)[0].tolist()
+        assert got == list(want), (pr, G, km, got, want)
+        cases += 1
+    assert cases > 200
+
+
+def test_allocation_groups_are_per_sample_and_type():
+    rng = np.random.default_rng(34)
+    pr, types = _alloc_case(rng, 3, 30, 8)
+    kby = [3, 2, 5, 6]
+    K = O.allocate_groups(pr, types, kby, 8)
+    for b in range(3):
+        for m in range(4):
+            i = np.nonzero(types[b] == m)[0]
+            alone = O.allocate_groups(pr[b, i][None], np.full(len(i), m), kby, 8)[0]
+            assert np.array_equal(K[b, i], alone)
+    # a token of no listed type keeps every group
+    t2 = types.copy()
+    t2[0, 3] = 7
+    assert O.allocate_groups(pr, t2, kby, 8)[0, 3] == 8
