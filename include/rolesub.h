@@ -250,6 +250,59 @@ rolesub_status rolesub_retain_tokens(int32_t B, int32_t N, int32_t n_seg, const 
 rolesub_status rolesub_gather_tokens(int32_t B, int32_t N, int32_t K, int64_t row_bytes, const int32_t* keep_idx,
                                      const void* src, void* dst, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * rolesub_allocate_groups: role-driven within-type budget allocation
+ * (Sec. 3.5, the allocator B), optionally followed by the Top-K_i group
+ * selection (Sec. 3.4) with the allocated budgets.
+ * Within each sample and token type m (ROLESUB_VIS..ROLESUB_ACT) the
+ * B_m = K_m * n_m groups of the type's n_m tokens are distributed by the
+ * tokens' role-derived priorities, with 0 <= K_i <= G and sum K_i = B_m:
+ *   weights    w_i = floor(min(max(p_i, 0), 256) * 2^16), NaN as 0 (exact);
+ *   shares     B_m * w_i / sum w; a token whose share exceeds G gets G and
+ *              the rest of the budget is shared again among the others;
+ *              all-zero weights count as equal;
+ *   rounding   the floors of the shares, then one more group to each of the
+ *              largest remainders (equal remainders: lower token index).
+ * K_m = 0 gives 0 and K_m = G gives G to every token of the type; a token of
+ * any other type value gets G.
+ *   k_by_type  4 host integers K_m, 0 <= K_m <= G
+ *   priority   [B,T] f32 (device), token_type [B,T] uint8 (device)
+ *   scores     [B,T,G] f32 (device) or NULL. Non-NULL: each token keeps its
+ *              K_i highest-scoring groups, order as rolesub_route, written
+ *              to mask (required), idx and count (optional, as
+ *              rolesub_route). NULL: mask, idx and count must be NULL.
+ *   k_out      [B,T] uint8 (device) or NULL: the K_i; required when scores
+ *              is NULL.
+ * 1 <= G <= 32, T <= 4096. B*T = 0 does nothing and returns OK.
+ * ------------------------------------------------------------------------ */
+rolesub_status rolesub_allocate_groups(int32_t B, int32_t T, int32_t G, const int32_t* k_by_type,
+                                       const float* priority, const uint8_t* token_type, const float* scores,
+                                       uint8_t* k_out, uint32_t* mask, uint8_t* idx, uint8_t* count,
+                                       void* stream);
+
+/* ---------------------------------------------------------------------------
+ * rolesub_route_allocate: routing with role-driven budgets (Eq. latentrole,
+ * Eq. routingscore, Sec. 3.5 allocator, Sec. 3.4 Top-K_i) in one call:
+ * the router's scores gamma and the token priority p_i = w_pri^T a_i from
+ * the latent role representation a_i, then rolesub_allocate_groups on them.
+ *   router, h, token_type, dims  as rolesub_route
+ *   w_pri        [C] priority weight per latent role (call dtype, device)
+ *   k_by_type    4 host integers K_m, 0 <= K_m <= G
+ *   priority_out [B,T] f32 or NULL, scores_out [B,T,G] f32 or NULL
+ *   k_out [B,T] uint8 or NULL; mask [B,T] uint32 (required); idx, count as
+ *   rolesub_route
+ *   workspace    at least rolesub_route_allocate_workspace_size() bytes
+ *                (device scratch, always required)
+ * T <= 4096. The kept-group total per sample equals that of the fixed
+ * budgets, so pack capacities sized for k_by_type hold.
+ * ------------------------------------------------------------------------ */
+size_t rolesub_route_allocate_workspace_size(const rolesub_dims* dims, const rolesub_router* router);
+rolesub_status rolesub_route_allocate(const rolesub_dims* dims, rolesub_dtype dtype, const rolesub_router* router,
+                                      const void* w_pri, const int32_t* k_by_type, const void* h,
+                                      const uint8_t* token_type, float* priority_out, float* scores_out,
+                                      uint8_t* k_out, uint32_t* mask, uint8_t* idx, uint8_t* count,
+                                      void* workspace, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -454,6 +454,12 @@ __global__ __launch_bounds__(256) void k_route_generic(RouteParams p) {
       sm += a[c];
     }
     for (int c = 0; c < C; ++c) a[c] /= sm;
+    if (p.priority) {
+      const T* wp = static_cast<const T*>(p.w_pri);
+      float pr = 0.f;
+      for (int c = 0; c < C; ++c) pr = fmaf(tof(wp[c]), a[c], pr);
+      p.priority[tok] = pr;
+    }
   }
   __syncthreads();
   if (p.kind == 0) {
@@ -484,8 +490,7 @@ __global__ __launch_bounds__(256) void k_route_generic(RouteParams p) {
     float g[32];
 #pragma unroll
     for (int s = 0; s < 32; ++s) g[s] = s < G ? gam[s] : 0.f;
-    const uint32_t m = select_token(p, g, p.types[tok]);
-    write_selection(p, tok, m);
+    if (p.mask) write_selection(p, tok, select_token(p, g, p.types[tok]));
     if (p.scores_out)
       for (int s = 0; s < G; ++s) p.scores_out[tok * G + s] = gam[s];
   }
@@ -524,7 +529,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
   constexpr int Hr = 128, kW2Stride = GP + 4;
   static_assert(Hr * (kFsStride + kW2Stride) * 4 <= kRtNB * kRtStage, "epilogue tiles fit the ring");
   __shared__ __attribute__((aligned(16))) char ring[kRtNB * kRtStage];
-  __shared__ float b2s[GP], brs[16];
+  __shared__ float b2s[GP], brs[16], wps[16];
   __shared__ __attribute__((aligned(16))) float cbs[PS ? 2 : 1][Hr];
   const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
@@ -578,6 +583,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
     }
     if (tid < GP) b2s[tid] = tid < G ? tof(static_cast<const bf16*>(p.b2)[tid]) : 0.f;
     if (tid < 16) brs[tid] = tid < C ? tof(static_cast<const bf16*>(p.b_r)[tid]) : 0.f;
+    if (tid < 16) wps[tid] = (p.priority && tid < C) ? tof(static_cast<const bf16*>(p.w_pri)[tid]) : 0.f;
   }
 
   const rsrc_t r_h = make_rsrc(static_cast<const bf16*>(p.h) + static_cast<size_t>(tok0) * d,
@@ -726,6 +732,12 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
   float a[16];  // role mixture weights; zero past C
 #pragma unroll
   for (int c = 0; c < 16; ++c) a[c] = __shfl(ex[c & 3], l16 + 16 * (c >> 2), kWave) * isum;
+  if (p.priority) {  // role priority w^T a (weights zero past C)
+    float pr = 0.f;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) pr = fmaf(wps[c], a[c], pr);
+    if (valid && g4 == 0) p.priority[tok] = pr;
+  }
 
   // F a on the f32 matrix cores: the accumulator layout is that of a 16x16x4
   // MFMA with A = F (rows 16m + t, roles k0 + q) and B = a (role k0 + q of the
@@ -818,7 +830,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
         if (s < G) p.scores_out[static_cast<size_t>(tok) * G + s] = mine[u];
       }
     }
-    if (g4 == 0) write_selection(p, tok, msk);
+    if (g4 == 0 && p.mask) write_selection(p, tok, msk);
   }
 }
 

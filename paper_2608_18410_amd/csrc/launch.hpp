@@ -22,7 +22,9 @@ struct RouteParams {
   int kmin, kmax;
   const float* scores_in;
   float* scores_out;
-  uint32_t* mask;
+  const void* w_pri;  // [C] role priority weights (call dtype), with priority
+  float* priority;    // [B][T] p = w^T a, or null
+  uint32_t* mask;     // null: scores (and priority) only, no selection
   uint8_t* idx;
   uint8_t* count;
 };
@@ -45,6 +47,21 @@ hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s);
 // LDS bytes the generic (one token per workgroup) router needs.
 size_t route_generic_shm(int d, int G, int C, int Hr, int kind);
 hipError_t launch_select(const RouteParams& p, hipStream_t s);
+
+// Role-driven within-type group allocation (and optional selection).
+constexpr int kAllocMaxT = 4096;  // tokens per sample
+struct AllocParams {
+  int B, T, G;
+  int k_by_type[4];
+  const float* priority;   // [B][T]
+  const uint8_t* types;    // [B][T]
+  const float* scores;     // [B][T][G] or null (no selection)
+  uint8_t* k_out;          // [B][T] or null
+  uint32_t* mask;          // [B][T], with scores
+  uint8_t* idx;            // [B][T][G] or null
+  uint8_t* count;          // [B][T] or null
+};
+hipError_t launch_allocate(const AllocParams& p, hipStream_t s);
 
 struct RotateParams {
   int ntok, T, H, G, tok_per_wg;

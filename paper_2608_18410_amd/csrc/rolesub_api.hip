@@ -109,6 +109,97 @@ size_t route_ws_bytes(const rolesub_dims* d, const rolesub_router* r) {
          align256(route_pcb_floats(d->B, d->d > 0 ? d->d : 0, r->Hr, r->kind) * sizeof(float));
 }
 
+// Checks the router and hidden states and fills the router part of p (B, T,
+// d, G already set); the route workspace sits at the start of `workspace`.
+rolesub_status setup_router(const char* fn, const rolesub_dims* dims, rolesub_dtype dtype,
+                            const rolesub_router* router, const void* h, void* workspace, size_t ws_bytes,
+                            RouteParams& p) {
+  if (!h) return fail(ROLESUB_ERR_INVALID_ARG, "%s: h must be non-NULL", fn);
+  if (dims->d < 1) return fail(ROLESUB_ERR_INVALID_ARG, "%s: hidden size d=%d", fn, dims->d);
+  if (router->C < 1 || router->C > 64)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: C=%d latent roles not supported (1..64)", fn, router->C);
+  if (!router->W_r || !router->b_r) return fail(ROLESUB_ERR_INVALID_ARG, "%s: W_r/b_r are NULL", fn);
+  if (router->kind == ROLESUB_ROUTER_MLP2) {
+    if (router->d_e < 1 || router->Hr < 1)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: need d_e >= 1 and Hr >= 1", fn);
+    if (!router->E || !router->W1 || !router->b1 || !router->W2 || !router->b2)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: MLP2 router weights are NULL", fn);
+    if (static_cast<int64_t>(router->C) * router->d_e > dims->d)
+      return fail(ROLESUB_ERR_UNSUPPORTED, "%s: C*d_e=%d exceeds d=%d", fn, router->C * router->d_e, dims->d);
+  } else if (router->kind == ROLESUB_ROUTER_ADDITIVE) {
+    if (!router->W_tok || !router->b_tok || !router->W_role || !router->W_lang || !router->b_lang)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: additive router weights are NULL", fn);
+  } else {
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: unknown router kind %d", fn, router->kind);
+  }
+  if (route_generic_shm(dims->d, dims->G, router->C, router->Hr, router->kind) > 64 * 1024 ||
+      static_cast<size_t>(dims->d) * sizeof(float) > 64 * 1024)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: hidden size d=%d too large", fn, dims->d);
+  if (static_cast<size_t>(dims->T) * dims->d * esize(dtype) >= kMaxRegion ||
+      static_cast<size_t>(router->Hr) * (2 * static_cast<size_t>(dims->d) + router->d_e) * esize(dtype) >= kMaxRegion)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: one sample's hidden states exceed 2 GiB", fn);
+  const size_t need = route_ws_bytes(dims, router);
+  if (ws_bytes < need || (need && !workspace))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws_bytes);
+
+  p.d_e = router->d_e;
+  p.Hr = router->Hr;
+  p.C = router->C;
+  p.kind = router->kind;
+  p.alpha_role = router->alpha_role;
+  p.alpha_lang = router->alpha_lang;
+  p.h = h;
+  p.W_r = router->W_r;
+  p.b_r = router->b_r;
+  p.E = router->E;
+  p.W1 = router->W1;
+  p.b1 = router->b1;
+  p.W2 = router->W2;
+  p.b2 = router->b2;
+  p.W_tok = router->W_tok;
+  p.b_tok = router->b_tok;
+  p.W_role = router->W_role;
+  p.W_lang = router->W_lang;
+  p.b_lang = router->b_lang;
+  char* ws = static_cast<char*>(workspace);
+  p.cb = reinterpret_cast<float*>(ws);
+  const size_t off_F = align256(route_cb_floats(p.B, p.Hr, p.G, p.kind) * sizeof(float));
+  const size_t off_h = off_F + align256(route_F_floats(p.Hr, p.G, p.C, p.kind) * sizeof(float));
+  const size_t off_p = off_h + align256(route_hbar_floats(p.B, p.d) * sizeof(float));
+  p.F = reinterpret_cast<float*>(ws + off_F);
+  p.hbar = reinterpret_cast<float*>(ws + off_h);
+  p.pcb = reinterpret_cast<float*>(ws + off_p);
+  return ROLESUB_OK;
+}
+
+rolesub_status check_alloc(const char* fn, int32_t B, int32_t T, int32_t G, const int32_t* k_by_type) {
+  if (B < 0 || T < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: need B >= 0, T >= 0", fn);
+  if (G < 1 || G > 32) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: G=%d groups not supported (1..32)", fn, G);
+  if (!k_by_type) return fail(ROLESUB_ERR_INVALID_ARG, "%s: k_by_type is NULL", fn);
+  for (int t = 0; t < 4; ++t)
+    if (k_by_type[t] < 0 || k_by_type[t] > G)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: k_by_type[%d]=%d outside 0..G=%d", fn, t, k_by_type[t], G);
+  if (T > kAllocMaxT)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: T=%d tokens per sample above %d", fn, T, kAllocMaxT);
+  if (static_cast<int64_t>(B) * 5 > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B too large", fn);
+  return ROLESUB_OK;
+}
+
+AllocParams alloc_params(int32_t B, int32_t T, int32_t G, const int32_t* k_by_type) {
+  AllocParams a = {};
+  a.B = B;
+  a.T = T;
+  a.G = G;
+  for (int t = 0; t < 4; ++t) a.k_by_type[t] = k_by_type[t];
+  return a;
+}
+
+size_t route_allocate_ws_bytes(const rolesub_dims* d, const rolesub_router* r) {
+  if (!d || !r || d->B <= 0 || d->T <= 0 || d->G < 1) return 0;
+  const size_t ntok = static_cast<size_t>(d->B) * d->T;
+  return route_ws_bytes(d, r) + align256(ntok * d->G * sizeof(float)) + align256(ntok * sizeof(float));
+}
+
 }  // namespace
 
 extern "C" {
@@ -191,62 +282,88 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype, cons
   if (scores_in) return from_hip(launch_select(p, s), fn);
 
   if (!router) return fail(ROLESUB_ERR_INVALID_ARG, "%s: router is NULL and no scores_in given", fn);
-  if (!h) return fail(ROLESUB_ERR_INVALID_ARG, "%s: h must be non-NULL", fn);
-  if (dims->d < 1) return fail(ROLESUB_ERR_INVALID_ARG, "%s: hidden size d=%d", fn, dims->d);
-  if (router->C < 1 || router->C > 64)
-    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: C=%d latent roles not supported (1..64)", fn, router->C);
-  if (!router->W_r || !router->b_r) return fail(ROLESUB_ERR_INVALID_ARG, "%s: W_r/b_r are NULL", fn);
-  if (router->kind == ROLESUB_ROUTER_MLP2) {
-    if (router->d_e < 1 || router->Hr < 1)
-      return fail(ROLESUB_ERR_INVALID_ARG, "%s: need d_e >= 1 and Hr >= 1", fn);
-    if (!router->E || !router->W1 || !router->b1 || !router->W2 || !router->b2)
-      return fail(ROLESUB_ERR_INVALID_ARG, "%s: MLP2 router weights are NULL", fn);
-    if (static_cast<int64_t>(router->C) * router->d_e > dims->d)
-      return fail(ROLESUB_ERR_UNSUPPORTED, "%s: C*d_e=%d exceeds d=%d", fn, router->C * router->d_e, dims->d);
-  } else if (router->kind == ROLESUB_ROUTER_ADDITIVE) {
-    if (!router->W_tok || !router->b_tok || !router->W_role || !router->W_lang || !router->b_lang)
-      return fail(ROLESUB_ERR_INVALID_ARG, "%s: additive router weights are NULL", fn);
-  } else {
-    return fail(ROLESUB_ERR_INVALID_ARG, "%s: unknown router kind %d", fn, router->kind);
-  }
-  if (route_generic_shm(dims->d, dims->G, router->C, router->Hr, router->kind) > 64 * 1024 ||
-      static_cast<size_t>(dims->d) * sizeof(float) > 64 * 1024)
-    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: hidden size d=%d too large", fn, dims->d);
-  if (static_cast<size_t>(dims->T) * dims->d * esize(dtype) >= kMaxRegion ||
-      static_cast<size_t>(router->Hr) * (2 * static_cast<size_t>(dims->d) + router->d_e) * esize(dtype) >= kMaxRegion)
-    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: one sample's hidden states exceed 2 GiB", fn);
-  const size_t need = route_ws_bytes(dims, router);
-  if (ws_bytes < need || (need && !workspace))
+  st = setup_router(fn, dims, dtype, router, h, workspace, ws_bytes, p);
+  if (st) return st;
+  return from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
+}
+
+rolesub_status rolesub_allocate_groups(int32_t B, int32_t T, int32_t G, const int32_t* k_by_type,
+                                       const float* priority, const uint8_t* token_type, const float* scores,
+                                       uint8_t* k_out, uint32_t* mask, uint8_t* idx, uint8_t* count, void* stream) {
+  const char* fn = "rolesub_allocate_groups";
+  rolesub_status st = check_alloc(fn, B, T, G, k_by_type);
+  if (st) return st;
+  if (static_cast<int64_t>(B) * T == 0) return ROLESUB_OK;
+  if (!priority || !token_type) return fail(ROLESUB_ERR_INVALID_ARG, "%s: priority and token_type must be non-NULL", fn);
+  if (scores && !mask) return fail(ROLESUB_ERR_INVALID_ARG, "%s: scores given but mask is NULL", fn);
+  if (!scores && (mask || idx || count))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: selection outputs given without scores", fn);
+  if (!scores && !k_out) return fail(ROLESUB_ERR_INVALID_ARG, "%s: nothing to write (k_out and scores NULL)", fn);
+  AllocParams a = alloc_params(B, T, G, k_by_type);
+  a.priority = priority;
+  a.types = token_type;
+  a.scores = scores;
+  a.k_out = k_out;
+  a.mask = mask;
+  a.idx = idx;
+  a.count = count;
+  return from_hip(launch_allocate(a, static_cast<hipStream_t>(stream)), fn);
+}
+
+size_t rolesub_route_allocate_workspace_size(const rolesub_dims* dims, const rolesub_router* router) {
+  return route_allocate_ws_bytes(dims, router);
+}
+
+rolesub_status rolesub_route_allocate(const rolesub_dims* dims, rolesub_dtype dtype, const rolesub_router* router,
+                                      const void* w_pri, const int32_t* k_by_type, const void* h,
+                                      const uint8_t* token_type, float* priority_out, float* scores_out,
+                                      uint8_t* k_out, uint32_t* mask, uint8_t* idx, uint8_t* count,
+                                      void* workspace, size_t ws_bytes, void* stream) {
+  const char* fn = "rolesub_route_allocate";
+  if (!dims) return fail(ROLESUB_ERR_INVALID_ARG, "%s: dims is NULL", fn);
+  rolesub_status st = check_alloc(fn, dims->B, dims->T, dims->G, k_by_type);
+  if (st) return st;
+  if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+  const size_t ntok = static_cast<size_t>(dims->B) * dims->T;
+  if (ntok == 0) return ROLESUB_OK;
+  if (ntok > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
+  if (!router) return fail(ROLESUB_ERR_INVALID_ARG, "%s: router is NULL", fn);
+  if (!w_pri) return fail(ROLESUB_ERR_INVALID_ARG, "%s: w_pri is NULL", fn);
+  if (!token_type || !mask) return fail(ROLESUB_ERR_INVALID_ARG, "%s: token_type and mask must be non-NULL", fn);
+  const size_t need = route_allocate_ws_bytes(dims, router);
+  if (ws_bytes < need || !workspace)
     return fail(ROLESUB_ERR_INVALID_ARG, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws_bytes);
 
-  p.d_e = router->d_e;
-  p.Hr = router->Hr;
-  p.C = router->C;
-  p.kind = router->kind;
-  p.alpha_role = router->alpha_role;
-  p.alpha_lang = router->alpha_lang;
-  p.h = h;
-  p.W_r = router->W_r;
-  p.b_r = router->b_r;
-  p.E = router->E;
-  p.W1 = router->W1;
-  p.b1 = router->b1;
-  p.W2 = router->W2;
-  p.b2 = router->b2;
-  p.W_tok = router->W_tok;
-  p.b_tok = router->b_tok;
-  p.W_role = router->W_role;
-  p.W_lang = router->W_lang;
-  p.b_lang = router->b_lang;
-  char* ws = static_cast<char*>(workspace);
-  p.cb = reinterpret_cast<float*>(ws);
-  const size_t off_F = align256(route_cb_floats(p.B, p.Hr, p.G, p.kind) * sizeof(float));
-  const size_t off_h = off_F + align256(route_F_floats(p.Hr, p.G, p.C, p.kind) * sizeof(float));
-  const size_t off_p = off_h + align256(route_hbar_floats(p.B, p.d) * sizeof(float));
-  p.F = reinterpret_cast<float*>(ws + off_F);
-  p.hbar = reinterpret_cast<float*>(ws + off_h);
-  p.pcb = reinterpret_cast<float*>(ws + off_p);
-  return from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
+  RouteParams p = {};
+  p.B = dims->B;
+  p.T = dims->T;
+  p.d = dims->d;
+  p.G = dims->G;
+  p.types = token_type;
+  st = setup_router(fn, dims, dtype, router, h, workspace, ws_bytes, p);
+  if (st) return st;
+  // scores and priorities go to the caller's buffers or to the workspace tail
+  char* tail = static_cast<char*>(workspace) + route_ws_bytes(dims, router);
+  float* sc = scores_out ? scores_out : reinterpret_cast<float*>(tail);
+  float* pr = priority_out ? priority_out : reinterpret_cast<float*>(tail + align256(ntok * dims->G * sizeof(float)));
+  p.mode = ROLESUB_BUDGET_TOPK;
+  for (int t = 0; t < 4; ++t) p.k_by_type[t] = k_by_type[t];
+  p.scores_out = sc;
+  p.w_pri = w_pri;
+  p.priority = pr;
+  p.mask = nullptr;  // the selection waits for the allocation
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  st = from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
+  if (st) return st;
+  AllocParams a = alloc_params(dims->B, dims->T, dims->G, k_by_type);
+  a.priority = pr;
+  a.types = token_type;
+  a.scores = sc;
+  a.k_out = k_out;
+  a.mask = mask;
+  a.idx = idx;
+  a.count = count;
+  return from_hip(launch_allocate(a, s), fn);
 }
 
 rolesub_status rolesub_pack_kv(const rolesub_dims* dims, rolesub_dtype dtype, const rolesub_budget* budget,

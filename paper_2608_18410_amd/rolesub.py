@@ -25,6 +25,7 @@ EXPORTS = (
     "rolesub_rotate_values", "rolesub_route_workspace_size", "rolesub_route",
     "rolesub_pack_kv", "rolesub_rotate_pack", "rolesub_attend_workspace_size", "rolesub_attend",
     "rolesub_attend_causal", "rolesub_retain_tokens", "rolesub_gather_tokens",
+    "rolesub_allocate_groups", "rolesub_route_allocate_workspace_size", "rolesub_route_allocate",
 )
 
 
@@ -83,6 +84,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                           ctypes.c_int, P, SZ, P]
     lib.rolesub_retain_tokens.argtypes = [I32, I32, I32, P, P, P, P, P]
     lib.rolesub_gather_tokens.argtypes = [I32, I32, I32, I64, P, P, P, P]
+    lib.rolesub_allocate_groups.argtypes = [I32, I32, I32, P, P, P, P, P, P, P, P, P]
+    lib.rolesub_route_allocate_workspace_size.argtypes = [P, P]
+    lib.rolesub_route_allocate.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_rotate_pack",
                "rolesub_attend"):
         getattr(lib, fn).restype = ctypes.c_int
@@ -305,3 +309,69 @@ def gather_tokens(x, idx, out=None, stream=None):
     _check("rolesub_gather_tokens", load().rolesub_gather_tokens(
         B, N, K, row_bytes, _ptr(idx, torch.int32), _ptr(x), _ptr(o), _stream(stream)))
     return o
+
+
+def allocate_groups(priority, token_type, k_by_type, G: int, scores=None, *, want_k=True, want_idx=True,
+                    want_count=True, out=None, stream=None):
+    """Role-driven within-type group budgets K_i from token priorities, and with
+    scores the Top-K_i selection on them. Returns dict(k, mask, idx, count)."""
+    B, T = token_type.shape
+    dev = token_type.device
+    o = out or {}
+
+    def buf(name, shape, dtype, want=True):
+        if not want:
+            return None
+        return o[name] if name in o else torch.empty(shape, dtype=dtype, device=dev)
+
+    sel = scores is not None
+    kk = buf("k", (B, T), torch.uint8, want_k)
+    mask = buf("mask", (B, T), torch.int32, sel)
+    idx = buf("idx", (B, T, G), torch.uint8, sel and want_idx)
+    cnt = buf("count", (B, T), torch.uint8, sel and want_count)
+    kby = (ctypes.c_int32 * 4)(*[int(x) for x in k_by_type])
+    _check("rolesub_allocate_groups", load().rolesub_allocate_groups(
+        B, T, G, kby, _ptr(priority, torch.float32), _ptr(token_type, torch.uint8), _ptr(scores, torch.float32),
+        _ptr(kk), _ptr(mask), _ptr(idx), _ptr(cnt), _stream(stream)))
+    return {"k": kk, "mask": mask, "idx": idx, "count": cnt}
+
+
+def route_allocate_workspace_size(B, T, G, d, router: Router) -> int:
+    dims = Dims(B, T, 1, 64, G, d)
+    desc = router.desc()
+    return load().rolesub_route_allocate_workspace_size(ctypes.byref(dims), ctypes.byref(desc))
+
+
+def route_allocate(token_type, k_by_type, G: int, h, router: Router, w_pri, *, want_priority=True,
+                   want_scores=True, want_k=True, want_idx=True, want_count=True, workspace=None, out=None,
+                   stream=None):
+    """Routing with role-driven budgets: scores, priorities p = w_pri^T a, the
+    allocated K_i and the Top-K_i selection. Returns dict(mask, idx, count, k,
+    scores, priority)."""
+    B, T = token_type.shape
+    dev = token_type.device
+    d = h.shape[2]
+    o = out or {}
+
+    def buf(name, shape, dtype, want=True):
+        if not want:
+            return None
+        return o[name] if name in o else torch.empty(shape, dtype=dtype, device=dev)
+
+    mask = buf("mask", (B, T), torch.int32)
+    idx = buf("idx", (B, T, G), torch.uint8, want_idx)
+    cnt = buf("count", (B, T), torch.uint8, want_count)
+    kk = buf("k", (B, T), torch.uint8, want_k)
+    sco = buf("scores", (B, T, G), torch.float32, want_scores)
+    pri = buf("priority", (B, T), torch.float32, want_priority)
+    dims = Dims(B, T, 1, 64, G, d)
+    desc = router.desc()
+    ws_bytes = load().rolesub_route_allocate_workspace_size(ctypes.byref(dims), ctypes.byref(desc))
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    kby = (ctypes.c_int32 * 4)(*[int(x) for x in k_by_type])
+    _check("rolesub_route_allocate", load().rolesub_route_allocate(
+        ctypes.byref(dims), F32 if h.dtype == torch.float32 else BF16, ctypes.byref(desc), _ptr(w_pri, h.dtype),
+        kby, _ptr(h), _ptr(token_type, torch.uint8), _ptr(pri), _ptr(sco), _ptr(kk), _ptr(mask), _ptr(idx),
+        _ptr(cnt), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return {"mask": mask, "idx": idx, "count": cnt, "k": kk, "scores": sco, "priority": pri}

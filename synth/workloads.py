@@ -32,7 +32,7 @@ __all__ = [
     "VIS", "LANG", "PROP", "ACT", "TOPK", "THRESHOLD", "Workload", "WORKLOADS",
     "workload", "bf16_round", "round_to", "layer_weights", "additive_weights",
     "sample_activations", "layer_activations", "sample_scores", "synthetic_z",
-    "synthetic_masks", "haar_orthogonal",
+    "synthetic_masks", "haar_orthogonal", "priority_weights", "sample_priorities",
 ]
 
 
@@ -162,8 +162,9 @@ def haar_orthogonal(rng: np.random.Generator, n: int) -> np.ndarray:
 # weight tensor ids inside a layer (kind 0)
 _W_R, _W_BR, _W_E, _W_W1, _W_B1, _W_W2, _W_B2, _W_TOK, _W_BTOK, _W_ROLE, _W_LANG, _W_BLANG = range(12)
 _W_ROT = 100
+_W_PRI = 101
 # activation tensor ids inside a (layer, sample) (kind 1)
-_A_H, _A_Q, _A_K, _A_V, _A_S, _A_PERM, _A_J, _A_Z, _A_MASK = range(9)
+_A_H, _A_Q, _A_K, _A_V, _A_S, _A_PERM, _A_J, _A_Z, _A_MASK, _A_PRI, _A_PRI_KIND = range(11)
 
 
 def layer_weights(w: Workload, layer: int) -> dict:
@@ -271,3 +272,31 @@ def synthetic_masks(w: Workload, layer: int, b: int, counts=None) -> np.ndarray:
             m |= 1 << int(s_)
         masks[t] = m
     return masks
+
+
+def priority_weights(w: Workload, layer: int) -> np.ndarray:
+    """One priority weight per latent role [C]: 1 + N(0, 1), so that most roles
+    raise a token's priority and some lower it (rounded to the workload dtype)."""
+    return round_to(1.0 + _normal(w.seed, (layer, 0, 0, _W_PRI), (w.C,), 1.0), w.dtype)
+
+
+def sample_priorities(w: Workload, layer: int, b: int) -> np.ndarray:
+    """Synthetic token priorities [T] float32 for testing the allocation alone.
+
+    Most tokens draw an exponential priority with mean 1; a seeded tenth each
+    are exact zeros, negative, exact copies of another token's priority (ties),
+    values above the 256 clip, NaN, and multiples of 2^-16 (integer weights
+    whose proportional shares often tie)."""
+    g = _rng(w.seed, layer, 1, b, _A_PRI)
+    T = w.T
+    x = g.exponential(1.0, size=T).astype(np.float32)
+    kind = _rng(w.seed, layer, 1, b, _A_PRI_KIND).integers(0, 10, size=T)
+    x[kind == 0] = 0.0
+    x[kind == 1] = -x[kind == 1]
+    if T > 1:
+        src = g.integers(0, T, size=T)
+        x[kind == 2] = x[src[kind == 2]]
+    x[kind == 3] = 300.0 + x[kind == 3]
+    x[kind == 4] = np.nan
+    x[kind == 5] = (g.integers(1, 8, size=int(np.sum(kind == 5))) * 2.0 ** -16).astype(np.float32)
+    return x

@@ -326,6 +326,140 @@ def test_gather_tokens_rows():
             assert np.array_equal(got2[b, j], y[b, t] if 0 <= t < 9 else np.zeros(3, np.float32))
 
 
+# ----------------------------------------------------------------------------
+# Role-driven within-type budget allocation (Sec. 3.5): bit-exact
+# ----------------------------------------------------------------------------
+
+def _alloc_inputs(w, B, types=None, seed_layer=0):
+    pr = np.stack([synth.sample_priorities(w, seed_layer, b) for b in range(B)])
+    if types is None:
+        types = stack_types(w, B)
+    return pr, types
+
+
+def _check_allocation(pr, types, kby, G, scores=None, label=""):
+    want_k = O.allocate_groups(pr, types, kby, G)
+    r = rs.allocate_groups(torch.from_numpy(pr).to(DEV), put_u8(types), kby, G,
+                           scores=None if scores is None else put(scores, torch.float32))
+    torch.cuda.synchronize()
+    got_k = host(r["k"])
+    _say(f"allocate {label}: B={types.shape[0]} T={types.shape[1]} G={G} K_m={tuple(kby)}: "
+         f"{int(np.sum(got_k != want_k))} K mismatches")
+    assert np.array_equal(got_k, want_k)
+    if scores is not None:
+        want = O.select_groups(scores, want_k)
+        assert np.array_equal(host_mask(r["mask"]), want)
+        idx, cnt = O.mask_to_idx(want, G)
+        assert np.array_equal(host(r["count"]), cnt)
+        assert np.array_equal(host(r["idx"]), idx)
+
+
+@pytest.mark.parametrize("cid,B,G,kby", [
+    (4, 64, 8, (4, 6, 8, 8)),          # 7B stack: 128 visual, 48 language, 1 proprio token per prefix
+    (3, 16, 8, (2, 4, 8, 8)),          # aggressive budgets
+    (2, 2, 16, (3, 5, 1, 0)),          # 305 tokens, another G
+    (1, 3, 32, (31, 1, 16, 7)),        # G = 32, near-full and near-empty types
+    (1, 2, 1, (1, 0, 1, 1)),           # G = 1: no allocation possible
+])
+def test_allocate_groups_bit_exact(cid, B, G, kby):
+    w = synth.workload(cid).replace(B=B)
+    pr, types = _alloc_inputs(w, B)
+    r = np.random.default_rng(cid)
+    scores = r.standard_normal((B, w.T, G)).astype(np.float32)
+    scores[:, ::3, : max(1, G // 2)] = 0.5                       # tied groups
+    _check_allocation(pr, types, kby, G, scores, f"workload {cid}")
+    _check_allocation(pr, types, kby, G, None, f"workload {cid}, K only")
+
+
+def test_allocate_groups_edge_cases():
+    w = synth.workload(1)
+    r = np.random.default_rng(41)
+    # random types including values outside the four (they keep every group)
+    T = 600
+    types = r.integers(0, 6, size=(5, T)).astype(np.uint8)
+    pr = np.stack([synth.sample_priorities(w.replace(n_vis=T, n_lang=0), 1, b) for b in range(5)])
+    pr[1] = 0.0                                                  # all-zero priorities: equal shares
+    pr[2] = 2.5                                                  # uniform: the fixed K_m
+    pr[3, ::2] = 1e6                                             # half the tokens clipped and capped
+    _check_allocation(pr, types, (3, 5, 7, 1), 8, r.standard_normal((5, T, 8)).astype(np.float32), "mixed")
+    # the longest prefix, one type
+    T = 4096
+    types = np.zeros((2, T), dtype=np.uint8)
+    pr = np.stack([synth.sample_priorities(w.replace(n_vis=T, n_lang=0), 2, b) for b in range(2)])
+    _check_allocation(pr, types, (5, 0, 0, 0), 16, None, "T=4096")
+    # one token per sample
+    _check_allocation(np.array([[3.0], [np.nan]], np.float32), np.zeros((2, 1), np.uint8), (2, 0, 0, 0), 8,
+                      None, "T=1")
+    # empty inputs are no-ops; sizes and budgets outside the limits are errors
+    e = rs.allocate_groups(torch.empty((0, 5), device=DEV), torch.empty((0, 5), dtype=torch.uint8, device=DEV),
+                           (1, 1, 1, 1), 8)
+    assert e["k"].shape == (0, 5)
+    with pytest.raises(rs.RolesubError, match="above 4096"):
+        rs.allocate_groups(torch.zeros((1, 4097), device=DEV), torch.zeros((1, 4097), dtype=torch.uint8,
+                                                                          device=DEV), (1, 1, 1, 1), 8)
+    with pytest.raises(rs.RolesubError, match="outside 0..G"):
+        rs.allocate_groups(torch.zeros((1, 8), device=DEV), torch.zeros((1, 8), dtype=torch.uint8, device=DEV),
+                           (9, 1, 1, 1), 8)
+
+
+def _route_allocate_check(w, B, router, wpri_np, prio_ref, score_ref, label):
+    dt = tdtype(w)
+    h = np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(B)])
+    types = stack_types(w, B)
+    kby = tuple(w.k_by_type)
+    r = rs.route_allocate(put_u8(types), kby, w.G, put(h, dt), router, put(wpri_np, dt))
+    torch.cuda.synchronize()
+    perr = max_rel(host(r["priority"]), prio_ref(h))
+    serr = max_rel(host(r["scores"]), score_ref(h, types))
+    # allocation and selection: the stated constraints on the GPU's own priorities and scores
+    k = host(r["k"]).astype(np.int64)
+    qp = np.floor(np.clip(np.nan_to_num(host(r["priority"]).astype(np.float64), nan=0.0), 0, 256) * 65536)
+    for b in range(B):
+        for m in range(4):
+            i = np.nonzero(types[b] == m)[0]
+            km = min(kby[m], w.G)
+            assert k[b, i].sum() == km * len(i)
+            hi = qp[b, i][:, None] > qp[b, i][None, :]
+            assert np.all((k[b, i][:, None] >= k[b, i][None, :]) | ~hi)
+    assert np.all((k >= 0) & (k <= w.G))
+    mask = host_mask(r["mask"])
+    assert np.array_equal(O.popcount(mask), k)
+    assert np.array_equal(host(r["count"]), k)
+    sc = host(r["scores"])
+    bits = (mask[..., None] >> np.arange(w.G, dtype=np.uint32)) & 1
+    lo_kept = np.where(bits == 1, sc, np.inf).min(-1)
+    hi_drop = np.where(bits == 0, sc, -np.inf).max(-1)
+    assert np.all(lo_kept >= hi_drop)
+    agree = float(np.mean(k == O.allocate_groups(prio_ref(h).astype(np.float32), types, kby, w.G)))
+    _say(f"route_allocate {label}: priority max rel err {perr:.2e}, scores {serr:.2e}; "
+         f"K equal to the oracle's on {100 * agree:.1f}% of tokens")
+    assert perr <= 1e-4 and serr <= 1e-4
+
+
+@pytest.mark.parametrize("cid,B", [(4, 8), (2, 1), (1, 2)])
+def test_route_allocate(cid, B):
+    w = synth.workload(cid).replace(B=B)
+    wt = synth.layer_weights(w, 0)
+    wpri = synth.priority_weights(w, 0)
+    prio = lambda hh: O.role_priority(hh, wt["W_r"], wt["b_r"], wpri)
+    ref = lambda hh, tt: O.router_mlp2(hh, tt, wt["W_r"], wt["b_r"], wt["E"], wt["W1"], wt["b1"],
+                                       wt["W2"], wt["b2"])
+    _route_allocate_check(w, B, router_tensors(wt, tdtype(w)), wpri, prio, ref, f"mlp2 workload {cid} B={B}")
+
+
+def test_route_allocate_additive_router():
+    w = synth.workload(2).replace(B=2, d=512, G=16, C=6, n_vis=40, n_lang=9, n_prop=1, k_vis=3, k_lang=5,
+                                  k_prop=16)
+    aw = synth.additive_weights(w, 0)
+    wpri = synth.priority_weights(w, 0)
+    router = rs.Router.additive(*(put(aw[n], torch.bfloat16) for n in ("W_tok", "b_tok", "W_r", "b_r", "W_role",
+                                                                       "W_lang", "b_lang")))
+    prio = lambda hh: O.role_priority(hh, aw["W_r"], aw["b_r"], wpri)
+    ref = lambda hh, tt: O.router_additive(hh, tt, aw["W_tok"], aw["b_tok"], aw["W_r"], aw["b_r"],
+                                           aw["W_role"], aw["W_lang"], aw["b_lang"], 0.1, 0.1)
+    _route_allocate_check(w, 2, router, wpri, prio, ref, "additive bf16")
+
+
 def test_attend_stack_layer_shape():
     # the 7B-stack layer shape with its per-type kept counts (4 of 8 groups for
     # 128 visual tokens, 6 for 48 language tokens, all 8 for the proprio token)
