@@ -14,6 +14,12 @@ B * Tq * L / step time. `roofline` is measured live for the attention kernel
 with HIP events around back-to-back replays of the 32 attention launches right
 after the timed steps; `cpu_baseline` times the float64 oracle on a bounded
 sample on the host cores.
+
+--allocation routes with role-driven per-token budgets instead (the router
+also emits each token's role priority, then one kernel apportions every type's
+group budget over its tokens and selects their groups); the rest of the step
+is unchanged. --prefix-attention and --retention time the other rows of the
+path at the same shape.
 """
 from __future__ import annotations
 
@@ -31,6 +37,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "compressed-KV attention query-tokens/sec at 7B shape; achieved HBM GB/s vs peak"
 PREFIX_METRIC = "prefix self-attention (causal) over the compressed cache, query-tokens/sec at 7B shape"
+ALLOC_METRIC = ("compressed-KV attention query-tokens/sec at 7B shape with role-driven per-token budgets; "
+                "achieved HBM GB/s vs peak")
 RETAIN_METRIC = "token retention (top scores per view) + gather of the retained hidden states, tokens/sec"
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
@@ -76,26 +84,28 @@ def _traffic(launches_bytes_hint):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(w, budget_s: float = 12.0) -> dict:
+def cpu_baseline(w, budget_s: float = 12.0, allocation: bool = False) -> dict:
     """The float64 oracle (test infrastructure) on whole prefixes of layer 0."""
     import oracle as O
     import synth
     from threadpoolctl import threadpool_info
 
     wt = synth.layer_weights(w, 0)
+    wpri = synth.priority_weights(w, 0) if allocation else None
     cap = sum(n * min(k, w.G) for n, k in zip(w.type_counts(), w.k_by_type))
     done, spent = 0, 0.0
     while spent < budget_s and done < w.B:
         a = synth.sample_activations(w, 0, done)
         t0 = time.perf_counter()
         O.pipeline(a["h"][None], a["q"][None], a["k"][None], a["v"][None], w.types(), wt, w.mode,
-                   w.k_by_type, w.G, w.tau, w.kmin, w.kmax, cap=cap)
+                   w.k_by_type, w.G, w.tau, w.kmin, w.kmax, cap=cap, w_pri=wpri)
         spent += time.perf_counter() - t0
         done += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": done * w.Tq / spent, "unit": "query-tokens/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"layer 0, prefixes 0..{done - 1} of {w.B}: route->rotate->pack->attend in float64 "
+            "sample": f"layer 0, prefixes 0..{done - 1} of {w.B}: route->"
+                      f"{'allocate->' if allocation else ''}rotate->pack->attend in float64 "
                       f"({spent:.1f} s); BLAS pool {threads} threads, Python loops on one core"}
 
 
@@ -317,6 +327,8 @@ def main():
     ap.add_argument("--eager", action="store_true", help="issue the calls directly, no HIP graphs")
     ap.add_argument("--prefix-attention", action="store_true",
                     help="time prefix self-attention (rolesub_attend_causal) at the same shape instead")
+    ap.add_argument("--allocation", action="store_true",
+                    help="route with role-driven per-token budgets (rolesub_route_allocate) in the step")
     ap.add_argument("--retention", action="store_true",
                     help="time token retention + gather of the retained hidden states instead")
     ap.add_argument("--copy-probe", action="store_true",
@@ -357,6 +369,8 @@ def main():
         retention(args, w)
         return
     dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    if args.allocation and (w.scores_in or w.mode != rs.TOPK):
+        raise SystemExit("--allocation needs a workload with a router and fixed per-type budgets")
     budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
     cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
     types = torch.from_numpy(np.broadcast_to(w.types(), (w.B, w.T)).copy()).to(dev)
@@ -383,19 +397,32 @@ def main():
         scores = None
         if w.scores_in:
             scores = torch.from_numpy(np.stack([synth.sample_scores(w, l, b) for b in range(w.B)])).to(dev)
-        ws = rs.route_workspace_size(w.B, w.T, w.G, w.d, router)
+        if args.allocation:
+            ws = rs.route_allocate_workspace_size(w.B, w.T, w.G, w.d, router)
+        else:
+            ws = rs.route_workspace_size(w.B, w.T, w.G, w.d, router)
         bufs = LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, dt, ws_bytes=ws, device=dev,
                                      with_z=False)
+        alloc = None
+        if args.allocation:
+            alloc = dict(w_pri=put(synth.priority_weights(w, l)),
+                         priority=torch.empty((w.B, w.T), dtype=torch.float32, device=dev),
+                         k=torch.empty((w.B, w.T), dtype=torch.uint8, device=dev))
         layers.append(dict(acts=acts, router=router if scores is None else None, scores=scores,
-                           R=put(wt["R"]), bufs=bufs))
+                           R=put(wt["R"]), bufs=bufs, alloc=alloc))
         print(f"# layer {l} inputs resident ({time.time() - t_gen:.1f} s)", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
 
     def pre(L):
-        a, bf = L["acts"], L["bufs"]
-        rs.route(types, budget, w.G, h=a.get("h"), router=L["router"], scores_in=L["scores"],
-                 workspace=bf.workspace,
-                 out={"mask": bf.mask, "idx": bf.idx, "count": bf.count, "scores": bf.scores})
+        a, bf, al = L["acts"], L["bufs"], L["alloc"]
+        if al is not None:
+            rs.route_allocate(types, w.k_by_type, w.G, a["h"], L["router"], al["w_pri"], workspace=bf.workspace,
+                              out={"mask": bf.mask, "idx": bf.idx, "count": bf.count, "scores": bf.scores,
+                                   "priority": al["priority"], "k": al["k"]})
+        else:
+            rs.route(types, budget, w.G, h=a.get("h"), router=L["router"], scores_in=L["scores"],
+                     workspace=bf.workspace,
+                     out={"mask": bf.mask, "idx": bf.idx, "count": bf.count, "scores": bf.scores})
         rs.rotate_pack(a["v"], L["R"], bf.mask, w.G, cap, out=(bf.offsets, bf.Vp))
 
     def att(L):
@@ -465,14 +492,43 @@ def main():
     if not torch.equal(layers[-1]["bufs"].out, eager_out):
         raise RuntimeError("attention replay output differs from the eager pass")
 
+    alloc_us = None
+    if args.allocation:
+        # the allocation + selection kernel alone: the same call on the step's
+        # own priorities and scores (it rewrites identical budgets and masks)
+        def alloc_all():
+            for L in layers:
+                bf, al = L["bufs"], L["alloc"]
+                rs.allocate_groups(al["priority"], types, w.k_by_type, w.G, scores=bf.scores,
+                                   out={"k": al["k"], "mask": bf.mask, "idx": bf.idx, "count": bf.count})
+        if not args.eager:
+            g_alloc = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_alloc, stream=stream):
+                alloc_all()
+            alloc_run = g_alloc.replay
+        else:
+            alloc_run = alloc_all
+        alloc_run()
+        torch.cuda.synchronize()
+        a0.record()
+        for _ in range(reps):
+            alloc_run()
+        a1.record()
+        torch.cuda.synchronize()
+        alloc_us = a0.elapsed_time(a1) / (reps * len(layers)) * 1e3
+
     sum_k = int(layers[0]["bufs"].offsets[:, -1].sum().item()) // w.B
     per_stage = stage_bytes(w, sum_k)
+    if args.allocation:
+        # over the fixed-budget route: scores read again, priorities written
+        # and read, token types and the budgets K_i
+        per_stage["allocate"] = w.B * w.T * (4 * w.G + 8 + 1 + 1)
     a_bytes = per_stage["attend"]
     achieved = a_bytes / (att_ms * 1e-3) / 1e9
     value = w.B * w.Tq * w.L / (ms_step * 1e-3)
 
     line = {
-        "metric": METRIC,
+        "metric": ALLOC_METRIC if args.allocation else METRIC,
         "value": value,
         "unit": "query-tokens/s",
         "n_gpus": 1,
@@ -489,6 +545,8 @@ def main():
                    "heads": w.H, "head_dim": w.dh, "hidden": w.d, "groups": w.G,
                    "keep": {"vis": w.k_vis, "lang": w.k_lang, "prop": w.k_prop}
                    if w.mode == 0 else {"threshold": w.tau, "kmin": w.kmin, "kmax": w.kmax},
+                   "budgets": "role-driven per-token allocation within each type (priority w^T a)"
+                   if args.allocation else "fixed per type",
                    "value_counts": "query tokens x layers per second (B*Tq*L / step time)",
                    "graphs": not args.eager},
         "roofline": {"kernel": "rolesub_attend (k_attend_bf16)", "bound": "hbm",
@@ -497,11 +555,12 @@ def main():
                      "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": att_ms * 1e3},
         "detail": {"attend_query_tokens_per_s": w.B * w.Tq / (att_ms * 1e-3),
                    "layers_per_s": w.L / (ms_step * 1e-3),
+                   "allocate_select_us_per_layer": alloc_us,
                    "stage_algorithmic_bytes": per_stage,
                    "step_algorithmic_GBs": w.L * sum(per_stage.values()) / (ms_step * 1e-3) / 1e9},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w)
+        line["cpu_baseline"] = cpu_baseline(w, allocation=args.allocation)
     print(json.dumps(line), flush=True)
 
 

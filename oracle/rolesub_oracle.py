@@ -377,17 +377,24 @@ def attend_plain(q, k, v, mask, R, G, scale=None):
 # ----------------------------------------------------------------------------
 
 def pipeline(h, q, k, v, types, weights, mode, k_by_type, G, tau=0.0, kmin=0, kmax=0,
-             scores=None, cap=None):
+             scores=None, cap=None, w_pri=None):
     """route -> rotate -> pack -> attend for one layer.
 
     weights: dict with R and the MLP2 router weights (W_r, b_r, E, W1, b1, W2, b2).
-    scores: optional given logits (selection only). Returns a dict of every
-    intermediate."""
+    scores: optional given logits (selection only). w_pri: optional priority
+    weights per latent role; with them (fixed budgets only) the per-token
+    budgets come from the role-driven allocation of Sec. 3.5 on float32
+    priorities. Returns a dict of every intermediate."""
     T = np.asarray(k).shape[1]
     if scores is None:
         scores = router_mlp2(h, types, weights["W_r"], weights["b_r"], weights["E"],
                              weights["W1"], weights["b1"], weights["W2"], weights["b2"])
-    K = group_budget(scores, types, mode, k_by_type, G, tau, kmin, kmax)
+    if w_pri is not None:
+        assert mode == TOPK, "role-driven allocation distributes fixed per-type budgets"
+        pri = role_priority(h, weights["W_r"], weights["b_r"], w_pri).astype(np.float32)
+        K = allocate_groups(pri, types, k_by_type, G)
+    else:
+        K = group_budget(scores, types, mode, k_by_type, G, tau, kmin, kmax)
     mask = select_groups(scores, K)
     z = rotate(v, weights["R"])
     if cap is None:

@@ -747,3 +747,16 @@ def test_allocation_groups_are_per_sample_and_type():
     t2 = types.copy()
     t2[0, 3] = 7
     assert O.allocate_groups(pr, t2, kby, 8)[0, 3] == 8
+
+
+def test_pipeline_with_allocation_keeps_the_type_budgets():
+    w = synth.workload(1)
+    wt = synth.layer_weights(w, 0)
+    a = synth.layer_activations(w, 0)
+    wpri = synth.priority_weights(w, 0)
+    r = O.pipeline(a["h"], a["q"], a["k"], a["v"], w.types(), wt, w.mode, w.k_by_type, w.G, w_pri=wpri)
+    pri = O.role_priority(a["h"], wt["W_r"], wt["b_r"], wpri).astype(np.float32)
+    assert np.array_equal(r["K"], O.allocate_groups(pri, w.types(), w.k_by_type, w.G))
+    assert np.array_equal(O.popcount(r["mask"]), r["K"])
+    assert r["offsets"][0, -1] == 64 * 4 + 16 * 6        # same total as the fixed budgets
+    assert len(np.unique(r["K"][0][w.types() == O.VIS])) > 1   # budgets do vary by token
