@@ -28,7 +28,11 @@ notes of the repository):
     that does not divide evenly gives the first views one more token;
   * role-driven budget allocation: priorities are an input, quantised to
     integers, and each type's budget is apportioned by largest remainders
-    with a cap of G groups per token (details at allocate_groups).
+    with a cap of G groups per token (details at allocate_groups);
+  * full-width routing space (the paper's own operating point): one R over
+    all H*dh value dimensions, S groups of H*dh/S consecutive rotated
+    dimensions; a token keeping all S groups is cached in value space (its
+    routed value is v itself), a routed token caches its kept groups of z.
 
 Parity: every function here is pinned by CPU tests against closed forms, the
 paper's printed KV fractions, brute-force enumeration and textbook special
@@ -52,6 +56,7 @@ __all__ = [
     "attend_packed_causal", "attend_plain_causal",
     "retained_count", "split_evenly", "retain_tokens", "gather_tokens",
     "role_priority", "quantize_priority", "allocate_groups",
+    "rotate_full", "routed_values_full", "pack_full", "values_full", "attend_full", "attend_full_plain",
     "mask_to_idx", "popcount", "pack", "unpack", "expand_mask", "routed_values",
     "attend_packed", "attend_plain", "softmax", "pipeline",
     "kv_fraction", "packed_groups",
@@ -370,6 +375,102 @@ def attend_plain(q, k, v, mask, R, G, scale=None):
     s = np.einsum("bqhd,bthd->bhqt", q, k) * _scale(dh, scale)
     p = softmax(s, axis=-1)
     return np.einsum("bhqt,bthd->bqhd", p, vt)
+
+
+# ----------------------------------------------------------------------------
+# Full-width routing space (Sec. 3.2 with d_v = H * dh; Sec. 4.1 configuration)
+# ----------------------------------------------------------------------------
+
+def rotate_full(v, R):
+    """z = R^T v over the whole value vector (Sec. 3.2): v [B,T,H,dh] is read as
+    [B,T,d_v] with d_v = H*dh; R [d_v, d_v]; z_j = sum_k R[k, j] v_k."""
+    v = _f64(v)
+    B, T = v.shape[:2]
+    return v.reshape(B, T, -1) @ _f64(R)
+
+
+def routed_values_full(v, mask, R, S):
+    """v~ = R M R^T v over the whole value vector with M = diag(m_1 I, ..., m_S I)
+    (Sec. 3.2). v [B,T,H,dh], mask [B,T] (bit s = group s kept), R [d_v, d_v].
+    Returns [B,T,H,dh] float64."""
+    v = _f64(v)
+    B, T, H, dh = v.shape
+    R = _f64(R)
+    m = expand_mask(mask, S, H * dh)                 # [B,T,d_v]
+    z = v.reshape(B, T, -1) @ R
+    return ((z * m) @ R.T).reshape(B, T, H, dh)
+
+
+def pack_full(v, mask, R, S, cap):
+    """Compact cache of the full-width routed values: offsets [B,T+1] in group
+    units as pack(); Vp [B, cap, d_v/S]. A token that keeps all S groups is
+    stored as its value vector cut into S pieces (v~ = v exactly, since
+    R R^T = I); any other token stores its kept groups of z = R^T v in
+    ascending group order."""
+    v = _f64(v)
+    B, T, H, dh = v.shape
+    dv = H * dh
+    ds = dv // S
+    full = (1 << S) - 1
+    z = rotate_full(v, R)
+    vf = v.reshape(B, T, dv)
+    pc = popcount(np.asarray(mask, dtype=np.uint64) & np.uint64(full))
+    offsets = np.zeros((B, T + 1), dtype=np.int64)
+    offsets[:, 1:] = np.cumsum(pc, axis=1)
+    Vp = np.zeros((B, cap, ds))
+    for b in range(B):
+        for t in range(T):
+            mt = int(mask[b, t]) & full
+            src = vf[b, t] if mt == full else z[b, t]
+            r = 0
+            for g in range(S):
+                if (mt >> g) & 1:
+                    slot = offsets[b, t] + r
+                    if slot < cap:
+                        Vp[b, slot] = src[g * ds:(g + 1) * ds]
+                    r += 1
+    return offsets, Vp
+
+
+def values_full(offsets, Vp, mask, R, S, H):
+    """Routed values [B,T,H,dh] from the full-width cache: v for tokens keeping
+    all S groups, R z~ for the others (dropped groups are zero)."""
+    Vp, R = _f64(Vp), _f64(R)
+    B, cap, ds = Vp.shape
+    T = np.asarray(offsets).shape[1] - 1
+    dv = ds * S
+    full = (1 << S) - 1
+    out = np.zeros((B, T, dv))
+    for b in range(B):
+        for t in range(T):
+            mt = int(mask[b, t]) & full
+            zt = np.zeros(dv)
+            r = 0
+            for g in range(S):
+                if (mt >> g) & 1:
+                    zt[g * ds:(g + 1) * ds] = Vp[b, int(offsets[b, t]) + r]
+                    r += 1
+            out[b, t] = zt if mt == full else R @ zt
+    return out.reshape(B, T, H, dv // H)
+
+
+def attend_full(q, k, mask, offsets, Vp, R, S, scale=None):
+    """Method form at full width: textbook attention per head with unchanged
+    q, k (Sec. 3) over the routed values rebuilt from the cache."""
+    q, k = _f64(q), _f64(k)
+    H, dh = q.shape[2], q.shape[3]
+    vt = values_full(offsets, Vp, mask, R, S, H)
+    s_ = np.einsum("bqhd,bthd->bhqt", q, k) * _scale(dh, scale)
+    return np.einsum("bhqt,bthd->bqhd", softmax(s_, axis=-1), vt)
+
+
+def attend_full_plain(q, k, v, mask, R, S, scale=None):
+    """Plain form at full width: textbook attention over v~ = R M R^T v."""
+    q, k = _f64(q), _f64(k)
+    dh = q.shape[3]
+    vt = routed_values_full(v, mask, R, S)
+    s_ = np.einsum("bqhd,bthd->bhqt", q, k) * _scale(dh, scale)
+    return np.einsum("bhqt,bthd->bqhd", softmax(s_, axis=-1), vt)
 
 
 # ----------------------------------------------------------------------------

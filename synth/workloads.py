@@ -32,7 +32,7 @@ __all__ = [
     "VIS", "LANG", "PROP", "ACT", "TOPK", "THRESHOLD", "Workload", "WORKLOADS",
     "workload", "bf16_round", "round_to", "layer_weights", "additive_weights",
     "sample_activations", "layer_activations", "sample_scores", "synthetic_z",
-    "synthetic_masks", "haar_orthogonal", "priority_weights", "sample_priorities",
+    "synthetic_masks", "haar_orthogonal", "priority_weights", "sample_priorities", "full_rotation",
 ]
 
 
@@ -64,6 +64,7 @@ class Workload:
     tau: float = 0.0
     scores_in: bool = False          # selection from synthetic logits
     near_frac: float = 0.0           # fraction of tokens with near-threshold logits
+    full_width: bool = False         # one R over all H*dh value dims, G groups of H*dh/G
 
     @property
     def T(self) -> int:
@@ -71,7 +72,11 @@ class Workload:
 
     @property
     def ds(self) -> int:
-        return self.dh // self.G
+        return (self.H * self.dh if self.full_width else self.dh) // self.G
+
+    @property
+    def dv(self) -> int:
+        return self.H * self.dh
 
     @property
     def k_by_type(self) -> tuple:
@@ -111,6 +116,16 @@ WORKLOADS = {
                 n_lang=256, n_prop=0, Tq=64, dtype="bf16", mode=THRESHOLD, k_vis=32, k_lang=32,
                 k_prop=32, C=8, d_e=128, Hr=128, seed=5, kmin=1, kmax=32, tau=0.0,
                 scores_in=True, near_frac=0.3),
+    # The paper's own routing space (Sec. 4.1): one R over d_v = 4096, S = 16 groups of 256,
+    # C = 6 latent roles; 32 retained visual tokens (1/16 of 512) keep K_vis = 4 groups,
+    # language and proprio values uncompressed.
+    6: Workload(6, "7b-fullwidth-stack32-b64", B=64, L=32, H=32, dh=128, d=4096, G=16, n_vis=32,
+                n_lang=48, n_prop=1, Tq=56, dtype="bf16", mode=TOPK, k_vis=4, k_lang=16, k_prop=16,
+                C=6, d_e=128, Hr=128, seed=6, full_width=True),
+    # A smaller full-width case for whole-tensor parity: d_v = 1024, S = 16 groups of 64.
+    7: Workload(7, "fullwidth-small", B=3, L=1, H=8, dh=128, d=1024, G=16, n_vis=40, n_lang=20,
+                n_prop=1, Tq=16, dtype="bf16", mode=TOPK, k_vis=2, k_lang=16, k_prop=16, C=6,
+                d_e=128, Hr=128, seed=7, full_width=True),
 }
 
 
@@ -163,6 +178,7 @@ def haar_orthogonal(rng: np.random.Generator, n: int) -> np.ndarray:
 _W_R, _W_BR, _W_E, _W_W1, _W_B1, _W_W2, _W_B2, _W_TOK, _W_BTOK, _W_ROLE, _W_LANG, _W_BLANG = range(12)
 _W_ROT = 100
 _W_PRI = 101
+_W_ROT_FULL = 102
 # activation tensor ids inside a (layer, sample) (kind 1)
 _A_H, _A_Q, _A_K, _A_V, _A_S, _A_PERM, _A_J, _A_Z, _A_MASK, _A_PRI, _A_PRI_KIND = range(11)
 
@@ -300,3 +316,12 @@ def sample_priorities(w: Workload, layer: int, b: int) -> np.ndarray:
     x[kind == 4] = np.nan
     x[kind == 5] = (g.integers(1, 8, size=int(np.sum(kind == 5))) * 2.0 ** -16).astype(np.float32)
     return x
+
+
+def full_rotation(w: Workload, layer: int) -> dict:
+    """The layer's full-width rotation over d_v = H*dh value dims (Haar, Sec. 4.1
+    initialises R from a random Stiefel matrix): 'R_master' float64 and 'R'
+    rounded to the workload dtype, both [d_v, d_v] with R[k, j] the k-th value
+    coordinate of rotated coordinate j."""
+    m = haar_orthogonal(_rng(w.seed, layer, 0, 0, _W_ROT_FULL), w.dv)
+    return {"R_master": m, "R": round_to(m, w.dtype)}

@@ -760,3 +760,82 @@ def test_pipeline_with_allocation_keeps_the_type_budgets():
     assert np.array_equal(O.popcount(r["mask"]), r["K"])
     assert r["offsets"][0, -1] == 64 * 4 + 16 * 6        # same total as the fixed budgets
     assert len(np.unique(r["K"][0][w.types() == O.VIS])) > 1   # budgets do vary by token
+
+
+# ----------------------------------------------------------------------------
+# Full-width routing space (Sec. 3.2 with one R over all heads; Sec. 4.1)
+# ----------------------------------------------------------------------------
+
+def _block_rotation_full(R_heads, S):
+    """The full-width R that reproduces per-head routing with S groups: R_full =
+    blockdiag(R_h) with columns permuted so that full-width group s (d_v/S
+    consecutive dims) holds slice s of every head's rotated value."""
+    H, dh, _ = R_heads.shape
+    ds = dh // S
+    dv = H * dh
+    Rf = np.zeros((dv, dv))
+    for h in range(H):
+        for j in range(dh):
+            s, r = divmod(j, ds)
+            c = s * (H * ds) + h * ds + r
+            Rf[h * dh:(h + 1) * dh, c] = R_heads[h][:, j]
+    return Rf
+
+
+def test_full_width_with_block_rotation_equals_per_head_routing():
+    rng = np.random.default_rng(40)
+    H, dh, S, B, T, Tq = 4, 16, 4, 2, 9, 3
+    R_heads = np.stack([synth.haar_orthogonal(rng, dh) for _ in range(H)])
+    Rf = _block_rotation_full(R_heads, S)
+    assert np.allclose(Rf.T @ Rf, np.eye(H * dh), atol=1e-12)
+    q = rng.standard_normal((B, Tq, H, dh))
+    k = rng.standard_normal((B, T, H, dh))
+    v = rng.standard_normal((B, T, H, dh))
+    mask = rng.integers(0, 1 << S, size=(B, T)).astype(np.uint32)
+    mask[0, 0] = (1 << S) - 1
+    assert np.allclose(O.routed_values_full(v, mask, Rf, S), O.routed_values(v, mask, R_heads, S), atol=1e-12)
+    ref = O.attend_plain(q, k, v, mask, R_heads, S)
+    assert np.allclose(O.attend_full_plain(q, k, v, mask, Rf, S), ref, atol=1e-12)
+    off, Vp = O.pack_full(v, mask, Rf, S, T * S)
+    assert np.allclose(O.attend_full(q, k, mask, off, Vp, Rf, S), ref, atol=1e-12)
+
+
+def test_full_width_plane_rotation_closed_form():
+    th = 0.3
+    c, s_ = np.cos(th), np.sin(th)
+    R = np.array([[c, -s_], [s_, c]])
+    v = np.array([1.0, 0.0]).reshape(1, 1, 1, 2)
+    # z = R^T v = (c, -s); keeping group 0 leaves (c, 0); back: R (c, 0) = c (c, s)
+    got = O.routed_values_full(v, np.array([[1]], np.uint32), R, 2)
+    assert np.allclose(got.reshape(2), [c * c, c * s_], atol=1e-15)
+    got1 = O.routed_values_full(v, np.array([[2]], np.uint32), R, 2)
+    assert np.allclose(got1.reshape(2), [s_ * s_, -c * s_], atol=1e-15)   # the other group: the rest of v
+    assert np.allclose(got.reshape(2) + got1.reshape(2), [1.0, 0.0], atol=1e-15)
+
+
+def test_full_width_cache_special_cases():
+    rng = np.random.default_rng(41)
+    H, dh, S, B, T = 2, 8, 4, 2, 6
+    Rf = synth.haar_orthogonal(rng, H * dh)
+    v = rng.standard_normal((B, T, H, dh))
+    full = (1 << S) - 1
+    mask = np.array([[full, 0, 5, full, 1, 8], [3, full, full, 0, 15, 6]], np.uint32)
+    z = O.rotate_full(v, Rf)
+    assert np.allclose(z @ Rf.T, v.reshape(B, T, -1), atol=1e-12)                 # R R^T = I
+    assert np.allclose(np.sum(z ** 2, -1), np.sum(v.reshape(B, T, -1) ** 2, -1))  # Parseval
+    off, Vp = O.pack_full(v, mask, Rf, S, T * S)
+    assert off[0, -1] == 4 + 0 + 2 + 4 + 1 + 1
+    # a token keeping every group is cached as its value vector, exactly
+    assert np.array_equal(Vp[0, 0:4].reshape(-1), v[0, 0].reshape(-1))
+    # a routed token caches its kept groups of z, ascending
+    assert np.array_equal(Vp[0, 4:6], np.stack([z[0, 2, 0:4], z[0, 2, 8:12]]))
+    vt = O.values_full(off, Vp, mask, Rf, S, H)
+    assert np.array_equal(vt[0, 0], v[0, 0]) and np.all(vt[0, 1] == 0) and np.all(vt[1, 3] == 0)
+    assert np.allclose(vt, O.routed_values_full(v, mask, Rf, S), atol=1e-12)
+    # all groups kept everywhere: textbook attention
+    q = rng.standard_normal((B, 3, H, dh))
+    k = rng.standard_normal((B, T, H, dh))
+    allm = np.full((B, T), full, np.uint32)
+    sc = np.einsum("bqhd,bthd->bhqt", q, k) / np.sqrt(dh)
+    want = np.einsum("bhqt,bthd->bqhd", sp_softmax(sc, axis=-1), v)
+    assert np.allclose(O.attend_full_plain(q, k, v, allm, Rf, S), want, atol=1e-12)
