@@ -303,6 +303,53 @@ rolesub_status rolesub_route_allocate(const rolesub_dims* dims, rolesub_dtype dt
                                       uint8_t* k_out, uint32_t* mask, uint8_t* idx, uint8_t* count,
                                       void* workspace, size_t ws_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Full-width routing space (Sec. 3.2 with a single R over the whole value
+ * vector, d_v = H*dh; Sec. 4.1 uses d_v = 4096, S = 16 groups of 256).
+ * dims->G is S; group s is rotated dims [s*ds, (s+1)*ds), ds = d_v/S. One
+ * mask per token (bit s = group s kept), as rolesub_route writes with G = S.
+ * Cache: offsets [B,T+1] as rolesub_pack_kv; Vp [B,cap_groups,ds] (sample-
+ * major, one slot = one group of ds values). A token that keeps all S groups
+ * has R M R^T v = v and is stored in value space: its S consecutive slots
+ * hold v itself. Any other token stores its kept groups of z = R^T v in
+ * ascending group order. Requirements: bf16; dh = 128; 1 <= S <= 32 with ds a
+ * multiple of 32; B, T <= 4096; values, cache and R each below 2 GiB.
+ * workspace: at least rolesub_full_workspace_size(B, T) bytes of device
+ * scratch (per-sample routed-token lists), not kept between calls.
+ * ------------------------------------------------------------------------ */
+size_t rolesub_full_workspace_size(int32_t B, int32_t T);
+
+/* Rt[j][k] = R[k][j] for an n x n bf16 matrix (n a multiple of 64): the
+ * operand layout rolesub_full_rotate_pack takes. R is frozen per layer, so
+ * this runs once per layer, not per call. */
+rolesub_status rolesub_full_transpose(int32_t n, rolesub_dtype dtype, const void* R, void* Rt, void* stream);
+
+/* z = R^T v for the routed tokens, their kept groups and the value-space
+ * tokens into the cache (Sec. 3.2).
+ *   Rt   [d_v, d_v] = R^T (rolesub_full_transpose of R; R[k][j] is value
+ *        coordinate k of rotated coordinate j)
+ *   v    [B,T,H,dh] (= [B,T,d_v]); mask [B,T] uint32
+ *   offsets [B,T+1] int32 written; Vp [B,cap_groups,ds] written (slots at or
+ *        past cap_groups are never written; offsets still count them)
+ *   budget, type_counts: optional capacity check as rolesub_pack_kv. */
+rolesub_status rolesub_full_rotate_pack(const rolesub_dims* dims, rolesub_dtype dtype, const void* Rt,
+                                        const void* v, const uint32_t* mask, int32_t* offsets, void* Vp,
+                                        int64_t cap_groups, const rolesub_budget* budget,
+                                        const int32_t* type_counts, void* workspace, size_t ws_bytes,
+                                        void* stream);
+
+/* Routed values from the cache, head-major for attention (Sec. 3.2):
+ *   Vh[b,h,t,:] = (R z~_t)[h*dh : (h+1)*dh] for routed tokens (dropped groups
+ *   are zero, so a token keeping none gets 0), and v_t's slice for tokens
+ *   stored in value space.
+ *   R [d_v, d_v]; mask, offsets, Vp as written by rolesub_full_rotate_pack;
+ *   Vh [B,H,T,dh] written. rolesub_attend with G = 1, mask bit 0 set,
+ *   offsets[b,t] = t, Vp = Vh (cap_groups = T) and identity rotations then
+ *   gives the paper's attention over these values. */
+rolesub_status rolesub_full_values(const rolesub_dims* dims, rolesub_dtype dtype, const void* R,
+                                   const uint32_t* mask, const int32_t* offsets, const void* Vp, int64_t cap_groups,
+                                   void* Vh, void* workspace, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librolesub.so")
 SOURCES = ["rolesub_api.hip", "k_route.hip", "k_rotate.hip", "k_pack.hip", "k_attend.hip", "k_retain.hip",
-           "k_alloc.hip"]
+           "k_alloc.hip", "k_full.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

@@ -1,0 +1,380 @@
+// Full-width routing space (Sec. 3.2 with one R over the whole value vector,
+// d_v = H*dh; Sec. 4.1 runs d_v = 4096 with S = 16 groups of 256).
+//
+// Tokens that keep all S groups have R M R^T v = v, so the cache holds their
+// value vector (S consecutive slots = d_v contiguous values). Routed tokens
+// (any other mask) go through two dense contractions on the bf16 matrix cores:
+//   rotate:  z  = R^T v  for every routed token, only the kept groups stored;
+//   values:  v~ = R z~   for every routed token, written head-major
+//            [B][H][T][dh] for the attention kernel.
+// Both are one gather-GEMM C[m][n] = sum_k A[m][k] * Bt[n][k] over the routed
+// tokens of all samples (m), with Bt = R^T (rotate; the caller supplies the
+// transpose of the frozen R) or Bt = R (values), so that both operands are
+// read along k. A routed-token list per sample and the cache offsets come from
+// a small preparation kernel.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace rolesub {
+namespace {
+
+constexpr int kBM = 128, kBN = 128, kBK = 32;
+constexpr int kLd = kBK + 8;  // LDS row stride (elements): 80 bytes, conflict-free 16-byte fragment reads
+constexpr int kPrepChunks = 4;
+
+__device__ __forceinline__ uint32_t full_bits(int S) { return S >= 32 ? 0xFFFFFFFFu : ((1u << S) - 1u); }
+
+// Inclusive scan over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, kWave);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// Per sample: the routed-token list (and its length), the cache offsets
+// (PACK), and the value-space copies of the tokens that keep every group:
+// into the cache (PACK: v -> Vp) or from it into the head-major values
+// (!PACK: Vp -> Vh, at the given offsets). kPrepChunks workgroups per sample
+// share the copies; the first one writes the list, count and offsets.
+template <bool PACK>
+__global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
+  __shared__ int s_off[kFullMaxT + 1];
+  __shared__ uint16_t s_full[kFullMaxT];
+  __shared__ int wtot[4], wfull[4];
+  const int b = blockIdx.x / kPrepChunks, chunk = blockIdx.x % kPrepChunks;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int T = p.T, S = p.S;
+  const uint32_t full = full_bits(S);
+  const uint32_t* mk = p.mask + static_cast<size_t>(b) * T;
+  int run_pc = 0, run_rt = 0, run_full = 0;
+  for (int c0 = 0; c0 < T; c0 += 256) {
+    const int t = c0 + tid;
+    const bool valid = t < T;
+    const uint32_t m = valid ? (mk[t] & full) : 0u;
+    const bool routed = valid && m != full, isfull = valid && m == full;
+    // packed scan: kept-group count (low 16 bits, at most 256 * 32 per
+    // chunk) and routed flag (high bits); full tokens by ballot
+    const int x = (valid ? __popc(m) : 0) | (routed ? (1 << 16) : 0);
+    const int inc = wave_incl_scan(x);
+    const uint64_t bal = __ballot(isfull);
+    if (lane == 63) wtot[w] = inc;
+    if (lane == 0) wfull[w] = __popcll(bal);
+    __syncthreads();
+    int before = 0, before_full = 0;
+    for (int v = 0; v < w; ++v) {
+      before += wtot[v];
+      before_full += wfull[v];
+    }
+    const int ex = before + inc - x;
+    const int ex_pc = ex & 0xFFFF, ex_rt = ex >> 16;
+    const int ex_full = before_full + __popcll(bal & ((1ull << lane) - 1ull));
+    if (valid) s_off[t] = run_pc + ex_pc;
+    if (chunk == 0 && routed) p.rlist[static_cast<size_t>(b) * T + run_rt + ex_rt] = t;
+    if (isfull) s_full[run_full + ex_full] = static_cast<uint16_t>(t);
+    const int tot = wtot[0] + wtot[1] + wtot[2] + wtot[3];
+    run_pc += tot & 0xFFFF;
+    run_rt += tot >> 16;
+    run_full += wfull[0] + wfull[1] + wfull[2] + wfull[3];
+    __syncthreads();
+  }
+  if (chunk == 0) {
+    if (tid == 0) p.counts[b] = run_rt;
+    if (PACK) {
+      int32_t* off = p.offsets + static_cast<size_t>(b) * (T + 1);
+      for (int t = tid; t < T; t += 256) off[t] = s_off[t];
+      if (tid == 0) off[T] = run_pc;
+    }
+  }
+  // value-space copies of the full tokens: d_v/8 16-byte pieces each, work
+  // items (token, piece) spread over the chunk's threads, 8 loads in flight
+  const int pieces = p.dv / 8, dh = p.dv / p.H;
+  const int n_items = run_full * pieces;
+  const rsrc_t r_cache = make_rsrc(static_cast<const bf16*>(p.Vp) + static_cast<size_t>(b) * p.cap * p.ds,
+                                   clamp_bytes(static_cast<size_t>(p.cap) * p.ds * 2));
+  const rsrc_t r_v = make_rsrc(static_cast<const bf16*>(p.v) + static_cast<size_t>(b) * T * p.dv,
+                               clamp_bytes(static_cast<size_t>(T) * p.dv * 2));
+  const int32_t* goff = p.offsets + static_cast<size_t>(b) * (T + 1);
+  for (int i0 = (chunk * 256 + tid); i0 < n_items; i0 += 8 * 256 * kPrepChunks) {
+    u32x4 val[8];
+    int tok[8], pc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * 256 * kPrepChunks;
+      const bool ok = i < n_items;
+      tok[u] = ok ? s_full[i / pieces] : 0;
+      pc[u] = i % pieces;
+      uint32_t src;
+      if (PACK) {
+        src = oob_unless(ok, static_cast<uint32_t>((tok[u] * p.dv + 8 * pc[u]) * 2));
+        val[u] = bload16(r_v, src);
+      } else {
+        // the piece lies in slot o + 8 pc / ds of the token's S consecutive slots
+        const int o = ok ? goff[tok[u]] : 0;
+        const bool in_cap = o + (8 * pc[u]) / p.ds < p.cap;
+        src = oob_unless(ok && in_cap, static_cast<uint32_t>((static_cast<size_t>(o) * p.ds + 8 * pc[u]) * 2));
+        val[u] = bload16(r_cache, src);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * 256 * kPrepChunks;
+      if (i >= n_items) continue;
+      if (PACK) {
+        const int o = s_off[tok[u]];
+        if (o + (8 * pc[u]) / p.ds < p.cap) {
+          bf16* dst = static_cast<bf16*>(p.Vp) + (static_cast<size_t>(b) * p.cap + o) * p.ds + 8 * pc[u];
+          *reinterpret_cast<u32x4*>(dst) = val[u];
+        }
+      } else {
+        const int e = 8 * pc[u], h = e / dh;
+        bf16* dst = static_cast<bf16*>(p.Vh) + ((static_cast<size_t>(b) * p.H + h) * T + tok[u]) * dh + (e - h * dh);
+        *reinterpret_cast<u32x4*>(dst) = val[u];
+      }
+    }
+  }
+}
+
+// C[m][n] = sum_k A[m][k] * Bt[n][k] on 16x16x32 bf16 MFMA; 128 x 128 tile per
+// workgroup, four waves of 64 x 64, k in steps of 32 through a double-buffered
+// LDS tile (one barrier per step). Rows are the routed tokens of all samples,
+// in sample order; the workgroup maps its rows to (sample, token) through the
+// prefix of the per-sample counts. The 1D grid puts the column tiles
+// n = xcd + 8j on XCD xcd, so each XCD reads a quarter of Bt into its L2.
+//   MODE 0 (rotate): A = v rows, Bt = R^T; kept groups to the cache.
+//   MODE 1 (values): A = the cached groups of z~ (zero where dropped; steps of
+//   groups that no row of the tile keeps are skipped), Bt = R; head-major out.
+template <int MODE>
+__global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
+  // A and B tiles (double-buffered) in one region, reused for the output tile
+  constexpr int kTileA = kBM * kLd, kTileB = kBN * kLd;
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * kTileA + 2 * kTileB];
+  // tile i of A at smem + i * kTileA, of B at smem + 2 * kTileA + i * kTileB
+  __shared__ int pre[kFullMaxB + 1];
+  __shared__ int r_b[kBM], r_t[kBM], r_off[kBM];
+  __shared__ uint32_t r_mask[kBM];
+  __shared__ uint32_t s_or;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
+  const int B = p.B, T = p.T, dv = p.dv, S = p.S, ds = p.ds;
+  const int ntn = dv / kBN;
+  // column tile on this workgroup's XCD (consecutive ids go round-robin to 8 XCDs)
+  const int lin = blockIdx.x;
+  int nt, mt;
+  if ((ntn & 7) == 0) {
+    const int xcd = lin & 7, slot = lin >> 3, per = ntn >> 3;
+    nt = xcd + 8 * (slot % per);
+    mt = slot / per;
+  } else {
+    nt = lin % ntn;
+    mt = lin / ntn;
+  }
+  const int n0 = nt * kBN, m0 = mt * kBM;
+
+  // prefix of the routed counts (one wave, 64 samples per step)
+  if (w == 0) {
+    int run = 0;
+    for (int c0 = 0; c0 < B; c0 += 64) {
+      const int x = c0 + lane < B ? p.counts[c0 + lane] : 0;
+      const int inc = wave_incl_scan(x);
+      if (c0 + lane < B) pre[c0 + lane] = run + inc - x;
+      run += __shfl(inc, 63, kWave);
+    }
+    if (lane == 0) pre[B] = run;
+  }
+  if (tid == 0) s_or = 0;
+  __syncthreads();
+  const int total = pre[B];
+  if (m0 >= total) return;  // the same in every thread
+  if (tid < kBM) {
+    const int r = m0 + tid;
+    int bb = -1, tt = 0, oo = 0;
+    uint32_t mm = 0;
+    if (r < total) {
+      int lo = 0, hi = B - 1;  // largest bb with pre[bb] <= r
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (pre[mid] <= r) lo = mid; else hi = mid - 1;
+      }
+      bb = lo;
+      tt = p.rlist[static_cast<size_t>(bb) * T + (r - pre[bb])];
+      mm = p.mask[static_cast<size_t>(bb) * T + tt] & full_bits(S);
+      oo = p.offsets[static_cast<size_t>(bb) * (T + 1) + tt];
+      if (MODE == 1) atomicOr(&s_or, mm);
+    }
+    r_b[tid] = bb;
+    r_t[tid] = tt;
+    r_mask[tid] = mm;
+    r_off[tid] = oo;
+  }
+  __syncthreads();
+  const uint32_t tile_or = MODE == 1 ? s_or : full_bits(S);
+
+  // operand sources
+  const rsrc_t r_A = MODE == 0
+      ? make_rsrc(p.v, clamp_bytes(static_cast<size_t>(B) * T * dv * 2))
+      : make_rsrc(p.Vp, clamp_bytes(static_cast<size_t>(B) * p.cap * ds * 2));
+  const rsrc_t r_B = make_rsrc(p.Rm, clamp_bytes(static_cast<size_t>(dv) * dv * 2));
+  // this thread's two A pieces and two B pieces per step: piece q = tid + 256 u,
+  // row q / 4, 16-byte chunk q % 4
+  int arow[2], ach[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    arow[u] = (tid + 256 * u) >> 2;
+    ach[u] = (tid + 256 * u) & 3;
+  }
+  auto a_off = [&](int u, int k0) -> uint32_t {
+    const int row = arow[u];
+    const int bb = r_b[row];
+    if (MODE == 0) {
+      const size_t e = (static_cast<size_t>(bb) * T + r_t[row]) * dv + k0 + 8 * ach[u];
+      return oob_unless(bb >= 0, static_cast<uint32_t>(e * 2));
+    } else {
+      const int g = k0 / ds;
+      const uint32_t mm = r_mask[row];
+      const int slot = r_off[row] + __popc(mm & ((1u << g) - 1u));
+      const bool ok = bb >= 0 && ((mm >> g) & 1u) && slot < p.cap;
+      const size_t e = (static_cast<size_t>(bb) * p.cap + slot) * ds + (k0 - g * ds) + 8 * ach[u];
+      return oob_unless(ok, static_cast<uint32_t>(e * 2));
+    }
+  };
+  auto b_off = [&](int u, int k0) -> uint32_t {
+    const size_t e = static_cast<size_t>(n0 + arow[u]) * dv + k0 + 8 * ach[u];
+    return static_cast<uint32_t>(e * 2);
+  };
+  // k steps: every step of every group in tile_or (MODE 0: all groups)
+  auto next_k = [&](int k0) -> int {
+    const int k1 = k0 + kBK;
+    if (k1 >= dv) return dv;
+    if (k1 % ds != 0) return k1;
+    const uint32_t rest = tile_or >> (k1 / ds);
+    if (rest == 0) return dv;
+    return k1 + (__builtin_ctz(rest)) * ds;
+  };
+  int k0 = tile_or == 0 ? dv : __builtin_ctz(tile_or) * ds;
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int wm = w >> 1, wn = w & 1;
+  u32x4 ra[2], rbv[2];
+  if (k0 < dv) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      ra[u] = bload16(r_A, a_off(u, k0));
+      rbv[u] = bload16(r_B, b_off(u, k0));
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      *reinterpret_cast<u32x4*>(&(smem + (0) * kTileA)[arow[u] * kLd + 8 * ach[u]]) = ra[u];
+      *reinterpret_cast<u32x4*>(&(smem + 2 * kTileA + (0) * kTileB)[arow[u] * kLd + 8 * ach[u]]) = rbv[u];
+    }
+  }
+  __syncthreads();
+  int buf = 0;
+  while (k0 < dv) {
+    const int k1 = next_k(k0);
+    if (k1 < dv) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        ra[u] = bload16(r_A, a_off(u, k1));
+        rbv[u] = bload16(r_B, b_off(u, k1));
+      }
+    }
+    bf16x8 af[4], bfr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      af[i] = *reinterpret_cast<const bf16x8*>(&(smem + (buf) * kTileA)[(64 * wm + 16 * i + l16) * kLd + 8 * g4]);
+      bfr[i] = *reinterpret_cast<const bf16x8*>(&(smem + 2 * kTileA + (buf) * kTileB)[(64 * wn + 16 * i + l16) * kLd + 8 * g4]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x32(af[i], bfr[j], acc[i][j]);
+    if (k1 < dv) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        *reinterpret_cast<u32x4*>(&(smem + (buf ^ 1) * kTileA)[arow[u] * kLd + 8 * ach[u]]) = ra[u];
+        *reinterpret_cast<u32x4*>(&(smem + 2 * kTileA + (buf ^ 1) * kTileB)[arow[u] * kLd + 8 * ach[u]]) = rbv[u];
+      }
+    }
+    __syncthreads();
+    buf ^= 1;
+    k0 = k1;
+  }
+
+  // stage the bf16 tile in LDS (row stride kBN + 8), then 16-byte stores
+  constexpr int kCs = kBN + 8;
+  static_assert(kBM * kCs <= 2 * kTileA + 2 * kTileB, "C tile fits the A and B buffers");
+  bf16* Cs = smem;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        Cs[(64 * wm + 16 * i + 4 * g4 + e) * kCs + 64 * wn + 16 * j + l16] = static_cast<bf16>(acc[i][j][e]);
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kBM * kBN / 8 / 256; ++u) {
+    const int q = tid + 256 * u, row = q / (kBN / 8), c = q % (kBN / 8);
+    const int bb = r_b[row];
+    if (bb < 0) continue;
+    const u32x4 val = *reinterpret_cast<const u32x4*>(&Cs[row * kCs + 8 * c]);
+    const int n = n0 + 8 * c;
+    if (MODE == 0) {
+      const int g = n / ds;
+      const uint32_t mm = r_mask[row];
+      const int slot = r_off[row] + __popc(mm & ((1u << g) - 1u));
+      if (((mm >> g) & 1u) && slot < p.cap) {
+        bf16* dst = static_cast<bf16*>(p.Vp) + (static_cast<size_t>(bb) * p.cap + slot) * ds + (n - g * ds);
+        *reinterpret_cast<u32x4*>(dst) = val;
+      }
+    } else {
+      const int dh = dv / p.H, h = n / dh;
+      bf16* dst = static_cast<bf16*>(p.Vh) + ((static_cast<size_t>(bb) * p.H + h) * T + r_t[row]) * dh + (n - h * dh);
+      *reinterpret_cast<u32x4*>(dst) = val;
+    }
+  }
+}
+
+// Rt[j][k] = R[k][j] for an n x n bf16 matrix, 64 x 64 tiles through LDS.
+__global__ __launch_bounds__(256) void k_transpose_bf16(const bf16* __restrict__ R, bf16* __restrict__ Rt, int n) {
+  __shared__ bf16 tile[64][66];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int bx = blockIdx.x % (n / 64), by = blockIdx.x / (n / 64);
+  for (int r = ty; r < 64; r += 4) tile[r][tx] = R[static_cast<size_t>(by * 64 + r) * n + bx * 64 + tx];
+  __syncthreads();
+  for (int r = ty; r < 64; r += 4) Rt[static_cast<size_t>(bx * 64 + r) * n + by * 64 + tx] = tile[tx][r];
+}
+
+}  // namespace
+
+hipError_t launch_full(const FullParams& p, int mode, hipStream_t s) {
+  if (p.B == 0 || p.T == 0) return hipSuccess;
+  const dim3 gprep(static_cast<unsigned>(p.B) * kPrepChunks);
+  const unsigned ntn = static_cast<unsigned>(p.dv / kBN);
+  const unsigned nmt = static_cast<unsigned>((static_cast<size_t>(p.B) * p.T + kBM - 1) / kBM);
+  if (mode == 0) {
+    hipLaunchKernelGGL(k_full_prep<true>, gprep, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_full_gemm<0>, dim3(ntn * nmt), dim3(256), 0, s, p);
+  } else {
+    hipLaunchKernelGGL(k_full_prep<false>, gprep, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_full_gemm<1>, dim3(ntn * nmt), dim3(256), 0, s, p);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose(const void* R, void* Rt, int n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_transpose_bf16, dim3(static_cast<unsigned>((n / 64) * (n / 64))), dim3(256), 0, s,
+                     static_cast<const bf16*>(R), static_cast<bf16*>(Rt), n);
+  return hipGetLastError();
+}
+
+}  // namespace rolesub

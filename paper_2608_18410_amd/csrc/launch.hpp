@@ -63,6 +63,24 @@ struct AllocParams {
 };
 hipError_t launch_allocate(const AllocParams& p, hipStream_t s);
 
+// Full-width routing space: one R over d_v = H*dh value dims, S groups of ds.
+constexpr int kFullMaxT = 4096, kFullMaxB = 4096;
+struct FullParams {
+  int B, T, H, dv, S, ds;
+  int64_t cap;
+  const uint32_t* mask;  // [B][T]
+  int32_t* offsets;      // [B][T+1]: written by the rotate step, read by the values step
+  int32_t* counts;       // [B] routed tokens per sample (workspace)
+  int32_t* rlist;        // [B][T] routed token indices (workspace)
+  const void* v;         // [B][T][dv] (rotate)
+  const void* Rm;        // [dv][dv]: R^T (rotate) or R (values)
+  void* Vp;              // [B][cap][ds] cache: written (rotate) or read (values)
+  void* Vh;              // [B][H][T][dh] routed values (values)
+};
+// mode 0: rotate + pack; mode 1: values from the cache
+hipError_t launch_full(const FullParams& p, int mode, hipStream_t s);
+hipError_t launch_transpose(const void* R, void* Rt, int n, hipStream_t s);
+
 struct RotateParams {
   int ntok, T, H, G, tok_per_wg;
   const void* v;

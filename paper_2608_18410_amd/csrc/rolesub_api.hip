@@ -200,6 +200,44 @@ size_t route_allocate_ws_bytes(const rolesub_dims* d, const rolesub_router* r) {
   return route_ws_bytes(d, r) + align256(ntok * d->G * sizeof(float)) + align256(ntok * sizeof(float));
 }
 
+// Shapes the full-width kernels take; fills the shape part of p.
+rolesub_status full_setup(const char* fn, const rolesub_dims* dims, rolesub_dtype dtype, int64_t cap,
+                          void* workspace, size_t ws_bytes, FullParams& p) {
+  if (!dims) return fail(ROLESUB_ERR_INVALID_ARG, "%s: dims is NULL", fn);
+  if (dtype != ROLESUB_BF16) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: bf16 only", fn);
+  if (dims->B < 0 || dims->T < 0 || dims->H < 1)
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: need B >= 0, T >= 0, H >= 1", fn);
+  if (dims->dh != 128) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: head dim %d not supported (128)", fn, dims->dh);
+  const int64_t dv = static_cast<int64_t>(dims->H) * dims->dh;
+  const int S = dims->G;
+  if (S < 1 || S > 32 || dv % S != 0 || (dv / S) % 32 != 0)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: S=%d groups of d_v=%lld: need 1 <= S <= 32 and d_v/S a multiple of 32",
+                fn, S, static_cast<long long>(dv));
+  if (dims->T > kFullMaxT || dims->B > kFullMaxB)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: at most %d prefixes of %d tokens", fn, kFullMaxB, kFullMaxT);
+  if (cap < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: cap_groups < 0", fn);
+  const int64_t ds = dv / S;
+  if (static_cast<int64_t>(dims->B) * dims->T * dv * 2 >= static_cast<int64_t>(kMaxRegion) ||
+      static_cast<int64_t>(dims->B) * cap * ds * 2 >= static_cast<int64_t>(kMaxRegion) ||
+      dv * dv * 2 >= static_cast<int64_t>(kMaxRegion))
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: values, cache or R exceed 2 GiB", fn);
+  const size_t need = rolesub_full_workspace_size(dims->B, dims->T);
+  if (ws_bytes < need || (need && !workspace))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws_bytes);
+  p = FullParams{};
+  p.B = dims->B;
+  p.T = dims->T;
+  p.H = dims->H;
+  p.dv = static_cast<int>(dv);
+  p.S = S;
+  p.ds = static_cast<int>(ds);
+  p.cap = cap;
+  char* ws = static_cast<char*>(workspace);
+  p.counts = reinterpret_cast<int32_t*>(ws);
+  p.rlist = reinterpret_cast<int32_t*>(ws + align256(static_cast<size_t>(dims->B) * sizeof(int32_t)));
+  return ROLESUB_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -364,6 +402,69 @@ rolesub_status rolesub_route_allocate(const rolesub_dims* dims, rolesub_dtype dt
   a.idx = idx;
   a.count = count;
   return from_hip(launch_allocate(a, s), fn);
+}
+
+// ---------------------------------------------------------------------------
+// Full-width routing space
+
+size_t rolesub_full_workspace_size(int32_t B, int32_t T) {
+  if (B <= 0 || T <= 0) return 0;
+  return align256(static_cast<size_t>(B) * sizeof(int32_t)) + align256(static_cast<size_t>(B) * T * sizeof(int32_t));
+}
+
+rolesub_status rolesub_full_transpose(int32_t n, rolesub_dtype dtype, const void* R, void* Rt, void* stream) {
+  const char* fn = "rolesub_full_transpose";
+  if (dtype != ROLESUB_BF16) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: bf16 only", fn);
+  if (n < 0 || n % 64 != 0) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: n=%d must be a multiple of 64", fn, n);
+  if (n == 0) return ROLESUB_OK;
+  if (!R || !Rt) return fail(ROLESUB_ERR_INVALID_ARG, "%s: R and Rt must be non-NULL", fn);
+  if (ranges_overlap(R, static_cast<size_t>(n) * n * 2, Rt, static_cast<size_t>(n) * n * 2))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: Rt overlaps R", fn);
+  return from_hip(launch_transpose(R, Rt, n, static_cast<hipStream_t>(stream)), fn);
+}
+
+rolesub_status rolesub_full_rotate_pack(const rolesub_dims* dims, rolesub_dtype dtype, const void* Rt,
+                                        const void* v, const uint32_t* mask, int32_t* offsets, void* Vp,
+                                        int64_t cap_groups, const rolesub_budget* budget,
+                                        const int32_t* type_counts, void* workspace, size_t ws_bytes,
+                                        void* stream) {
+  const char* fn = "rolesub_full_rotate_pack";
+  FullParams p;
+  rolesub_status st = full_setup(fn, dims, dtype, cap_groups, workspace, ws_bytes, p);
+  if (st) return st;
+  if (static_cast<int64_t>(p.B) * p.T == 0) return ROLESUB_OK;
+  if (!Rt || !v || !mask || !offsets || !Vp)
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: Rt, v, mask, offsets and Vp must be non-NULL", fn);
+  st = check_capacity(dims, budget, type_counts, cap_groups, fn);
+  if (st) return st;
+  if (ranges_overlap(v, static_cast<size_t>(p.B) * p.T * p.dv * 2, Vp, static_cast<size_t>(p.B) * cap_groups * p.ds * 2))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: Vp overlaps v", fn);
+  p.mask = mask;
+  p.offsets = offsets;
+  p.v = v;
+  p.Rm = Rt;
+  p.Vp = Vp;
+  return from_hip(launch_full(p, 0, static_cast<hipStream_t>(stream)), fn);
+}
+
+rolesub_status rolesub_full_values(const rolesub_dims* dims, rolesub_dtype dtype, const void* R,
+                                   const uint32_t* mask, const int32_t* offsets, const void* Vp, int64_t cap_groups,
+                                   void* Vh, void* workspace, size_t ws_bytes, void* stream) {
+  const char* fn = "rolesub_full_values";
+  FullParams p;
+  rolesub_status st = full_setup(fn, dims, dtype, cap_groups, workspace, ws_bytes, p);
+  if (st) return st;
+  if (static_cast<int64_t>(p.B) * p.T == 0) return ROLESUB_OK;
+  if (!R || !mask || !offsets || !Vp || !Vh)
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: R, mask, offsets, Vp and Vh must be non-NULL", fn);
+  if (ranges_overlap(Vh, static_cast<size_t>(p.B) * p.T * p.dv * 2, Vp, static_cast<size_t>(p.B) * cap_groups * p.ds * 2))
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: Vh overlaps Vp", fn);
+  p.mask = mask;
+  p.offsets = const_cast<int32_t*>(offsets);
+  p.Rm = R;
+  p.Vp = const_cast<void*>(Vp);
+  p.Vh = Vh;
+  return from_hip(launch_full(p, 1, static_cast<hipStream_t>(stream)), fn);
 }
 
 rolesub_status rolesub_pack_kv(const rolesub_dims* dims, rolesub_dtype dtype, const rolesub_budget* budget,

@@ -65,3 +65,46 @@ def run_layer(h, q, k, v, types, R, budget: rs.Budget, G: int, bufs: LayerBuffer
                    out=(bufs.offsets, bufs.Vp), stream=stream)
     rs.attend(q, k, bufs.mask, bufs.offsets, bufs.Vp, R, G, out=bufs.out, stream=stream)
     return bufs
+
+
+@dataclass
+class FullWidthBuffers:
+    """Buffers of one full-width layer call: the cache (offsets, Vp), the
+    head-major routed values Vh, and the constants that let the attention
+    kernel read Vh as a one-group cache (unit masks, offsets[b,t] = t,
+    identity rotations)."""
+    offsets: torch.Tensor
+    Vp: torch.Tensor
+    Vh: torch.Tensor
+    out: torch.Tensor
+    workspace: torch.Tensor
+    ones: torch.Tensor
+    arange: torch.Tensor
+    eye: torch.Tensor
+
+    @staticmethod
+    def allocate(B, T, H, dh, S, Tq, cap, dtype, out_dtype=None, device="cuda"):
+        dv = H * dh
+        return FullWidthBuffers(
+            offsets=torch.empty((B, T + 1), dtype=torch.int32, device=device),
+            Vp=torch.empty((B, cap, dv // S), dtype=dtype, device=device),
+            Vh=torch.empty((B, H, T, dh), dtype=dtype, device=device),
+            out=torch.empty((B, Tq, H, dh), dtype=out_dtype or dtype, device=device),
+            workspace=torch.empty(max(rs.full_workspace_size(B, T), 256), dtype=torch.uint8, device=device),
+            ones=torch.ones((B, T), dtype=torch.int32, device=device),
+            arange=torch.arange(T + 1, dtype=torch.int32, device=device).repeat(B, 1).contiguous(),
+            eye=torch.eye(dh, dtype=dtype, device=device).repeat(H, 1, 1).contiguous(),
+        )
+
+
+def run_full_layer(q, k, v, mask, Rt, R, S: int, bufs: FullWidthBuffers, budget=None, type_counts=None,
+                   stream=None):
+    """Full-width routing space for one layer, given the group masks:
+    rotate + pack (routed tokens' kept groups of R^T v, value-space tokens
+    verbatim) -> routed values from the cache -> attention per head."""
+    B, T, H, dh = v.shape
+    rs.full_rotate_pack(v, Rt, mask, S, bufs.Vp.shape[1], budget=budget, type_counts=type_counts,
+                        workspace=bufs.workspace, out=(bufs.offsets, bufs.Vp), stream=stream)
+    rs.full_values(R, mask, bufs.offsets, bufs.Vp, S, H, workspace=bufs.workspace, out=bufs.Vh, stream=stream)
+    rs.attend(q, k, bufs.ones, bufs.arange, bufs.Vh, bufs.eye, 1, out=bufs.out, stream=stream)
+    return bufs

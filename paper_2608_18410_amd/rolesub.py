@@ -26,6 +26,7 @@ EXPORTS = (
     "rolesub_pack_kv", "rolesub_rotate_pack", "rolesub_attend_workspace_size", "rolesub_attend",
     "rolesub_attend_causal", "rolesub_retain_tokens", "rolesub_gather_tokens",
     "rolesub_allocate_groups", "rolesub_route_allocate_workspace_size", "rolesub_route_allocate",
+    "rolesub_full_workspace_size", "rolesub_full_transpose", "rolesub_full_rotate_pack", "rolesub_full_values",
 )
 
 
@@ -87,6 +88,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rolesub_allocate_groups.argtypes = [I32, I32, I32, P, P, P, P, P, P, P, P, P]
     lib.rolesub_route_allocate_workspace_size.argtypes = [P, P]
     lib.rolesub_route_allocate.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.rolesub_full_workspace_size.argtypes = [I32, I32]
+    lib.rolesub_full_workspace_size.restype = SZ
+    lib.rolesub_full_transpose.argtypes = [I32, ctypes.c_int, P, P, P]
+    lib.rolesub_full_rotate_pack.argtypes = [P, ctypes.c_int, P, P, P, P, P, I64, P, P, P, SZ, P]
+    lib.rolesub_full_values.argtypes = [P, ctypes.c_int, P, P, P, P, I64, P, P, SZ, P]
     for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_rotate_pack",
                "rolesub_attend"):
         getattr(lib, fn).restype = ctypes.c_int
@@ -375,3 +381,55 @@ def route_allocate(token_type, k_by_type, G: int, h, router: Router, w_pri, *, w
         kby, _ptr(h), _ptr(token_type, torch.uint8), _ptr(pri), _ptr(sco), _ptr(kk), _ptr(mask), _ptr(idx),
         _ptr(cnt), _ptr(workspace), workspace.numel(), _stream(stream)))
     return {"mask": mask, "idx": idx, "count": cnt, "k": kk, "scores": sco, "priority": pri}
+
+
+# ----------------------------------------------------------------------------
+# Full-width routing space (one R over all H*dh value dims, S groups)
+# ----------------------------------------------------------------------------
+
+def full_workspace_size(B, T) -> int:
+    return load().rolesub_full_workspace_size(B, T)
+
+
+def full_transpose(R, out=None, stream=None):
+    """R^T of a frozen [d_v, d_v] rotation (the layout full_rotate_pack takes)."""
+    n = R.shape[0]
+    Rt = torch.empty_like(R) if out is None else out
+    _check("rolesub_full_transpose", load().rolesub_full_transpose(n, _code(R), _ptr(R), _ptr(Rt, R.dtype),
+                                                                   _stream(stream)))
+    return Rt
+
+
+def full_rotate_pack(v, Rt, mask, S: int, cap: int, budget: Budget | None = None, type_counts=None,
+                     workspace=None, out=None, stream=None):
+    """Full-width cache: (offsets [B,T+1] int32, Vp [B,cap,d_v/S])."""
+    B, T, H, dh = v.shape
+    dv = H * dh
+    if out is None:
+        out = (torch.empty((B, T + 1), dtype=torch.int32, device=v.device),
+               torch.empty((B, cap, dv // S), dtype=v.dtype, device=v.device))
+    offsets, Vp = out
+    if workspace is None:
+        workspace = torch.empty(max(full_workspace_size(B, T), 1), dtype=torch.uint8, device=v.device)
+    tc = (ctypes.c_int32 * 4)(*[int(x) for x in type_counts]) if type_counts is not None else None
+    dims = Dims(B, T, H, dh, S, 0)
+    _check("rolesub_full_rotate_pack", load().rolesub_full_rotate_pack(
+        ctypes.byref(dims), _code(v), _ptr(Rt, v.dtype), _ptr(v), _ptr(mask), _ptr(offsets, torch.int32),
+        _ptr(Vp, v.dtype), cap, ctypes.byref(budget) if budget is not None else None, tc, _ptr(workspace),
+        workspace.numel(), _stream(stream)))
+    return offsets, Vp
+
+
+def full_values(R, mask, offsets, Vp, S: int, H: int, workspace=None, out=None, stream=None):
+    """Routed values [B,H,T,dh] (head-major) from the full-width cache."""
+    B, cap, ds = Vp.shape
+    T = offsets.shape[1] - 1
+    dh = ds * S // H
+    Vh = torch.empty((B, H, T, dh), dtype=Vp.dtype, device=Vp.device) if out is None else out
+    if workspace is None:
+        workspace = torch.empty(max(full_workspace_size(B, T), 1), dtype=torch.uint8, device=Vp.device)
+    dims = Dims(B, T, H, dh, S, 0)
+    _check("rolesub_full_values", load().rolesub_full_values(
+        ctypes.byref(dims), _code(Vp), _ptr(R, Vp.dtype), _ptr(mask), _ptr(offsets, torch.int32), _ptr(Vp),
+        cap, _ptr(Vh, Vp.dtype), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return Vh

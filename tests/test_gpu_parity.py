@@ -522,7 +522,7 @@ def _route_check(w, h, types, router, wt_or_scores_fn, label):
     return r
 
 
-@pytest.mark.parametrize("cid,B", [(1, 1), (2, 1), (3, 16), (5, 2)])
+@pytest.mark.parametrize("cid,B", [(1, 1), (2, 1), (3, 16), (5, 2), (6, 2)])
 def test_route_mlp2(cid, B):
     w = synth.workload(cid).replace(B=B)
     wt = synth.layer_weights(w, 0)
@@ -667,3 +667,155 @@ def test_pipeline_stress_full_batch_sampled():
     K = O.group_budget(scores, stack_types(w), O.THRESHOLD, w.k_by_type, w.G, 0.0, 1, 32)
     assert np.array_equal(host(bufs.count).astype(np.int64), K)
     assert np.array_equal(host(bufs.offsets)[:, -1], K.sum(axis=1))
+
+
+# ----------------------------------------------------------------------------
+# Full-width routing space (one R over d_v = H*dh, S groups; Sec. 3.2, 4.1)
+# ----------------------------------------------------------------------------
+
+def _full_masks(rng, w, B, kinds=None):
+    """Masks for the full-width tests: the workload's per-type budgets with
+    random kept groups, plus special samples: kinds[b] = 'budget', 'all_full',
+    'all_routed' (random K in 0..S-1, K = 0 included) or 'mixed'."""
+    S, T = w.G, w.T
+    full = (1 << S) - 1
+    kinds = kinds or ["budget"] * B
+    kk = np.array([w.k_vis] * w.n_vis + [w.k_lang] * w.n_lang + [w.k_prop] * w.n_prop)
+    out = np.zeros((B, T), dtype=np.uint32)
+    for b in range(B):
+        if kinds[b] == "all_full":
+            K = np.full(T, S)
+        elif kinds[b] == "all_routed":
+            K = rng.integers(0, S, size=T)
+            K[:3] = 0
+        elif kinds[b] == "mixed":
+            K = rng.integers(0, S + 1, size=T)
+        else:
+            K = kk
+        for t in range(T):
+            gs = rng.choice(S, size=int(K[t]), replace=False)
+            out[b, t] = int(np.sum(1 << gs.astype(np.int64))) if len(gs) else 0
+    assert np.all(out <= full)
+    return out
+
+
+def _full_case(w, B, seed, kinds=None):
+    rng = np.random.default_rng(seed)
+    R = synth.full_rotation(w, 0)["R"]
+    v = synth.round_to(rng.standard_normal((B, w.T, w.H, w.dh)), "bf16")
+    mask = _full_masks(rng, w, B, kinds)
+    return R, v, mask
+
+
+def _dev_bf16(a):
+    return put(a, torch.bfloat16)
+
+
+def test_full_transpose_exact():
+    for n in (1024, 4096):
+        R = synth.round_to(np.random.default_rng(n).standard_normal((n, n)), "bf16")
+        got = host(rs.full_transpose(_dev_bf16(R)))
+        assert np.array_equal(got, R.T)
+
+
+@pytest.mark.parametrize("cid,B,kinds,T", [
+    (7, 3, ["budget", "mixed", "all_routed"], None),
+    (7, 4, ["all_full", "budget", "mixed", "budget"], 200),      # ragged T, one sample with no routed token
+    (6, 2, ["budget", "mixed"], None),                           # d_v = 4096, S = 16 groups of 256
+])
+def test_full_rotate_pack(cid, B, kinds, T):
+    w = synth.workload(cid)
+    if T is not None:
+        w = w.replace(n_vis=T - w.n_lang - w.n_prop)
+    R, v, mask = _full_case(w, B, 50 + cid, kinds)
+    S = w.G
+    cap = w.T * S
+    Rd = _dev_bf16(R)
+    off, Vp = rs.full_rotate_pack(_dev_bf16(v), rs.full_transpose(Rd), put_mask(mask), S, cap)
+    torch.cuda.synchronize()
+    want_off, want_Vp = O.pack_full(v, mask, R, S, cap)
+    got_off, got_Vp = host(off), host(Vp)
+    assert np.array_equal(got_off, want_off)
+    full = (1 << S) - 1
+    routed_slot = np.zeros((B, cap), dtype=bool)
+    full_slot = np.zeros((B, cap), dtype=bool)
+    for b in range(B):
+        for t in range(w.T):
+            o, n = want_off[b, t], want_off[b, t + 1] - want_off[b, t]
+            (full_slot if int(mask[b, t]) == full else routed_slot)[b, o:o + n] = True
+    assert np.array_equal(got_Vp[full_slot], want_Vp[full_slot])            # value-space tokens: exact copies
+    if routed_slot.any():
+        err = max_rel(got_Vp[routed_slot], want_Vp[routed_slot])
+        _say(f"full rotate+pack workload {cid} B={B} T={w.T}: routed groups max rel err {err:.2e}")
+        assert err <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("cid,B,kinds", [(7, 3, ["budget", "all_routed", "mixed"]), (6, 2, ["budget", "mixed"])])
+def test_full_values(cid, B, kinds):
+    w = synth.workload(cid)
+    R, v, mask = _full_case(w, B, 60 + cid, kinds)
+    S = w.G
+    cap = w.T * S
+    off, Vp = O.pack_full(v, mask, R, S, cap)
+    Vp = synth.round_to(Vp, "bf16")                 # the cache as the GPU stores it
+    got = host(rs.full_values(_dev_bf16(R), put_mask(mask), torch.from_numpy(off.astype(np.int32)).to(DEV),
+                              _dev_bf16(Vp), S, w.H))
+    want = O.values_full(off, Vp, mask, R, S, w.H).transpose(0, 2, 1, 3)   # [B,H,T,dh]
+    err = max_rel(got, want)
+    _say(f"full values workload {cid} B={B}: max rel err {err:.2e}")
+    assert err <= TOL["bf16"]
+    full = (1 << S) - 1
+    for b in range(B):
+        for t in range(w.T):
+            if int(mask[b, t]) == full:                                     # value-space tokens: exact
+                assert np.array_equal(got[b, :, t], want[b, :, t])
+            elif int(mask[b, t]) == 0:
+                assert np.all(got[b, :, t] == 0)
+
+
+@pytest.mark.parametrize("cid,B,kinds", [(7, 3, ["budget", "mixed", "all_routed"]), (6, 4, None)])
+def test_full_width_attention_end_to_end(cid, B, kinds):
+    from paper_2608_18410_amd.pipeline import FullWidthBuffers, run_full_layer
+    w = synth.workload(cid).replace(B=B)
+    R, v, mask = _full_case(w, B, 70 + cid, kinds)
+    rng = np.random.default_rng(71 + cid)
+    q = synth.round_to(rng.standard_normal((B, w.Tq, w.H, w.dh)), "bf16")
+    k = synth.round_to(rng.standard_normal((B, w.T, w.H, w.dh)), "bf16")
+    S = w.G
+    cap = sum(n * min(kk, S) for n, kk in zip(w.type_counts(), w.k_by_type)) if kinds is None else w.T * S
+    bufs = FullWidthBuffers.allocate(B, w.T, w.H, w.dh, S, w.Tq, cap, torch.bfloat16, out_dtype=torch.float32,
+                                     device=DEV)
+    Rd = _dev_bf16(R)
+    budget = rs.make_budget(rs.TOPK, w.k_by_type) if kinds is None else None
+    run_full_layer(_dev_bf16(q), _dev_bf16(k), _dev_bf16(v), put_mask(mask), rs.full_transpose(Rd), Rd, S, bufs,
+                   budget=budget, type_counts=w.type_counts() if kinds is None else None)
+    torch.cuda.synchronize()
+    want = O.attend_full_plain(q, k, v, mask, R, S)
+    err = max_rel(host(bufs.out), want)
+    _say(f"full-width attention workload {cid} B={B}: max rel err {err:.2e} vs the plain form")
+    assert err <= TOL["bf16"]
+
+
+def test_full_width_stack_shape_sampled():
+    """The 7B full-width layer at its full batch (64 prefixes, d_v = 4096,
+    S = 16) in the launch configuration the bench times; oracle on 3 prefixes."""
+    from paper_2608_18410_amd.pipeline import FullWidthBuffers, run_full_layer
+    w = synth.workload(6)
+    B = w.B
+    R, v, mask = _full_case(w, B, 80)
+    rng = np.random.default_rng(81)
+    q = synth.round_to(rng.standard_normal((B, w.Tq, w.H, w.dh)), "bf16")
+    k = synth.round_to(rng.standard_normal((B, w.T, w.H, w.dh)), "bf16")
+    S = w.G
+    cap = sum(n * min(kk, S) for n, kk in zip(w.type_counts(), w.k_by_type))
+    bufs = FullWidthBuffers.allocate(B, w.T, w.H, w.dh, S, w.Tq, cap, torch.bfloat16, device=DEV)
+    Rd = _dev_bf16(R)
+    run_full_layer(_dev_bf16(q), _dev_bf16(k), _dev_bf16(v), put_mask(mask), rs.full_transpose(Rd), Rd, S, bufs,
+                   budget=rs.make_budget(rs.TOPK, w.k_by_type), type_counts=w.type_counts())
+    torch.cuda.synchronize()
+    got = host(bufs.out)
+    for b in (0, 31, 63):
+        want = O.attend_full_plain(q[b:b + 1], k[b:b + 1], v[b:b + 1], mask[b:b + 1], R, S)
+        err = max_rel(got[b:b + 1], want)
+        _say(f"full-width stack prefix {b}: max rel err {err:.2e}")
+        assert err <= TOL["bf16"]
