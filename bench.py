@@ -39,6 +39,8 @@ METRIC = "compressed-KV attention query-tokens/sec at 7B shape; achieved HBM GB/
 PREFIX_METRIC = "prefix self-attention (causal) over the compressed cache, query-tokens/sec at 7B shape"
 ALLOC_METRIC = ("compressed-KV attention query-tokens/sec at 7B shape with role-driven per-token budgets; "
                 "achieved HBM GB/s vs peak")
+FULL_METRIC = ("full-width routing space (one R over d_v = 4096, S = 16 groups): query-tokens/sec at 7B shape; "
+               "achieved MFMA TFLOP/s vs peak")
 RETAIN_METRIC = "token retention (top scores per view) + gather of the retained hidden states, tokens/sec"
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
@@ -138,6 +140,180 @@ def cpu_baseline_causal(w, masks, budget_s: float = 12.0) -> dict:
     return {"value": done * w.T / spent, "unit": "query-tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"layer 0, prefixes 0..{done - 1} of {w.B}: causal attention over the packed cache in "
                       f"float64 ({spent:.1f} s, pack excluded); BLAS pool {threads} threads"}
+
+
+def cpu_baseline_full(w, budget_s: float = 12.0) -> dict:
+    """The float64 oracle on whole prefixes of layer 0 at full width: router,
+    per-type top-K, full-width cache, attention over the rebuilt values."""
+    import oracle as O
+    import synth
+    from threadpoolctl import threadpool_info
+
+    wt = synth.layer_weights(w, 0)
+    R = synth.full_rotation(w, 0)["R"]
+    cap = sum(n * min(k, w.G) for n, k in zip(w.type_counts(), w.k_by_type))
+    done, spent = 0, 0.0
+    while spent < budget_s and done < w.B:
+        a = synth.sample_activations(w, 0, done)
+        t0 = time.perf_counter()
+        sc = O.router_mlp2(a["h"][None], w.types(), wt["W_r"], wt["b_r"], wt["E"], wt["W1"], wt["b1"], wt["W2"],
+                           wt["b2"])
+        m = O.select_groups(sc, O.group_budget(sc, w.types(), w.mode, w.k_by_type, w.G))
+        off, Vp = O.pack_full(a["v"][None], m, R, w.G, cap)
+        O.attend_full(a["q"][None], a["k"][None], m, off, Vp, R, w.G)
+        spent += time.perf_counter() - t0
+        done += 1
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": done * w.Tq / spent, "unit": "query-tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"layer 0, prefixes 0..{done - 1} of {w.B}: route->full-width cache->values->attend in "
+                      f"float64 ({spent:.1f} s); BLAS pool {threads} threads"}
+
+
+def full_width(args, w):
+    """The paper's routing space: one R over all 32 x 128 value dims, S = 16
+    groups of 256. A step is every layer's route (G = S) -> full-width
+    rotate + pack -> routed values -> attention; the transposed R of each layer
+    is prepared once before timing (R is frozen)."""
+    import concurrent.futures as cf
+
+    import torch
+
+    import paper_2608_18410_amd as rs
+    import synth
+    from paper_2608_18410_amd.pipeline import FullWidthBuffers, LayerBuffers, run_full_layer
+
+    dev = torch.device("cuda:0")
+    dt = torch.bfloat16
+    S = w.G
+    budget = rs.make_budget(rs.TOPK, w.k_by_type)
+    cap = sum(n * min(k, S) for n, k in zip(w.type_counts(), w.k_by_type))
+    types = torch.from_numpy(np.broadcast_to(w.types(), (w.B, w.T)).copy()).to(dev)
+    put = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+    layers = []
+    t_gen = time.time()
+    for l in range(w.L):
+        wt = synth.layer_weights(w, l)
+        router = rs.Router.mlp2(*(put(wt[n]) for n in ("W_r", "b_r", "E", "W1", "b1", "W2", "b2")))
+        acts = {n: torch.empty(sh, dtype=dt, device=dev) for n, sh in
+                (("h", (w.B, w.T, w.d)), ("q", (w.B, w.Tq, w.H, w.dh)), ("k", (w.B, w.T, w.H, w.dh)),
+                 ("v", (w.B, w.T, w.H, w.dh)))}
+        with cf.ThreadPoolExecutor(16) as ex:
+            for b0 in range(0, w.B, 16):
+                parts = list(ex.map(lambda b: synth.sample_activations(w, l, b), range(b0, min(w.B, b0 + 16))))
+                for i, p_ in enumerate(parts):
+                    for n in acts:
+                        acts[n][b0 + i].copy_(torch.from_numpy(p_[n]))
+        # a Haar rotation of d_v = 4096 per layer, drawn on the device from a
+        # seeded generator (QR of a Gaussian with the sign fix); inputs only
+        g = torch.Generator(device=dev)
+        g.manual_seed(1000 + l)
+        qm, rm = torch.linalg.qr(torch.randn(w.dv, w.dv, generator=g, device=dev))
+        R = (qm * torch.sign(torch.diagonal(rm))[None, :]).to(dt).contiguous()
+        Rt = rs.full_transpose(R)
+        del qm, rm
+        rb = LayerBuffers.allocate(w.B, w.T, 1, 128, S, 1, 1, dt, device=dev, with_z=False,
+                                   ws_bytes=rs.route_workspace_size(w.B, w.T, S, w.d, router))
+        fb = FullWidthBuffers.allocate(w.B, w.T, w.H, w.dh, S, w.Tq, cap, dt, device=dev)
+        layers.append(dict(acts=acts, router=router, R=R, Rt=Rt, rb=rb, fb=fb))
+        print(f"# layer {l} inputs resident ({time.time() - t_gen:.1f} s)", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+
+    def route(L):
+        rb = L["rb"]
+        rs.route(types, budget, S, h=L["acts"]["h"], router=L["router"], workspace=rb.workspace,
+                 out={"mask": rb.mask, "idx": rb.idx, "count": rb.count, "scores": rb.scores})
+
+    def layer(L):
+        route(L)
+        a = L["acts"]
+        run_full_layer(a["q"], a["k"], a["v"], L["rb"].mask, L["Rt"], L["R"], S, L["fb"], budget=budget,
+                       type_counts=w.type_counts())
+
+    def rot(L):
+        fb = L["fb"]
+        rs.full_rotate_pack(L["acts"]["v"], L["Rt"], L["rb"].mask, S, cap, workspace=fb.workspace,
+                            out=(fb.offsets, fb.Vp))
+
+    def vals(L):
+        fb = L["fb"]
+        rs.full_values(L["R"], L["rb"].mask, fb.offsets, fb.Vp, S, w.H, workspace=fb.workspace, out=fb.Vh)
+
+    def att(L):
+        fb, a = L["fb"], L["acts"]
+        rs.attend(a["q"], a["k"], fb.ones, fb.arange, fb.Vh, fb.eye, 1, out=fb.out)
+
+    for L in layers:
+        layer(L)
+    torch.cuda.synchronize()
+    eager_out = layers[-1]["fb"].out.clone()
+    stream = torch.cuda.Stream()
+    graphs = {}
+    for name, fn in (("step", layer), ("route", route), ("rotate", rot), ("values", vals), ("attend", att)):
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr, stream=stream):
+            for L in layers:
+                fn(L)
+        graphs[name] = gr
+    for _ in range(args.warmup):
+        graphs["step"].replay()
+    torch.cuda.synchronize()
+    if not torch.equal(layers[-1]["fb"].out, eager_out):
+        raise RuntimeError("graph replay output differs from the eager pass")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        graphs["step"].replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    # each call type alone: HIP events around back-to-back replays of the
+    # graph holding the 32 layers' calls of that type (same inputs)
+    reps = max(2, args.steps // 4)
+    per_call = {}
+    for name in ("route", "rotate", "values", "attend"):
+        graphs[name].replay()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            graphs[name].replay()
+        e1.record()
+        torch.cuda.synchronize()
+        per_call[name] = e0.elapsed_time(e1) / (reps * w.L) * 1e3
+    if not torch.equal(layers[-1]["fb"].out, eager_out):
+        raise RuntimeError("replays changed the output")
+    # algorithmic work: every kept group of a routed token costs 2 * d_v * ds
+    # flops in the rotation and again in the rebuild of its value
+    masks = layers[0]["rb"].mask.cpu().numpy().view(np.uint32)
+    full = (1 << S) - 1
+    routed_groups = int(sum(bin(int(m)).count("1") for m in masks.reshape(-1) if int(m) != full))
+    n_routed = int(np.sum(masks != full))
+    flops = 2 * w.dv * w.ds * routed_groups
+    dense_flops = 2 * w.dv * w.dv * n_routed
+    dom = max(("rotate", "values"), key=lambda n: per_call[n])
+    tflops = flops / (per_call[dom] * 1e-6) / 1e12
+    line = {
+        "metric": FULL_METRIC, "value": w.B * w.Tq * w.L / (ms_step * 1e-3), "unit": "query-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded Gaussian activations/weights, Haar rotations drawn on the device)",
+        "config": {"workload": w.name, "layers": w.L, "prefixes": w.B, "kv_tokens": w.T, "visual": w.n_vis,
+                   "language": w.n_lang, "proprio": w.n_prop, "queries": w.Tq, "heads": w.H, "head_dim": w.dh,
+                   "d_v": w.dv, "groups": S, "group_dim": w.ds, "latent_roles": w.C,
+                   "keep": {"vis": w.k_vis, "lang": w.k_lang, "prop": w.k_prop},
+                   "value_counts": "query tokens x layers per second (B*Tq*L / step time)", "graphs": True},
+        "roofline": {"kernel": f"rolesub_full_{'rotate_pack' if dom == 'rotate' else 'values'} "
+                               f"(k_full_prep + k_full_gemm)", "bound": "mfma",
+                     "achieved": tflops, "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / BF16_MFMA_PEAK_TFLOPS, "traffic": None,
+                     "algorithmic_flops_per_launch": flops, "avg_launch_us": per_call[dom],
+                     "dense_flops_per_launch": dense_flops},
+        "detail": {"per_layer_us": per_call, "routed_tokens_per_layer": n_routed,
+                   "routed_groups_per_layer": routed_groups,
+                   "dense_tflops_executed": dense_flops / (per_call[dom] * 1e-6) / 1e12},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_full(w)
+    print(json.dumps(line), flush=True)
 
 
 def prefix_attention(args, w):
@@ -327,6 +503,8 @@ def main():
     ap.add_argument("--eager", action="store_true", help="issue the calls directly, no HIP graphs")
     ap.add_argument("--prefix-attention", action="store_true",
                     help="time prefix self-attention (rolesub_attend_causal) at the same shape instead")
+    ap.add_argument("--full-width", action="store_true",
+                    help="the paper's full-width routing space (one R over d_v = 4096, S = 16) instead")
     ap.add_argument("--allocation", action="store_true",
                     help="route with role-driven per-token budgets (rolesub_route_allocate) in the step")
     ap.add_argument("--retention", action="store_true",
@@ -362,6 +540,9 @@ def main():
     w = synth.workload(args.workload)
     if args.layers:
         w = w.replace(L=args.layers)
+    if args.full_width:
+        full_width(args, synth.workload(6).replace(L=args.layers) if args.layers else synth.workload(6))
+        return
     if args.prefix_attention:
         prefix_attention(args, w)
         return
