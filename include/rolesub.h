@@ -313,11 +313,11 @@ rolesub_status rolesub_route_allocate(const rolesub_dims* dims, rolesub_dtype dt
  * has R M R^T v = v and is stored in value space: its S consecutive slots
  * hold v itself. Any other token stores its kept groups of z = R^T v in
  * ascending group order. Requirements: bf16; dh = 128; 1 <= S <= 32 with ds a
- * multiple of 32; B, T <= 4096; values, cache and R each below 2 GiB.
- * workspace: at least rolesub_full_workspace_size(B, T) bytes of device
+ * multiple of 128; B <= 1024, T <= 4096; values, cache and R each below 2 GiB.
+ * workspace: at least rolesub_full_workspace_size(B, T, S) bytes of device
  * scratch (per-sample routed-token lists), not kept between calls.
  * ------------------------------------------------------------------------ */
-size_t rolesub_full_workspace_size(int32_t B, int32_t T);
+size_t rolesub_full_workspace_size(int32_t B, int32_t T, int32_t S);
 
 /* Rt[j][k] = R[k][j] for an n x n bf16 matrix (n a multiple of 64): the
  * operand layout rolesub_full_rotate_pack takes. R is frozen per layer, so

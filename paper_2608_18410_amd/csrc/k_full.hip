@@ -20,7 +20,7 @@ namespace {
 
 constexpr int kBM = 128, kBN = 128, kBK = 32;
 constexpr int kLd = kBK + 8;  // LDS row stride (elements): 80 bytes, conflict-free 16-byte fragment reads
-constexpr int kPrepChunks = 4;
+constexpr int kPrepChunks = 16;
 
 __device__ __forceinline__ uint32_t full_bits(int S) { return S >= 32 ? 0xFFFFFFFFu : ((1u << S) - 1u); }
 
@@ -44,6 +44,7 @@ template <bool PACK>
 __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
   __shared__ int s_off[kFullMaxT + 1];
   __shared__ uint16_t s_full[kFullMaxT];
+  __shared__ uint32_t s_mask[PACK ? kFullMaxT : 1];
   __shared__ int wtot[4], wfull[4];
   const int b = blockIdx.x / kPrepChunks, chunk = blockIdx.x % kPrepChunks;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -73,6 +74,7 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
     const int ex_pc = ex & 0xFFFF, ex_rt = ex >> 16;
     const int ex_full = before_full + __popcll(bal & ((1ull << lane) - 1ull));
     if (valid) s_off[t] = run_pc + ex_pc;
+    if (PACK && valid) s_mask[t] = m;
     if (chunk == 0 && routed) p.rlist[static_cast<size_t>(b) * T + run_rt + ex_rt] = t;
     if (isfull) s_full[run_full + ex_full] = static_cast<uint16_t>(t);
     const int tot = wtot[0] + wtot[1] + wtot[2] + wtot[3];
@@ -87,6 +89,30 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
       int32_t* off = p.offsets + static_cast<size_t>(b) * (T + 1);
       for (int t = tid; t < T; t += 256) off[t] = s_off[t];
       if (tid == 0) off[T] = run_pc;
+      // per group: the routed tokens that keep it, in token order
+      int32_t* pr = p.pairs + static_cast<size_t>(b) * T * S;
+      int start = 0;
+      for (int gg = 0; gg < S; ++gg) {
+        int cnt = 0;
+        for (int c0 = 0; c0 < T; c0 += 256) {
+          const int t = c0 + tid;
+          const uint32_t m = t < T ? s_mask[t] : full;
+          const bool keep = m != full && ((m >> gg) & 1u);
+          const uint64_t bal = __ballot(keep);
+          if (lane == 0) wtot[w] = __popcll(bal);
+          __syncthreads();
+          int o = start + cnt + __popcll(bal & ((1ull << lane) - 1ull));
+          for (int v = 0; v < w; ++v) o += wtot[v];
+          if (keep) pr[o] = t;
+          cnt += wtot[0] + wtot[1] + wtot[2] + wtot[3];
+          __syncthreads();
+        }
+        if (tid == 0) {
+          p.counts_g[static_cast<size_t>(b) * S + gg] = cnt;
+          p.starts_g[static_cast<size_t>(b) * S + gg] = start;
+        }
+        start += cnt;
+      }
     }
   }
   // value-space copies of the full tokens: d_v/8 16-byte pieces each, work
@@ -140,13 +166,20 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
 
 // C[m][n] = sum_k A[m][k] * Bt[n][k] on 16x16x32 bf16 MFMA; 128 x 128 tile per
 // workgroup, four waves of 64 x 64, k in steps of 32 through a double-buffered
-// LDS tile (one barrier per step). Rows are the routed tokens of all samples,
-// in sample order; the workgroup maps its rows to (sample, token) through the
-// prefix of the per-sample counts. The 1D grid puts the column tiles
-// n = xcd + 8j on XCD xcd, so each XCD reads a quarter of Bt into its L2.
-//   MODE 0 (rotate): A = v rows, Bt = R^T; kept groups to the cache.
-//   MODE 1 (values): A = the cached groups of z~ (zero where dropped; steps of
-//   groups that no row of the tile keeps are skipped), Bt = R; head-major out.
+// LDS tile (one barrier per step), the operands of the next three steps in
+// flight in registers.
+// About 46 KB of LDS; the four register sets need up to 256 registers: two
+// workgroups per CU.
+//   MODE 0 (rotate): rows are the routed tokens of all samples that keep the
+//   workgroup's group g (per-sample lists from the preparation kernel), so only
+//   kept groups are computed; A = v, Bt = the rows of R^T for group g's output
+//   dims; results to the cache.
+//   MODE 1 (values): rows are the routed tokens of all samples; A = their cached
+//   groups of z~ (zero where dropped; steps of groups that no row of the tile
+//   keeps are skipped), Bt = R; results head-major.
+// Rows map to (sample, token) through the prefix of the per-sample counts.
+// Groups (MODE 0) or column tiles (MODE 1) are pinned to XCDs so that each XCD
+// reads only its share of R into its L2.
 template <int MODE>
 __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
   // A and B tiles (double-buffered) in one region, reused for the output tile
@@ -159,25 +192,43 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
   __shared__ uint32_t s_or;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
   const int B = p.B, T = p.T, dv = p.dv, S = p.S, ds = p.ds;
-  const int ntn = dv / kBN;
-  // column tile on this workgroup's XCD (consecutive ids go round-robin to 8 XCDs)
+  // which tile: (group g, column sub-tile, row tile) or (column tile, row tile)
   const int lin = blockIdx.x;
-  int nt, mt;
-  if ((ntn & 7) == 0) {
-    const int xcd = lin & 7, slot = lin >> 3, per = ntn >> 3;
-    nt = xcd + 8 * (slot % per);
-    mt = slot / per;
+  int g = 0, n0 = 0, mt = 0;
+  if (MODE == 0) {
+    const int nsub = ds / kBN;
+    int rest;
+    if ((S & 7) == 0) {
+      const int xcd = lin & 7, slot = lin >> 3, per = S >> 3;
+      g = xcd + 8 * (slot % per);
+      rest = slot / per;
+    } else {
+      g = lin % S;
+      rest = lin / S;
+    }
+    n0 = g * ds + (rest % nsub) * kBN;
+    mt = rest / nsub;
   } else {
-    nt = lin % ntn;
-    mt = lin / ntn;
+    const int ntn = dv / kBN;
+    int nt;
+    if ((ntn & 7) == 0) {
+      const int xcd = lin & 7, slot = lin >> 3, per = ntn >> 3;
+      nt = xcd + 8 * (slot % per);
+      mt = slot / per;
+    } else {
+      nt = lin % ntn;
+      mt = lin / ntn;
+    }
+    n0 = nt * kBN;
   }
-  const int n0 = nt * kBN, m0 = mt * kBM;
+  const int m0 = mt * kBM;
 
-  // prefix of the routed counts (one wave, 64 samples per step)
+  // prefix over samples of the row counts (one wave, 64 samples per step)
   if (w == 0) {
     int run = 0;
     for (int c0 = 0; c0 < B; c0 += 64) {
-      const int x = c0 + lane < B ? p.counts[c0 + lane] : 0;
+      const int x = c0 + lane < B ? (MODE == 0 ? p.counts_g[static_cast<size_t>(c0 + lane) * S + g]
+                                               : p.counts[c0 + lane]) : 0;
       const int inc = wave_incl_scan(x);
       if (c0 + lane < B) pre[c0 + lane] = run + inc - x;
       run += __shfl(inc, 63, kWave);
@@ -199,7 +250,9 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
         if (pre[mid] <= r) lo = mid; else hi = mid - 1;
       }
       bb = lo;
-      tt = p.rlist[static_cast<size_t>(bb) * T + (r - pre[bb])];
+      const int j = r - pre[bb];
+      tt = MODE == 0 ? p.pairs[static_cast<size_t>(bb) * T * S + p.starts_g[static_cast<size_t>(bb) * S + g] + j]
+                     : p.rlist[static_cast<size_t>(bb) * T + j];
       mm = p.mask[static_cast<size_t>(bb) * T + tt] & full_bits(S);
       oo = p.offsets[static_cast<size_t>(bb) * (T + 1) + tt];
       if (MODE == 1) atomicOr(&s_or, mm);
@@ -225,35 +278,49 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     arow[u] = (tid + 256 * u) >> 2;
     ach[u] = (tid + 256 * u) & 3;
   }
-  auto a_off = [&](int u, int k0) -> uint32_t {
+  // this thread's two A rows, read once: MODE 0 the byte offset of the token's
+  // value row, MODE 1 the byte offset of the sample's cache and the token's
+  // mask and first slot
+  uint32_t a_base[2], a_mask[2];
+  int a_slot0[2];
+  bool a_ok[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
     const int row = arow[u];
     const int bb = r_b[row];
+    a_ok[u] = bb >= 0;
+    a_mask[u] = r_mask[row];
+    a_slot0[u] = r_off[row];
+    a_base[u] = MODE == 0 ? static_cast<uint32_t>(((static_cast<size_t>(bb < 0 ? 0 : bb) * T + r_t[row]) * dv + 8 * ach[u]) * 2)
+                          : static_cast<uint32_t>((static_cast<size_t>(bb < 0 ? 0 : bb) * p.cap * ds + 8 * ach[u]) * 2);
+  }
+  auto a_off = [&](int u, int k0) -> uint32_t {
     if (MODE == 0) {
-      const size_t e = (static_cast<size_t>(bb) * T + r_t[row]) * dv + k0 + 8 * ach[u];
-      return oob_unless(bb >= 0, static_cast<uint32_t>(e * 2));
+      return oob_unless(a_ok[u], a_base[u] + static_cast<uint32_t>(k0) * 2u);
     } else {
       const int g = k0 / ds;
-      const uint32_t mm = r_mask[row];
-      const int slot = r_off[row] + __popc(mm & ((1u << g) - 1u));
-      const bool ok = bb >= 0 && ((mm >> g) & 1u) && slot < p.cap;
-      const size_t e = (static_cast<size_t>(bb) * p.cap + slot) * ds + (k0 - g * ds) + 8 * ach[u];
-      return oob_unless(ok, static_cast<uint32_t>(e * 2));
+      const int slot = a_slot0[u] + __popc(a_mask[u] & ((1u << g) - 1u));
+      const bool ok = a_ok[u] && ((a_mask[u] >> g) & 1u) && slot < p.cap;
+      return oob_unless(ok, a_base[u] + static_cast<uint32_t>((slot * ds + (k0 - g * ds)) * 2));
     }
   };
   auto b_off = [&](int u, int k0) -> uint32_t {
     const size_t e = static_cast<size_t>(n0 + arow[u]) * dv + k0 + 8 * ach[u];
     return static_cast<uint32_t>(e * 2);
   };
-  // k steps: every step of every group in tile_or (MODE 0: all groups)
+  // k steps: every step of every group in tile_or (MODE 0: all groups);
+  // branch-free, and k >= dv stays at dv (loads past the end read zeros)
   auto next_k = [&](int k0) -> int {
     const int k1 = k0 + kBK;
-    if (k1 >= dv) return dv;
-    if (k1 % ds != 0) return k1;
-    const uint32_t rest = tile_or >> (k1 / ds);
-    if (rest == 0) return dv;
-    return k1 + (__builtin_ctz(rest)) * ds;
+    const int gb = k1 / ds;
+    const uint32_t rest = gb < 32 ? (tile_or >> gb) : 0u;
+    const int kg = rest ? (gb + static_cast<int>(__builtin_ctz(rest))) * ds : dv;
+    const int kn = (k1 % ds != 0) ? k1 : kg;
+    return k0 >= dv ? dv : (kn < dv ? kn : dv);
   };
-  int k0 = tile_or == 0 ? dv : __builtin_ctz(tile_or) * ds;
+  const int k_first = tile_or == 0 ? dv : static_cast<int>(__builtin_ctz(tile_or)) * ds;
+  // active steps: a multiple of 4 (ds is a multiple of 128)
+  const int nsteps = MODE == 0 ? dv / kBK : __popc(tile_or) * (ds / kBK);
 
   f32x4 acc[4][4];
 #pragma unroll
@@ -262,50 +329,58 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int wm = w >> 1, wn = w & 1;
-  u32x4 ra[2], rbv[2];
-  if (k0 < dv) {
+  // four register sets: step s's operands arrive in set s % 4, issued three
+  // steps before they are written to LDS
+  u32x4 ra[4][2], rbv[4][2];
+  auto load_set = [&](u32x4 (&a)[2], u32x4 (&bb)[2], int k0) {
+    const bool real = k0 < dv;
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      ra[u] = bload16(r_A, a_off(u, k0));
-      rbv[u] = bload16(r_B, b_off(u, k0));
+      a[u] = bload16(r_A, real ? a_off(u, k0) : kOOB);
+      bb[u] = bload16(r_B, real ? b_off(u, k0) : kOOB);
     }
+  };
+  auto store_set = [&](const u32x4 (&a)[2], const u32x4 (&bb)[2], int buf) {
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      *reinterpret_cast<u32x4*>(&(smem + (0) * kTileA)[arow[u] * kLd + 8 * ach[u]]) = ra[u];
-      *reinterpret_cast<u32x4*>(&(smem + 2 * kTileA + (0) * kTileB)[arow[u] * kLd + 8 * ach[u]]) = rbv[u];
+      *reinterpret_cast<u32x4*>(&(smem + buf * kTileA)[arow[u] * kLd + 8 * ach[u]]) = a[u];
+      *reinterpret_cast<u32x4*>(&(smem + 2 * kTileA + buf * kTileB)[arow[u] * kLd + 8 * ach[u]]) = bb[u];
     }
-  }
-  __syncthreads();
-  int buf = 0;
-  while (k0 < dv) {
-    const int k1 = next_k(k0);
-    if (k1 < dv) {
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        ra[u] = bload16(r_A, a_off(u, k1));
-        rbv[u] = bload16(r_B, b_off(u, k1));
-      }
-    }
+  };
+  auto compute = [&](int buf) {
     bf16x8 af[4], bfr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      af[i] = *reinterpret_cast<const bf16x8*>(&(smem + (buf) * kTileA)[(64 * wm + 16 * i + l16) * kLd + 8 * g4]);
-      bfr[i] = *reinterpret_cast<const bf16x8*>(&(smem + 2 * kTileA + (buf) * kTileB)[(64 * wn + 16 * i + l16) * kLd + 8 * g4]);
+      af[i] = *reinterpret_cast<const bf16x8*>(&(smem + buf * kTileA)[(64 * wm + 16 * i + l16) * kLd + 8 * g4]);
+      bfr[i] = *reinterpret_cast<const bf16x8*>(&(smem + 2 * kTileA + buf * kTileB)[(64 * wn + 16 * i + l16) * kLd + 8 * g4]);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x32(af[i], bfr[j], acc[i][j]);
-    if (k1 < dv) {
+  };
+  // prologue: steps 0..3 issued in the same order the loop keeps
+  int kq = k_first;
+  load_set(ra[0], rbv[0], kq);
+  kq = next_k(kq);
+  load_set(ra[1], rbv[1], kq);
+  kq = next_k(kq);
+  load_set(ra[2], rbv[2], kq);
+  kq = next_k(kq);
+  store_set(ra[0], rbv[0], 0);
+  load_set(ra[3], rbv[3], kq);
+  kq = next_k(kq);
+  __syncthreads();
+  for (int s = 0; s < nsteps; s += 4) {
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        *reinterpret_cast<u32x4*>(&(smem + (buf ^ 1) * kTileA)[arow[u] * kLd + 8 * ach[u]]) = ra[u];
-        *reinterpret_cast<u32x4*>(&(smem + 2 * kTileA + (buf ^ 1) * kTileB)[arow[u] * kLd + 8 * ach[u]]) = rbv[u];
-      }
+    for (int j = 0; j < 4; ++j) {
+      // set j is free (step s+j is in LDS): step s+j+4 into it
+      load_set(ra[j], rbv[j], kq);
+      kq = next_k(kq);
+      compute(j & 1);
+      store_set(ra[(j + 1) & 3], rbv[(j + 1) & 3], (j + 1) & 1);
+      __syncthreads();
     }
-    __syncthreads();
-    buf ^= 1;
-    k0 = k1;
   }
 
   // stage the bf16 tile in LDS (row stride kBN + 8), then 16-byte stores
@@ -328,10 +403,9 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     const u32x4 val = *reinterpret_cast<const u32x4*>(&Cs[row * kCs + 8 * c]);
     const int n = n0 + 8 * c;
     if (MODE == 0) {
-      const int g = n / ds;
       const uint32_t mm = r_mask[row];
       const int slot = r_off[row] + __popc(mm & ((1u << g) - 1u));
-      if (((mm >> g) & 1u) && slot < p.cap) {
+      if (slot < p.cap) {
         bf16* dst = static_cast<bf16*>(p.Vp) + (static_cast<size_t>(bb) * p.cap + slot) * ds + (n - g * ds);
         *reinterpret_cast<u32x4*>(dst) = val;
       }
@@ -358,13 +432,16 @@ __global__ __launch_bounds__(256) void k_transpose_bf16(const bf16* __restrict__
 hipError_t launch_full(const FullParams& p, int mode, hipStream_t s) {
   if (p.B == 0 || p.T == 0) return hipSuccess;
   const dim3 gprep(static_cast<unsigned>(p.B) * kPrepChunks);
-  const unsigned ntn = static_cast<unsigned>(p.dv / kBN);
+  // row tiles: at most every token of every sample is a row (upper bound;
+  // tiles past the actual count return at once)
   const unsigned nmt = static_cast<unsigned>((static_cast<size_t>(p.B) * p.T + kBM - 1) / kBM);
   if (mode == 0) {
     hipLaunchKernelGGL(k_full_prep<true>, gprep, dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_full_gemm<0>, dim3(ntn * nmt), dim3(256), 0, s, p);
+    const unsigned ncol = static_cast<unsigned>(p.S * (p.ds / kBN));
+    hipLaunchKernelGGL(k_full_gemm<0>, dim3(ncol * nmt), dim3(256), 0, s, p);
   } else {
     hipLaunchKernelGGL(k_full_prep<false>, gprep, dim3(256), 0, s, p);
+    const unsigned ntn = static_cast<unsigned>(p.dv / kBN);
     hipLaunchKernelGGL(k_full_gemm<1>, dim3(ntn * nmt), dim3(256), 0, s, p);
   }
   return hipGetLastError();

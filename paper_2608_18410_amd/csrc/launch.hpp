@@ -64,7 +64,7 @@ struct AllocParams {
 hipError_t launch_allocate(const AllocParams& p, hipStream_t s);
 
 // Full-width routing space: one R over d_v = H*dh value dims, S groups of ds.
-constexpr int kFullMaxT = 4096, kFullMaxB = 4096;
+constexpr int kFullMaxT = 4096, kFullMaxB = 1024;
 struct FullParams {
   int B, T, H, dv, S, ds;
   int64_t cap;
@@ -72,6 +72,9 @@ struct FullParams {
   int32_t* offsets;      // [B][T+1]: written by the rotate step, read by the values step
   int32_t* counts;       // [B] routed tokens per sample (workspace)
   int32_t* rlist;        // [B][T] routed token indices (workspace)
+  int32_t* counts_g;     // [B][S] routed tokens keeping group g (workspace)
+  int32_t* starts_g;     // [B][S] start of group g's list in pairs[b] (workspace)
+  int32_t* pairs;        // [B][T*S] per sample: the routed tokens keeping group 0, then 1, ... (workspace)
   const void* v;         // [B][T][dv] (rotate)
   const void* Rm;        // [dv][dv]: R^T (rotate) or R (values)
   void* Vp;              // [B][cap][ds] cache: written (rotate) or read (values)

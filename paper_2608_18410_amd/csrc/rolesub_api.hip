@@ -210,8 +210,8 @@ rolesub_status full_setup(const char* fn, const rolesub_dims* dims, rolesub_dtyp
   if (dims->dh != 128) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: head dim %d not supported (128)", fn, dims->dh);
   const int64_t dv = static_cast<int64_t>(dims->H) * dims->dh;
   const int S = dims->G;
-  if (S < 1 || S > 32 || dv % S != 0 || (dv / S) % 32 != 0)
-    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: S=%d groups of d_v=%lld: need 1 <= S <= 32 and d_v/S a multiple of 32",
+  if (S < 1 || S > 32 || dv % S != 0 || (dv / S) % 128 != 0)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: S=%d groups of d_v=%lld: need 1 <= S <= 32 and d_v/S a multiple of 128",
                 fn, S, static_cast<long long>(dv));
   if (dims->T > kFullMaxT || dims->B > kFullMaxB)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: at most %d prefixes of %d tokens", fn, kFullMaxB, kFullMaxT);
@@ -221,7 +221,7 @@ rolesub_status full_setup(const char* fn, const rolesub_dims* dims, rolesub_dtyp
       static_cast<int64_t>(dims->B) * cap * ds * 2 >= static_cast<int64_t>(kMaxRegion) ||
       dv * dv * 2 >= static_cast<int64_t>(kMaxRegion))
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: values, cache or R exceed 2 GiB", fn);
-  const size_t need = rolesub_full_workspace_size(dims->B, dims->T);
+  const size_t need = rolesub_full_workspace_size(dims->B, dims->T, S);
   if (ws_bytes < need || (need && !workspace))
     return fail(ROLESUB_ERR_INVALID_ARG, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws_bytes);
   p = FullParams{};
@@ -233,8 +233,17 @@ rolesub_status full_setup(const char* fn, const rolesub_dims* dims, rolesub_dtyp
   p.ds = static_cast<int>(ds);
   p.cap = cap;
   char* ws = static_cast<char*>(workspace);
-  p.counts = reinterpret_cast<int32_t*>(ws);
-  p.rlist = reinterpret_cast<int32_t*>(ws + align256(static_cast<size_t>(dims->B) * sizeof(int32_t)));
+  const size_t b = static_cast<size_t>(dims->B);
+  size_t o = 0;
+  p.counts = reinterpret_cast<int32_t*>(ws + o);
+  o += align256(b * sizeof(int32_t));
+  p.rlist = reinterpret_cast<int32_t*>(ws + o);
+  o += align256(b * dims->T * sizeof(int32_t));
+  p.counts_g = reinterpret_cast<int32_t*>(ws + o);
+  o += align256(b * S * sizeof(int32_t));
+  p.starts_g = reinterpret_cast<int32_t*>(ws + o);
+  o += align256(b * S * sizeof(int32_t));
+  p.pairs = reinterpret_cast<int32_t*>(ws + o);
   return ROLESUB_OK;
 }
 
@@ -407,9 +416,11 @@ rolesub_status rolesub_route_allocate(const rolesub_dims* dims, rolesub_dtype dt
 // ---------------------------------------------------------------------------
 // Full-width routing space
 
-size_t rolesub_full_workspace_size(int32_t B, int32_t T) {
-  if (B <= 0 || T <= 0) return 0;
-  return align256(static_cast<size_t>(B) * sizeof(int32_t)) + align256(static_cast<size_t>(B) * T * sizeof(int32_t));
+size_t rolesub_full_workspace_size(int32_t B, int32_t T, int32_t S) {
+  if (B <= 0 || T <= 0 || S <= 0) return 0;
+  const size_t b = static_cast<size_t>(B);
+  return align256(b * sizeof(int32_t)) + align256(b * T * sizeof(int32_t)) + 2 * align256(b * S * sizeof(int32_t)) +
+         align256(b * T * S * sizeof(int32_t));
 }
 
 rolesub_status rolesub_full_transpose(int32_t n, rolesub_dtype dtype, const void* R, void* Rt, void* stream) {

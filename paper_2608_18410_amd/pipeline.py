@@ -90,7 +90,7 @@ class FullWidthBuffers:
             Vp=torch.empty((B, cap, dv // S), dtype=dtype, device=device),
             Vh=torch.empty((B, H, T, dh), dtype=dtype, device=device),
             out=torch.empty((B, Tq, H, dh), dtype=out_dtype or dtype, device=device),
-            workspace=torch.empty(max(rs.full_workspace_size(B, T), 256), dtype=torch.uint8, device=device),
+            workspace=torch.empty(max(rs.full_workspace_size(B, T, S), 256), dtype=torch.uint8, device=device),
             ones=torch.ones((B, T), dtype=torch.int32, device=device),
             arange=torch.arange(T + 1, dtype=torch.int32, device=device).repeat(B, 1).contiguous(),
             eye=torch.eye(dh, dtype=dtype, device=device).repeat(H, 1, 1).contiguous(),

@@ -88,7 +88,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rolesub_allocate_groups.argtypes = [I32, I32, I32, P, P, P, P, P, P, P, P, P]
     lib.rolesub_route_allocate_workspace_size.argtypes = [P, P]
     lib.rolesub_route_allocate.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
-    lib.rolesub_full_workspace_size.argtypes = [I32, I32]
+    lib.rolesub_full_workspace_size.argtypes = [I32, I32, I32]
     lib.rolesub_full_workspace_size.restype = SZ
     lib.rolesub_full_transpose.argtypes = [I32, ctypes.c_int, P, P, P]
     lib.rolesub_full_rotate_pack.argtypes = [P, ctypes.c_int, P, P, P, P, P, I64, P, P, P, SZ, P]
@@ -387,8 +387,8 @@ def route_allocate(token_type, k_by_type, G: int, h, router: Router, w_pri, *, w
 # Full-width routing space (one R over all H*dh value dims, S groups)
 # ----------------------------------------------------------------------------
 
-def full_workspace_size(B, T) -> int:
-    return load().rolesub_full_workspace_size(B, T)
+def full_workspace_size(B, T, S) -> int:
+    return load().rolesub_full_workspace_size(B, T, S)
 
 
 def full_transpose(R, out=None, stream=None):
@@ -410,7 +410,7 @@ def full_rotate_pack(v, Rt, mask, S: int, cap: int, budget: Budget | None = None
                torch.empty((B, cap, dv // S), dtype=v.dtype, device=v.device))
     offsets, Vp = out
     if workspace is None:
-        workspace = torch.empty(max(full_workspace_size(B, T), 1), dtype=torch.uint8, device=v.device)
+        workspace = torch.empty(max(full_workspace_size(B, T, S), 1), dtype=torch.uint8, device=v.device)
     tc = (ctypes.c_int32 * 4)(*[int(x) for x in type_counts]) if type_counts is not None else None
     dims = Dims(B, T, H, dh, S, 0)
     _check("rolesub_full_rotate_pack", load().rolesub_full_rotate_pack(
@@ -427,7 +427,7 @@ def full_values(R, mask, offsets, Vp, S: int, H: int, workspace=None, out=None, 
     dh = ds * S // H
     Vh = torch.empty((B, H, T, dh), dtype=Vp.dtype, device=Vp.device) if out is None else out
     if workspace is None:
-        workspace = torch.empty(max(full_workspace_size(B, T), 1), dtype=torch.uint8, device=Vp.device)
+        workspace = torch.empty(max(full_workspace_size(B, T, S), 1), dtype=torch.uint8, device=Vp.device)
     dims = Dims(B, T, H, dh, S, 0)
     _check("rolesub_full_values", load().rolesub_full_values(
         ctypes.byref(dims), _code(Vp), _ptr(R, Vp.dtype), _ptr(mask), _ptr(offsets, torch.int32), _ptr(Vp),

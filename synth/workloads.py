@@ -122,9 +122,9 @@ WORKLOADS = {
     6: Workload(6, "7b-fullwidth-stack32-b64", B=64, L=32, H=32, dh=128, d=4096, G=16, n_vis=32,
                 n_lang=48, n_prop=1, Tq=56, dtype="bf16", mode=TOPK, k_vis=4, k_lang=16, k_prop=16,
                 C=6, d_e=128, Hr=128, seed=6, full_width=True),
-    # A smaller full-width case for whole-tensor parity: d_v = 1024, S = 16 groups of 64.
-    7: Workload(7, "fullwidth-small", B=3, L=1, H=8, dh=128, d=1024, G=16, n_vis=40, n_lang=20,
-                n_prop=1, Tq=16, dtype="bf16", mode=TOPK, k_vis=2, k_lang=16, k_prop=16, C=6,
+    # A smaller full-width case for whole-tensor parity: d_v = 1024, S = 8 groups of 128.
+    7: Workload(7, "fullwidth-small", B=3, L=1, H=8, dh=128, d=1024, G=8, n_vis=40, n_lang=20,
+                n_prop=1, Tq=16, dtype="bf16", mode=TOPK, k_vis=2, k_lang=8, k_prop=8, C=6,
                 d_e=128, Hr=128, seed=7, full_width=True),
 }
 
