@@ -18,7 +18,7 @@
 namespace rolesub {
 namespace {
 
-constexpr int kBM = 128, kBN = 128, kBK = 32;
+constexpr int kBM0 = 64, kBM1 = 128, kBN = 128, kBK = 32;  // row tiles: rotate, values
 constexpr int kLd = kBK + 8;  // LDS row stride (elements): 80 bytes, conflict-free 16-byte fragment reads
 constexpr int kPrepChunks = 16;
 
@@ -42,10 +42,14 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
 // share the copies; the first one writes the list, count and offsets.
 template <bool PACK>
 __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
-  __shared__ int s_off[kFullMaxT + 1];
-  __shared__ uint16_t s_full[kFullMaxT];
-  __shared__ uint32_t s_mask[PACK ? kFullMaxT : 1];
+  // offsets, the value-space token list and (PACK) the masks of the sample,
+  // sized by T at launch (prep_shm)
+  extern __shared__ __attribute__((aligned(16))) char prep_smem[];
+  int* s_off = reinterpret_cast<int*>(prep_smem);
+  uint32_t* s_mask = reinterpret_cast<uint32_t*>(prep_smem + 4 * (p.T + 1));
+  uint16_t* s_full = reinterpret_cast<uint16_t*>(prep_smem + 4 * (p.T + 1) + (PACK ? 4 * p.T : 0));
   __shared__ int wtot[4], wfull[4];
+  __shared__ int wcnt[4][32];
   const int b = blockIdx.x / kPrepChunks, chunk = blockIdx.x % kPrepChunks;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int T = p.T, S = p.S;
@@ -89,47 +93,72 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
       int32_t* off = p.offsets + static_cast<size_t>(b) * (T + 1);
       for (int t = tid; t < T; t += 256) off[t] = s_off[t];
       if (tid == 0) off[T] = run_pc;
-      // per group: the routed tokens that keep it, in token order
+      // per group: the routed tokens that keep it, in token order. Pass 1
+      // counts every group's tokens (one ballot per group, one barrier per
+      // chunk), pass 2 places them after the earlier groups'.
       int32_t* pr = p.pairs + static_cast<size_t>(b) * T * S;
-      int start = 0;
-      for (int gg = 0; gg < S; ++gg) {
-        int cnt = 0;
+      int run_g[32];
+#pragma unroll
+      for (int gg = 0; gg < 32; ++gg) run_g[gg] = 0;
+      for (int pass = 0; pass < 2; ++pass) {
+        if (pass == 1) {
+          int start = 0;
+#pragma unroll
+          for (int gg = 0; gg < 32; ++gg) {
+            const int n = run_g[gg];
+            if (gg < S && tid == 0) {
+              p.counts_g[static_cast<size_t>(b) * S + gg] = n;
+              p.starts_g[static_cast<size_t>(b) * S + gg] = start;
+            }
+            run_g[gg] = start;
+            start += n;
+          }
+        }
         for (int c0 = 0; c0 < T; c0 += 256) {
           const int t = c0 + tid;
           const uint32_t m = t < T ? s_mask[t] : full;
-          const bool keep = m != full && ((m >> gg) & 1u);
-          const uint64_t bal = __ballot(keep);
-          if (lane == 0) wtot[w] = __popcll(bal);
+          const uint32_t kept = m != full ? m : 0u;
+          uint64_t bal[32];
+#pragma unroll
+          for (int gg = 0; gg < 32; ++gg) {
+            bal[gg] = gg < S ? __ballot((kept >> gg) & 1u) : 0ull;
+            if (lane == 0 && gg < S) wcnt[w][gg] = __popcll(bal[gg]);
+          }
           __syncthreads();
-          int o = start + cnt + __popcll(bal & ((1ull << lane) - 1ull));
-          for (int v = 0; v < w; ++v) o += wtot[v];
-          if (keep) pr[o] = t;
-          cnt += wtot[0] + wtot[1] + wtot[2] + wtot[3];
+#pragma unroll
+          for (int gg = 0; gg < 32; ++gg) {
+            if (gg < S) {
+              if (pass == 1 && ((kept >> gg) & 1u)) {
+                int o = run_g[gg] + __popcll(bal[gg] & ((1ull << lane) - 1ull));
+                for (int v = 0; v < w; ++v) o += wcnt[v][gg];
+                pr[o] = t;
+              }
+              run_g[gg] += wcnt[0][gg] + wcnt[1][gg] + wcnt[2][gg] + wcnt[3][gg];
+            }
+          }
           __syncthreads();
         }
-        if (tid == 0) {
-          p.counts_g[static_cast<size_t>(b) * S + gg] = cnt;
-          p.starts_g[static_cast<size_t>(b) * S + gg] = start;
-        }
-        start += cnt;
       }
     }
   }
   // value-space copies of the full tokens: d_v/8 16-byte pieces each, work
-  // items (token, piece) spread over the chunk's threads, 8 loads in flight
+  // items (token, piece) spread over the chunks' threads, 8 loads in flight.
+  // With PACK the first chunk builds the group lists above and copies nothing.
   const int pieces = p.dv / 8, dh = p.dv / p.H;
+  const int cc = PACK ? chunk - 1 : chunk, ncc = PACK ? kPrepChunks - 1 : kPrepChunks;
+  if (cc < 0) return;
   const int n_items = run_full * pieces;
   const rsrc_t r_cache = make_rsrc(static_cast<const bf16*>(p.Vp) + static_cast<size_t>(b) * p.cap * p.ds,
                                    clamp_bytes(static_cast<size_t>(p.cap) * p.ds * 2));
   const rsrc_t r_v = make_rsrc(static_cast<const bf16*>(p.v) + static_cast<size_t>(b) * T * p.dv,
                                clamp_bytes(static_cast<size_t>(T) * p.dv * 2));
   const int32_t* goff = p.offsets + static_cast<size_t>(b) * (T + 1);
-  for (int i0 = (chunk * 256 + tid); i0 < n_items; i0 += 8 * 256 * kPrepChunks) {
+  for (int i0 = (cc * 256 + tid); i0 < n_items; i0 += 8 * 256 * ncc) {
     u32x4 val[8];
     int tok[8], pc[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * 256 * kPrepChunks;
+      const int i = i0 + u * 256 * ncc;
       const bool ok = i < n_items;
       tok[u] = ok ? s_full[i / pieces] : 0;
       pc[u] = i % pieces;
@@ -147,7 +176,7 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * 256 * kPrepChunks;
+      const int i = i0 + u * 256 * ncc;
       if (i >= n_items) continue;
       if (PACK) {
         const int o = s_off[tok[u]];
@@ -180,15 +209,16 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
 // Rows map to (sample, token) through the prefix of the per-sample counts.
 // Groups (MODE 0) or column tiles (MODE 1) are pinned to XCDs so that each XCD
 // reads only its share of R into its L2.
-template <int MODE>
+template <int MODE, int TBM>
 __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
   // A and B tiles (double-buffered) in one region, reused for the output tile
-  constexpr int kTileA = kBM * kLd, kTileB = kBN * kLd;
+  constexpr int kTileA = TBM * kLd, kTileB = kBN * kLd;
+  constexpr int NA = TBM / 64, MI = TBM / 32;  // A pieces per thread, 16-row blocks per wave
   __shared__ __attribute__((aligned(16))) bf16 smem[2 * kTileA + 2 * kTileB];
   // tile i of A at smem + i * kTileA, of B at smem + 2 * kTileA + i * kTileB
   __shared__ int pre[kFullMaxB + 1];
-  __shared__ int r_b[kBM], r_t[kBM], r_off[kBM];
-  __shared__ uint32_t r_mask[kBM];
+  __shared__ int r_b[TBM], r_t[TBM], r_off[TBM];
+  __shared__ uint32_t r_mask[TBM];
   __shared__ uint32_t s_or;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
   const int B = p.B, T = p.T, dv = p.dv, S = p.S, ds = p.ds;
@@ -221,7 +251,7 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     }
     n0 = nt * kBN;
   }
-  const int m0 = mt * kBM;
+  const int m0 = mt * TBM;
 
   // prefix over samples of the row counts (one wave, 64 samples per step)
   if (w == 0) {
@@ -239,7 +269,7 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
   __syncthreads();
   const int total = pre[B];
   if (m0 >= total) return;  // the same in every thread
-  if (tid < kBM) {
+  if (tid < TBM) {
     const int r = m0 + tid;
     int bb = -1, tt = 0, oo = 0;
     uint32_t mm = 0;
@@ -270,7 +300,7 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
       ? make_rsrc(p.v, clamp_bytes(static_cast<size_t>(B) * T * dv * 2))
       : make_rsrc(p.Vp, clamp_bytes(static_cast<size_t>(B) * p.cap * ds * 2));
   const rsrc_t r_B = make_rsrc(p.Rm, clamp_bytes(static_cast<size_t>(dv) * dv * 2));
-  // this thread's two A pieces and two B pieces per step: piece q = tid + 256 u,
+  // this thread's NA A pieces and two B pieces per step: piece q = tid + 256 u,
   // row q / 4, 16-byte chunk q % 4
   int arow[2], ach[2];
 #pragma unroll
@@ -278,14 +308,14 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     arow[u] = (tid + 256 * u) >> 2;
     ach[u] = (tid + 256 * u) & 3;
   }
-  // this thread's two A rows, read once: MODE 0 the byte offset of the token's
+  // this thread's A rows, read once: MODE 0 the byte offset of the token's
   // value row, MODE 1 the byte offset of the sample's cache and the token's
   // mask and first slot
-  uint32_t a_base[2], a_mask[2];
-  int a_slot0[2];
-  bool a_ok[2];
+  uint32_t a_base[NA], a_mask[NA];
+  int a_slot0[NA];
+  bool a_ok[NA];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
+  for (int u = 0; u < NA; ++u) {
     const int row = arow[u];
     const int bb = r_b[row];
     a_ok[u] = bb >= 0;
@@ -322,40 +352,41 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
   // active steps: a multiple of 4 (ds is a multiple of 128)
   const int nsteps = MODE == 0 ? dv / kBK : __popc(tile_or) * (ds / kBK);
 
-  f32x4 acc[4][4];
+  f32x4 acc[MI][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int wm = w >> 1, wn = w & 1;
   // four register sets: step s's operands arrive in set s % 4, issued three
   // steps before they are written to LDS
-  u32x4 ra[4][2], rbv[4][2];
-  auto load_set = [&](u32x4 (&a)[2], u32x4 (&bb)[2], int k0) {
+  u32x4 ra[4][NA], rbv[4][2];
+  auto load_set = [&](u32x4 (&a)[NA], u32x4 (&bb)[2], int k0) {
     const bool real = k0 < dv;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      a[u] = bload16(r_A, real ? a_off(u, k0) : kOOB);
-      bb[u] = bload16(r_B, real ? b_off(u, k0) : kOOB);
-    }
-  };
-  auto store_set = [&](const u32x4 (&a)[2], const u32x4 (&bb)[2], int buf) {
+    for (int u = 0; u < NA; ++u) a[u] = bload16(r_A, real ? a_off(u, k0) : kOOB);
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < 2; ++u) bb[u] = bload16(r_B, real ? b_off(u, k0) : kOOB);
+  };
+  auto store_set = [&](const u32x4 (&a)[NA], const u32x4 (&bb)[2], int buf) {
+#pragma unroll
+    for (int u = 0; u < NA; ++u)
       *reinterpret_cast<u32x4*>(&(smem + buf * kTileA)[arow[u] * kLd + 8 * ach[u]]) = a[u];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
       *reinterpret_cast<u32x4*>(&(smem + 2 * kTileA + buf * kTileB)[arow[u] * kLd + 8 * ach[u]]) = bb[u];
-    }
   };
   auto compute = [&](int buf) {
-    bf16x8 af[4], bfr[4];
+    bf16x8 af[MI], bfr[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      af[i] = *reinterpret_cast<const bf16x8*>(&(smem + buf * kTileA)[(64 * wm + 16 * i + l16) * kLd + 8 * g4]);
-      bfr[i] = *reinterpret_cast<const bf16x8*>(&(smem + 2 * kTileA + buf * kTileB)[(64 * wn + 16 * i + l16) * kLd + 8 * g4]);
-    }
+    for (int i = 0; i < MI; ++i)
+      af[i] = *reinterpret_cast<const bf16x8*>(&(smem + buf * kTileA)[((TBM / 2) * wm + 16 * i + l16) * kLd + 8 * g4]);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
+      bfr[i] = *reinterpret_cast<const bf16x8*>(&(smem + 2 * kTileA + buf * kTileB)[(64 * wn + 16 * i + l16) * kLd + 8 * g4]);
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x32(af[i], bfr[j], acc[i][j]);
   };
@@ -385,18 +416,18 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
 
   // stage the bf16 tile in LDS (row stride kBN + 8), then 16-byte stores
   constexpr int kCs = kBN + 8;
-  static_assert(kBM * kCs <= 2 * kTileA + 2 * kTileB, "C tile fits the A and B buffers");
+  static_assert(TBM * kCs <= 2 * kTileA + 2 * kTileB, "C tile fits the A and B buffers");
   bf16* Cs = smem;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        Cs[(64 * wm + 16 * i + 4 * g4 + e) * kCs + 64 * wn + 16 * j + l16] = static_cast<bf16>(acc[i][j][e]);
+        Cs[((TBM / 2) * wm + 16 * i + 4 * g4 + e) * kCs + 64 * wn + 16 * j + l16] = static_cast<bf16>(acc[i][j][e]);
   __syncthreads();
 #pragma unroll
-  for (int u = 0; u < kBM * kBN / 8 / 256; ++u) {
+  for (int u = 0; u < TBM * kBN / 8 / 256; ++u) {
     const int q = tid + 256 * u, row = q / (kBN / 8), c = q % (kBN / 8);
     const int bb = r_b[row];
     if (bb < 0) continue;
@@ -432,17 +463,22 @@ __global__ __launch_bounds__(256) void k_transpose_bf16(const bf16* __restrict__
 hipError_t launch_full(const FullParams& p, int mode, hipStream_t s) {
   if (p.B == 0 || p.T == 0) return hipSuccess;
   const dim3 gprep(static_cast<unsigned>(p.B) * kPrepChunks);
+  const size_t shm_pack = 4 * static_cast<size_t>(p.T + 1) + 4 * static_cast<size_t>(p.T) + 2 * static_cast<size_t>(p.T);
+  const size_t shm_vals = 4 * static_cast<size_t>(p.T + 1) + 2 * static_cast<size_t>(p.T);
   // row tiles: at most every token of every sample is a row (upper bound;
-  // tiles past the actual count return at once)
-  const unsigned nmt = static_cast<unsigned>((static_cast<size_t>(p.B) * p.T + kBM - 1) / kBM);
+  // tiles past the actual count return at once). The rotation has fewer rows
+  // per group than the values step has in all, so it takes 64-row tiles.
+  const size_t rows = static_cast<size_t>(p.B) * p.T;
   if (mode == 0) {
-    hipLaunchKernelGGL(k_full_prep<true>, gprep, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_full_prep<true>, gprep, dim3(256), shm_pack, s, p);
     const unsigned ncol = static_cast<unsigned>(p.S * (p.ds / kBN));
-    hipLaunchKernelGGL(k_full_gemm<0>, dim3(ncol * nmt), dim3(256), 0, s, p);
+    const unsigned nmt = static_cast<unsigned>((rows + kBM0 - 1) / kBM0);
+    hipLaunchKernelGGL((k_full_gemm<0, kBM0>), dim3(ncol * nmt), dim3(256), 0, s, p);
   } else {
-    hipLaunchKernelGGL(k_full_prep<false>, gprep, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_full_prep<false>, gprep, dim3(256), shm_vals, s, p);
     const unsigned ntn = static_cast<unsigned>(p.dv / kBN);
-    hipLaunchKernelGGL(k_full_gemm<1>, dim3(ntn * nmt), dim3(256), 0, s, p);
+    const unsigned nmt = static_cast<unsigned>((rows + kBM1 - 1) / kBM1);
+    hipLaunchKernelGGL((k_full_gemm<1, kBM1>), dim3(ntn * nmt), dim3(256), 0, s, p);
   }
   return hipGetLastError();
 }
