@@ -122,3 +122,82 @@ def test_attend_validation(lib):
     nan_args = args[:7] + (ctypes.c_float(float("nan")),) + args[8:]
     assert lib.rolesub_attend(ctypes.byref(d), rs.BF16, 4, *nan_args, rs.F32, None, 0, None) == 1
     assert lib.rolesub_attend_workspace_size(ctypes.byref(d), 4) == 0
+
+
+def _i32x(*vals):
+    return (ctypes.c_int32 * len(vals))(*vals)
+
+
+def test_retain_and_gather_validation(lib):
+    ok_len, ok_keep = _i32x(256, 256), _i32x(64, 64)
+    assert lib.rolesub_retain_tokens(2, 512, 0, ok_len, ok_keep, FAKE, FAKE, None) == 2
+    assert lib.rolesub_retain_tokens(2, 512, 17, ok_len, ok_keep, FAKE, FAKE, None) == 2
+    assert lib.rolesub_retain_tokens(2, 500, 2, ok_len, ok_keep, FAKE, FAKE, None) == 1
+    assert "sum to 512" in _last()
+    assert lib.rolesub_retain_tokens(2, 512, 2, ok_len, _i32x(64, 300), FAKE, FAKE, None) == 1
+    assert lib.rolesub_retain_tokens(1, 9000, 1, _i32x(9000), _i32x(5), FAKE, FAKE, None) == 2
+    assert lib.rolesub_retain_tokens(2, 512, 2, ok_len, ok_keep, None, FAKE, None) == 1
+    assert lib.rolesub_retain_tokens(0, 512, 2, ok_len, ok_keep, None, None, None) == 0   # no samples: no-op
+    assert lib.rolesub_gather_tokens(2, 9, 4, 6, FAKE, FAKE, FAKE, None) == 2            # row bytes % 4
+    assert lib.rolesub_gather_tokens(2, 9, 4, 16, None, FAKE, FAKE, None) == 1
+    assert lib.rolesub_gather_tokens(2, 9, 0, 16, None, None, None, None) == 0
+
+
+def test_allocate_validation(lib):
+    kby = _i32x(4, 6, 8, 8)
+    assert lib.rolesub_allocate_groups(1, 4097, 8, kby, FAKE, FAKE, None, FAKE, None, None, None, None) == 2
+    assert "4096" in _last()
+    assert lib.rolesub_allocate_groups(1, 8, 8, _i32x(9, 1, 1, 1), FAKE, FAKE, None, FAKE, None, None, None,
+                                       None) == 1
+    assert lib.rolesub_allocate_groups(1, 8, 33, kby, FAKE, FAKE, None, FAKE, None, None, None, None) == 2
+    assert lib.rolesub_allocate_groups(1, 8, 8, None, FAKE, FAKE, None, FAKE, None, None, None, None) == 1
+    assert lib.rolesub_allocate_groups(1, 8, 8, kby, FAKE, FAKE, None, FAKE, FAKE, None, None, None) == 1
+    assert "without scores" in _last()
+    assert lib.rolesub_allocate_groups(1, 8, 8, kby, FAKE, FAKE, FAKE, FAKE, None, None, None, None) == 1
+    assert lib.rolesub_allocate_groups(1, 8, 8, kby, FAKE, FAKE, None, None, None, None, None, None) == 1
+    assert lib.rolesub_allocate_groups(1, 8, 8, kby, None, FAKE, None, FAKE, None, None, None, None) == 1
+    assert lib.rolesub_allocate_groups(0, 8, 8, kby, None, None, None, None, None, None, None, None) == 0
+    # routing with allocation: router, priority weights and workspace are required
+    d = _dims(G=8, d=64)
+    desc = rs.RouterDesc()
+    desc.kind, desc.C, desc.d_e, desc.Hr = rs.MLP2, 4, 8, 16
+    for n in ("W_r", "b_r", "E", "W1", "b1", "W2", "b2"):
+        setattr(desc, n, 0x1000)
+    need = lib.rolesub_route_allocate_workspace_size(ctypes.byref(d), ctypes.byref(desc))
+    assert need >= lib.rolesub_route_workspace_size(ctypes.byref(d), ctypes.byref(desc))
+    args = (FAKE, FAKE, None, None, None, FAKE, None, None)
+    assert lib.rolesub_route_allocate(ctypes.byref(d), rs.BF16, ctypes.byref(desc), None, kby, *args,
+                                      FAKE, need, None) == 1
+    assert "w_pri" in _last()
+    assert lib.rolesub_route_allocate(ctypes.byref(d), rs.BF16, ctypes.byref(desc), FAKE, kby, *args,
+                                      FAKE, need - 1, None) == 1
+    assert "workspace" in _last()
+    assert lib.rolesub_route_allocate(ctypes.byref(d), rs.BF16, None, FAKE, kby, *args, FAKE, need, None) == 1
+
+
+def test_full_width_validation(lib):
+    ws = lib.rolesub_full_workspace_size(2, 81, 16)
+    assert ws > 2 * 81 * 16 * 4
+    d = rs.Dims(2, 81, 32, 128, 16, 0)
+    rp = lambda dims, dt=rs.BF16, cap=2 * 81 * 16, ws_bytes=ws, budget=None, tc=None: lib.rolesub_full_rotate_pack(
+        ctypes.byref(dims), dt, FAKE, FAKE, FAKE, FAKE, ctypes.c_void_p(0x10000000), cap, budget, tc, FAKE,
+        ws_bytes, None)
+    assert rp(d, dt=rs.F32) == 2
+    assert rp(rs.Dims(2, 81, 64, 64, 16, 0)) == 2                    # head dim 64
+    assert rp(rs.Dims(2, 81, 8, 128, 16, 0)) == 2                    # groups of 64 dims
+    assert "multiple of 128" in _last()
+    assert rp(rs.Dims(1025, 81, 32, 128, 16, 0)) == 2                # batch limit
+    assert rp(d, ws_bytes=ws - 1) == 1
+    assert rp(d, cap=-1) == 1
+    bu = rs.make_budget(rs.TOPK, (4, 16, 16, 16))
+    assert rp(d, cap=32 * 4 + 48 * 16, budget=ctypes.byref(bu), tc=_i32x(32, 48, 1, 0)) == 3   # 1 proprio short
+    assert rp(rs.Dims(0, 81, 32, 128, 16, 0), ws_bytes=0) == 0
+    # values: the head-major output may not overlap the cache
+    assert lib.rolesub_full_values(ctypes.byref(d), rs.BF16, FAKE, FAKE, FAKE, FAKE, 2 * 81 * 16, FAKE, FAKE, ws,
+                                   None) == 1
+    assert "overlaps" in _last()
+    assert lib.rolesub_full_values(ctypes.byref(d), rs.BF16, None, FAKE, FAKE, FAKE, 10, FAKE, FAKE, ws, None) == 1
+    assert lib.rolesub_full_transpose(100, rs.BF16, FAKE, FAKE, None) == 2
+    assert lib.rolesub_full_transpose(128, rs.BF16, FAKE, FAKE, None) == 1
+    assert lib.rolesub_full_transpose(128, rs.F32, FAKE, ctypes.c_void_p(0x10000000), None) == 2
+    assert lib.rolesub_full_transpose(0, rs.BF16, None, None, None) == 0
