@@ -39,7 +39,8 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
 // (PACK), and the value-space copies of the tokens that keep every group:
 // into the cache (PACK: v -> Vp) or from it into the head-major values
 // (!PACK: Vp -> Vh, at the given offsets). kPrepChunks workgroups per sample
-// share the copies; the first one writes the list, count and offsets.
+// share the copies; the first one writes the list, count and offsets, and
+// (PACK) the per-group lists instead of copying.
 template <bool PACK>
 __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
   // offsets, the value-space token list and (PACK) the masks of the sample,
@@ -93,9 +94,9 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
       int32_t* off = p.offsets + static_cast<size_t>(b) * (T + 1);
       for (int t = tid; t < T; t += 256) off[t] = s_off[t];
       if (tid == 0) off[T] = run_pc;
-      // per group: the routed tokens that keep it, in token order. Pass 1
-      // counts every group's tokens (one ballot per group, one barrier per
-      // chunk), pass 2 places them after the earlier groups'.
+      // per group: the routed tokens that keep it, in token order. The first
+      // pass counts every group's tokens (one ballot per group, one barrier
+      // per chunk), the second places them after the earlier groups'.
       int32_t* pr = p.pairs + static_cast<size_t>(b) * T * S;
       int run_g[32];
 #pragma unroll
@@ -197,8 +198,8 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
 // workgroup, four waves of 64 x 64, k in steps of 32 through a double-buffered
 // LDS tile (one barrier per step), the operands of the next three steps in
 // flight in registers.
-// About 46 KB of LDS; the four register sets need up to 256 registers: two
-// workgroups per CU.
+// 128-row tiles: about 46 KB of LDS and up to 256 registers (the four
+// register sets), two workgroups per CU; 64-row tiles: 35 KB, four per CU.
 //   MODE 0 (rotate): rows are the routed tokens of all samples that keep the
 //   workgroup's group g (per-sample lists from the preparation kernel), so only
 //   kept groups are computed; A = v, Bt = the rows of R^T for group g's output
@@ -209,7 +210,7 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
 // Rows map to (sample, token) through the prefix of the per-sample counts.
 // Groups (MODE 0) or column tiles (MODE 1) are pinned to XCDs so that each XCD
 // reads only its share of R into its L2.
-template <int MODE, int TBM>
+template <int MODE, int TBM, int NS>
 __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
   // A and B tiles (double-buffered) in one region, reused for the output tile
   constexpr int kTileA = TBM * kLd, kTileB = kBN * kLd;
@@ -349,7 +350,9 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     return k0 >= dv ? dv : (kn < dv ? kn : dv);
   };
   const int k_first = tile_or == 0 ? dv : static_cast<int>(__builtin_ctz(tile_or)) * ds;
-  // active steps: a multiple of 4 (ds is a multiple of 128)
+  // active steps: a multiple of NS = 4 (ds is a multiple of 128: at least 4
+  // steps per group). Eight sets for the rotation were measured slower (two
+  // workgroups per CU instead of four).
   const int nsteps = MODE == 0 ? dv / kBK : __popc(tile_or) * (ds / kBK);
 
   f32x4 acc[MI][4];
@@ -359,15 +362,28 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int wm = w >> 1, wn = w & 1;
-  // four register sets: step s's operands arrive in set s % 4, issued three
+  // NS register sets: step s's operands arrive in set s % NS, issued NS - 1
   // steps before they are written to LDS
-  u32x4 ra[4][NA], rbv[4][2];
+  u32x4 ra[NS][NA], rbv[NS][2];
+  // MODE 1 computes the offsets unconditionally: with a branch around its
+  // (longer) address computation the compiler reuses an in-flight load's
+  // registers and waits for every load (values 117.6 -> 110.4 us). The
+  // rotation's short computation is faster with the select (71.7 vs 82.2 us;
+  // both measured in one process).
   auto load_set = [&](u32x4 (&a)[NA], u32x4 (&bb)[2], int k0) {
     const bool real = k0 < dv;
+    if constexpr (MODE == 1) {
+      const int kk = real ? k0 : 0;
 #pragma unroll
-    for (int u = 0; u < NA; ++u) a[u] = bload16(r_A, real ? a_off(u, k0) : kOOB);
+      for (int u = 0; u < NA; ++u) a[u] = bload16(r_A, oob_unless(real, a_off(u, kk)));
 #pragma unroll
-    for (int u = 0; u < 2; ++u) bb[u] = bload16(r_B, real ? b_off(u, k0) : kOOB);
+      for (int u = 0; u < 2; ++u) bb[u] = bload16(r_B, oob_unless(real, b_off(u, kk)));
+    } else {
+#pragma unroll
+      for (int u = 0; u < NA; ++u) a[u] = bload16(r_A, real ? a_off(u, k0) : kOOB);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) bb[u] = bload16(r_B, real ? b_off(u, k0) : kOOB);
+    }
   };
   auto store_set = [&](const u32x4 (&a)[NA], const u32x4 (&bb)[2], int buf) {
 #pragma unroll
@@ -390,26 +406,25 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x32(af[i], bfr[j], acc[i][j]);
   };
-  // prologue: steps 0..3 issued in the same order the loop keeps
+  // prologue: steps 0..NS-1 issued in the same order the loop keeps
   int kq = k_first;
-  load_set(ra[0], rbv[0], kq);
-  kq = next_k(kq);
-  load_set(ra[1], rbv[1], kq);
-  kq = next_k(kq);
-  load_set(ra[2], rbv[2], kq);
-  kq = next_k(kq);
+#pragma unroll
+  for (int j = 0; j < NS - 1; ++j) {
+    load_set(ra[j], rbv[j], kq);
+    kq = next_k(kq);
+  }
   store_set(ra[0], rbv[0], 0);
-  load_set(ra[3], rbv[3], kq);
+  load_set(ra[NS - 1], rbv[NS - 1], kq);
   kq = next_k(kq);
   __syncthreads();
-  for (int s = 0; s < nsteps; s += 4) {
+  for (int s = 0; s < nsteps; s += NS) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      // set j is free (step s+j is in LDS): step s+j+4 into it
+    for (int j = 0; j < NS; ++j) {
+      // set j is free (step s+j is in LDS): step s+j+NS into it
       load_set(ra[j], rbv[j], kq);
       kq = next_k(kq);
       compute(j & 1);
-      store_set(ra[(j + 1) & 3], rbv[(j + 1) & 3], (j + 1) & 1);
+      store_set(ra[(j + 1) % NS], rbv[(j + 1) % NS], (j + 1) & 1);
       __syncthreads();
     }
   }
@@ -473,12 +488,12 @@ hipError_t launch_full(const FullParams& p, int mode, hipStream_t s) {
     hipLaunchKernelGGL(k_full_prep<true>, gprep, dim3(256), shm_pack, s, p);
     const unsigned ncol = static_cast<unsigned>(p.S * (p.ds / kBN));
     const unsigned nmt = static_cast<unsigned>((rows + kBM0 - 1) / kBM0);
-    hipLaunchKernelGGL((k_full_gemm<0, kBM0>), dim3(ncol * nmt), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((k_full_gemm<0, kBM0, 4>), dim3(ncol * nmt), dim3(256), 0, s, p);
   } else {
     hipLaunchKernelGGL(k_full_prep<false>, gprep, dim3(256), shm_vals, s, p);
     const unsigned ntn = static_cast<unsigned>(p.dv / kBN);
     const unsigned nmt = static_cast<unsigned>((rows + kBM1 - 1) / kBM1);
-    hipLaunchKernelGGL((k_full_gemm<1, kBM1>), dim3(ntn * nmt), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((k_full_gemm<1, kBM1, 4>), dim3(ntn * nmt), dim3(256), 0, s, p);
   }
   return hipGetLastError();
 }
