@@ -819,3 +819,49 @@ def test_full_width_stack_shape_sampled():
         err = max_rel(got[b:b + 1], want)
         _say(f"full-width stack prefix {b}: max rel err {err:.2e}")
         assert err <= TOL["bf16"]
+
+
+def test_full_width_with_role_driven_budgets_and_repeatable():
+    """Role-driven budgets (Sec. 3.5) feeding the full-width path at the
+    paper's router shape (C = 6, S = 16): masks from rolesub_route_allocate,
+    cache and attention against the oracle on those masks, and bitwise equal
+    results on a second run of every call."""
+    from paper_2608_18410_amd.pipeline import FullWidthBuffers, run_full_layer
+    w = synth.workload(6).replace(B=4, k_vis=4, k_lang=8)      # language routed too
+    B, S = w.B, w.G
+    wt = synth.layer_weights(w, 0)
+    wpri = synth.priority_weights(w, 0)
+    h = np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(B)])
+    types = stack_types(w, B)
+    r = rs.route_allocate(put_u8(types), w.k_by_type, S, put(h, torch.bfloat16), router_tensors(wt, torch.bfloat16),
+                          put(wpri, torch.bfloat16))
+    torch.cuda.synchronize()
+    mask = host_mask(r["mask"])
+    k = host(r["k"]).astype(np.int64)
+    for b in range(B):
+        for m in range(3):
+            sel = types[b] == m
+            assert k[b][sel].sum() == min(w.k_by_type[m], S) * sel.sum()
+    assert len(np.unique(k[0][types[0] == O.VIS])) > 1          # budgets vary by token
+    rng = np.random.default_rng(90)
+    R = synth.full_rotation(w, 0)["R"]
+    q = synth.round_to(rng.standard_normal((B, w.Tq, w.H, w.dh)), "bf16")
+    kk = synth.round_to(rng.standard_normal((B, w.T, w.H, w.dh)), "bf16")
+    v = synth.round_to(rng.standard_normal((B, w.T, w.H, w.dh)), "bf16")
+    cap = sum(n * min(x, S) for n, x in zip(w.type_counts(), w.k_by_type))
+    bufs = FullWidthBuffers.allocate(B, w.T, w.H, w.dh, S, w.Tq, cap, torch.bfloat16, device=DEV)
+    Rd = _dev_bf16(R)
+    Rt = rs.full_transpose(Rd)
+    args = (_dev_bf16(q), _dev_bf16(kk), _dev_bf16(v), put_mask(mask), Rt, Rd, S, bufs)
+    run_full_layer(*args, budget=rs.make_budget(rs.TOPK, w.k_by_type), type_counts=w.type_counts())
+    torch.cuda.synchronize()
+    first = [t.clone() for t in (bufs.offsets, bufs.Vp, bufs.Vh, bufs.out)]
+    want = O.attend_full_plain(q, kk, v, mask, R, S)
+    err = max_rel(host(bufs.out), want)
+    _say(f"full width with role-driven budgets: max rel err {err:.2e}")
+    assert err <= TOL["bf16"]
+    for _ in range(3):
+        run_full_layer(*args)
+    torch.cuda.synchronize()
+    for a, b_ in zip(first, (bufs.offsets, bufs.Vp, bufs.Vh, bufs.out)):
+        assert torch.equal(a, b_)
