@@ -240,7 +240,7 @@ def full_width(args, w):
 
     def att(L):
         fb, a = L["fb"], L["acts"]
-        rs.attend(a["q"], a["k"], fb.ones, fb.arange, fb.Vh, fb.eye, 1, out=fb.out)
+        rs.attend_values(a["q"], a["k"], fb.Vh, out=fb.out)
 
     for L in layers:
         layer(L)

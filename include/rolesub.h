@@ -251,6 +251,19 @@ rolesub_status rolesub_gather_tokens(int32_t B, int32_t N, int32_t K, int64_t ro
                                      const void* src, void* dst, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * rolesub_attend_values: attention with unchanged queries and keys (Sec. 3)
+ * over plain per-head values, for the full-width routing space whose routed
+ * values rolesub_full_values rebuilds:
+ *   out[b,q,h,:] = sum_t softmax_t(scale * q[b,q,h,:] . k[b,t,h,:]) V[b,h,t,:]
+ * q [B,Tq,H,dh], k [B,T,H,dh], V [B,H,T,dh] (head-major), out [B,Tq,H,dh];
+ * bf16 inputs, dh 64 or 128, out_dtype f32 or bf16; scale 0 means 1/sqrt(dh).
+ * dims->G and dims->d are not used. B = 0 or Tq = 0 does nothing.
+ * ------------------------------------------------------------------------ */
+rolesub_status rolesub_attend_values(const rolesub_dims* dims, rolesub_dtype dtype, int32_t Tq, const void* q,
+                                     const void* k, const void* V, float scale, void* out, rolesub_dtype out_dtype,
+                                     void* stream);
+
+/* ---------------------------------------------------------------------------
  * rolesub_allocate_groups: role-driven within-type budget allocation
  * (Sec. 3.5, the allocator B), optionally followed by the Top-K_i group
  * selection (Sec. 3.4) with the allocated budgets.
@@ -343,9 +356,8 @@ rolesub_status rolesub_full_rotate_pack(const rolesub_dims* dims, rolesub_dtype 
  *   are zero, so a token keeping none gets 0), and v_t's slice for tokens
  *   stored in value space.
  *   R [d_v, d_v]; mask, offsets, Vp as written by rolesub_full_rotate_pack;
- *   Vh [B,H,T,dh] written. rolesub_attend with G = 1, mask bit 0 set,
- *   offsets[b,t] = t, Vp = Vh (cap_groups = T) and identity rotations then
- *   gives the paper's attention over these values. */
+ *   Vh [B,H,T,dh] written; rolesub_attend_values then gives the paper's
+ *   attention over these values. */
 rolesub_status rolesub_full_values(const rolesub_dims* dims, rolesub_dtype dtype, const void* R,
                                    const uint32_t* mask, const int32_t* offsets, const void* Vp, int64_t cap_groups,
                                    void* Vh, void* workspace, size_t ws_bytes, void* stream);

@@ -55,7 +55,10 @@ __device__ __forceinline__ void sched_reads_ahead() {
 // VM: how the 8-dim chunks of the value tile map to packed groups:
 //   kWide  groups of >= 8 dims (one 16-byte load per token and chunk)
 //   kDs4   4-dim groups (two 8-byte loads), kDs2  2-dim groups (four 4-byte loads)
-constexpr int kWide = 0, kDs4 = 1, kDs2 = 2;
+//   kDense plain per-head values [B][H][T][dh] (the full-width routing space
+//          rebuilds them): token t is slot t, no masks, offsets or R_h, and
+//          the output is the normalised accumulator itself
+constexpr int kWide = 0, kDs4 = 1, kDs2 = 2, kDense = 3;
 
 // Three waves per SIMD (three workgroups per CU): the register budget is
 // capped at 168 so that occupancy, not just the pipeline, hides latency.
@@ -101,8 +104,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     }
     xcd_split(item, p.H, h, b);
   }
+  constexpr bool DENSE = VM == kDense;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
-  const int T = p.T, H = p.H, G = p.G, ds = DH / G;
+  const int T = p.T, H = p.H, G = DENSE ? 1 : p.G, ds = DH / G;
   const uint32_t gm = group_mask(G);
   const int qq = qb * 64 + 16 * w + l16;
   const int q_first = qb * 64 + 16 * __builtin_amdgcn_readfirstlane(w);  // this wave's first query
@@ -110,7 +114,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
 
   // R_h: wave w brings 1 KB blocks w*NRD .. w*NRD+NRD-1; lane i of a block
   // lands at byte 16i, which holds global chunk (16i % RBY)/16 ^ (row % RCH)
-  {
+  if constexpr (!DENSE) {
     constexpr int NRD = RB / 1024 / 4;
     const rsrc_t r_R = make_rsrc(static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH, RB);
     const uint32_t rbase = lds_addr(Rs);
@@ -154,8 +158,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   auto load_meta = [&](int t0, uint32_t& m, int32_t& o) {
     const int t = t0 + tid;
     const bool ok = tid < TK && t < T;
-    m = bload4(r_mask, oob_unless(ok, 4u * t));  // masked to G bits when stored (no wait here)
-    o = static_cast<int32_t>(bload4(r_off, oob_unless(ok, 4u * t)));
+    if constexpr (DENSE) {
+      m = ok ? 1u : 0u;
+      o = t;
+    } else {
+      m = bload4(r_mask, oob_unless(ok, 4u * t));  // masked to G bits when stored (no wait here)
+      o = static_cast<int32_t>(bload4(r_off, oob_unless(ok, 4u * t)));
+    }
   };
   // two register sets (A, B) for tile operands in flight
   u32x4 kA[NKP], kB[NKP];
@@ -190,7 +199,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
         const bool tok_ok = t0 + tl < T;
         const uint32_t m = s_mask[slot][tl];
         const int o = s_off[slot][tl];
-        if constexpr (VM == kWide) {
+        if constexpr (VM == kWide || DENSE) {
           const int g = (8 * cc) / ds;
           vreg[r][e] = bload16(r_v, slot_off(m, o, g, tok_ok, 8 * cc - g * ds));
         } else if constexpr (VM == kDs4) {
@@ -386,6 +395,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     o[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (DENSE) {
+      // no rotation: the normalised accumulator, which holds dims
+      // 16m + 4 g4 + i like the rotated result (the P.V order pairs acc[2ks]
+      // with dims 32ks + 4 g4.. and acc[2ks+1] with 32ks + 16 + 4 g4..)
+      o[m] = acc[m] * inv;
+      continue;
+    }
     // row 16m + l16, elements 32ks + 4g4 .. +3 and 32ks + 16 + 4g4 .. +3:
     // byte 8*(g4 & 1) of chunks 4ks + g4/2 and 4ks + 2 + g4/2
     const int row = 16 * m + l16;
@@ -505,10 +521,11 @@ hipError_t launch_attend(const AttendParams& p, bool bf16, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(p.B * p.H * ((p.Tq + 63) / 64)));
     const int ds = p.dh / p.G;
     const int vm = ds >= 8 ? kWide : (ds == 4 ? kDs4 : kDs2);
-    auto k = p.dh == 128 ? (vm == kWide ? k_attend_bf16<128, kWide> : vm == kDs4 ? k_attend_bf16<128, kDs4>
-                                                                                : k_attend_bf16<128, kDs2>)
-                         : (vm == kWide ? k_attend_bf16<64, kWide> : vm == kDs4 ? k_attend_bf16<64, kDs4>
-                                                                               : k_attend_bf16<64, kDs2>);
+    auto k = p.dense ? (p.dh == 128 ? k_attend_bf16<128, kDense> : k_attend_bf16<64, kDense>)
+             : p.dh == 128 ? (vm == kWide ? k_attend_bf16<128, kWide> : vm == kDs4 ? k_attend_bf16<128, kDs4>
+                                                                                  : k_attend_bf16<128, kDs2>)
+                           : (vm == kWide ? k_attend_bf16<64, kWide> : vm == kDs4 ? k_attend_bf16<64, kDs4>
+                                                                                 : k_attend_bf16<64, kDs2>);
     hipLaunchKernelGGL(k, grid, dim3(256), 0, s, p);
   } else {
     const dim3 grid(static_cast<unsigned>(static_cast<size_t>(p.B) * p.H * p.Tq));

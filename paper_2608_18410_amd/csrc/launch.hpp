@@ -119,6 +119,7 @@ struct AttendParams {
   void* out;
   int out_f32;
   int causal;  // prefix self-attention: Tq == T and query t sees keys 0..t
+  int dense;   // plain per-head values Vp = [B][H][T][dh]: no masks, offsets or rotation
 };
 hipError_t launch_attend(const AttendParams& p, bool bf16, hipStream_t s);
 

@@ -541,7 +541,8 @@ size_t rolesub_attend_workspace_size(const rolesub_dims* dims, int32_t Tq) {
   return 0;
 }
 
-static rolesub_status attend_call(const char* fn, bool causal, const rolesub_dims* dims, rolesub_dtype dtype,
+static rolesub_status attend_call(const char* fn, bool causal, bool dense, const rolesub_dims* dims,
+                                  rolesub_dtype dtype,
                                   int32_t Tq, const void* q, const void* k, const uint32_t* mask,
                                   const int32_t* offsets, const void* Vp, int64_t cap_groups, const void* R,
                                   float scale, void* out, rolesub_dtype out_dtype, void* workspace,
@@ -550,16 +551,19 @@ static rolesub_status attend_call(const char* fn, bool causal, const rolesub_dim
   (void)ws_bytes;
   rolesub_status st = check_value_dims(dims, fn);
   if (st) return st;
-  st = check_groups(dims, fn, true);
-  if (st) return st;
+  if (!dense) {
+    st = check_groups(dims, fn, true);
+    if (st) return st;
+  }
   if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+  if (dense && dtype != ROLESUB_BF16) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: bf16 only", fn);
   if (out_dtype != ROLESUB_F32 && out_dtype != dtype)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: out_dtype must be f32 or the input dtype", fn);
   if (Tq < 0 || cap_groups < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: Tq and cap_groups must be >= 0", fn);
   if (!std::isfinite(scale)) return fail(ROLESUB_ERR_INVALID_ARG, "%s: scale is not finite", fn);
   if (dims->B == 0 || Tq == 0) return ROLESUB_OK;
   if (dims->T < 1) return fail(ROLESUB_ERR_INVALID_ARG, "%s: attention over T=0 tokens is undefined", fn);
-  if (!q || !k || !mask || !offsets || !R || !out || (cap_groups > 0 && !Vp))
+  if (!q || !k || !out || (cap_groups > 0 && !Vp) || (!dense && (!mask || !offsets || !R)))
     return fail(ROLESUB_ERR_INVALID_ARG, "%s: a tensor pointer is NULL", fn);
   if (static_cast<size_t>(dims->B) * dims->H > 0x7FFFFFFF ||
       static_cast<size_t>(dims->B) * dims->H * Tq > 0x7FFFFFFF)
@@ -573,7 +577,7 @@ static rolesub_status attend_call(const char* fn, bool causal, const rolesub_dim
   p.T = dims->T;
   p.H = dims->H;
   p.dh = dims->dh;
-  p.G = dims->G;
+  p.G = dense ? 1 : dims->G;
   p.Tq = Tq;
   p.q = q;
   p.k = k;
@@ -586,6 +590,7 @@ static rolesub_status attend_call(const char* fn, bool causal, const rolesub_dim
   p.out = out;
   p.out_f32 = out_dtype == ROLESUB_F32;
   p.causal = causal ? 1 : 0;
+  p.dense = dense ? 1 : 0;
   return from_hip(launch_attend(p, dtype == ROLESUB_BF16, static_cast<hipStream_t>(stream)), fn);
 }
 
@@ -593,8 +598,16 @@ rolesub_status rolesub_attend(const rolesub_dims* dims, rolesub_dtype dtype, int
                               const void* k, const uint32_t* mask, const int32_t* offsets, const void* Vp,
                               int64_t cap_groups, const void* R, float scale, void* out,
                               rolesub_dtype out_dtype, void* workspace, size_t ws_bytes, void* stream) {
-  return attend_call("rolesub_attend", false, dims, dtype, Tq, q, k, mask, offsets, Vp, cap_groups, R, scale, out,
+  return attend_call("rolesub_attend", false, false, dims, dtype, Tq, q, k, mask, offsets, Vp, cap_groups, R, scale, out,
                      out_dtype, workspace, ws_bytes, stream);
+}
+
+rolesub_status rolesub_attend_values(const rolesub_dims* dims, rolesub_dtype dtype, int32_t Tq, const void* q,
+                                     const void* k, const void* V, float scale, void* out, rolesub_dtype out_dtype,
+                                     void* stream) {
+  if (!dims) return fail(ROLESUB_ERR_INVALID_ARG, "rolesub_attend_values: dims is NULL");
+  return attend_call("rolesub_attend_values", false, true, dims, dtype, Tq, q, k, nullptr, nullptr, V, dims->T,
+                     nullptr, scale, out, out_dtype, nullptr, 0, stream);
 }
 
 rolesub_status rolesub_attend_causal(const rolesub_dims* dims, rolesub_dtype dtype, const void* q,
@@ -605,7 +618,7 @@ rolesub_status rolesub_attend_causal(const rolesub_dims* dims, rolesub_dtype dty
   const char* fn = "rolesub_attend_causal";
   if (!dims) return fail(ROLESUB_ERR_INVALID_ARG, "%s: dims is NULL", fn);
   if (dims->T == 0) return ROLESUB_OK;  // no prefix tokens, no queries
-  return attend_call(fn, true, dims, dtype, dims->T, q, k, mask, offsets, Vp, cap_groups, R, scale, out,
+  return attend_call(fn, true, false, dims, dtype, dims->T, q, k, mask, offsets, Vp, cap_groups, R, scale, out,
                      out_dtype, workspace, ws_bytes, stream);
 }
 

@@ -70,17 +70,12 @@ def run_layer(h, q, k, v, types, R, budget: rs.Budget, G: int, bufs: LayerBuffer
 @dataclass
 class FullWidthBuffers:
     """Buffers of one full-width layer call: the cache (offsets, Vp), the
-    head-major routed values Vh, and the constants that let the attention
-    kernel read Vh as a one-group cache (unit masks, offsets[b,t] = t,
-    identity rotations)."""
+    head-major routed values Vh and the attention output."""
     offsets: torch.Tensor
     Vp: torch.Tensor
     Vh: torch.Tensor
     out: torch.Tensor
     workspace: torch.Tensor
-    ones: torch.Tensor
-    arange: torch.Tensor
-    eye: torch.Tensor
 
     @staticmethod
     def allocate(B, T, H, dh, S, Tq, cap, dtype, out_dtype=None, device="cuda"):
@@ -91,9 +86,6 @@ class FullWidthBuffers:
             Vh=torch.empty((B, H, T, dh), dtype=dtype, device=device),
             out=torch.empty((B, Tq, H, dh), dtype=out_dtype or dtype, device=device),
             workspace=torch.empty(max(rs.full_workspace_size(B, T, S), 256), dtype=torch.uint8, device=device),
-            ones=torch.ones((B, T), dtype=torch.int32, device=device),
-            arange=torch.arange(T + 1, dtype=torch.int32, device=device).repeat(B, 1).contiguous(),
-            eye=torch.eye(dh, dtype=dtype, device=device).repeat(H, 1, 1).contiguous(),
         )
 
 
@@ -106,5 +98,5 @@ def run_full_layer(q, k, v, mask, Rt, R, S: int, bufs: FullWidthBuffers, budget=
     rs.full_rotate_pack(v, Rt, mask, S, bufs.Vp.shape[1], budget=budget, type_counts=type_counts,
                         workspace=bufs.workspace, out=(bufs.offsets, bufs.Vp), stream=stream)
     rs.full_values(R, mask, bufs.offsets, bufs.Vp, S, H, workspace=bufs.workspace, out=bufs.Vh, stream=stream)
-    rs.attend(q, k, bufs.ones, bufs.arange, bufs.Vh, bufs.eye, 1, out=bufs.out, stream=stream)
+    rs.attend_values(q, k, bufs.Vh, out=bufs.out, stream=stream)
     return bufs

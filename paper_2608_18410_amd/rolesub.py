@@ -27,6 +27,7 @@ EXPORTS = (
     "rolesub_attend_causal", "rolesub_retain_tokens", "rolesub_gather_tokens",
     "rolesub_allocate_groups", "rolesub_route_allocate_workspace_size", "rolesub_route_allocate",
     "rolesub_full_workspace_size", "rolesub_full_transpose", "rolesub_full_rotate_pack", "rolesub_full_values",
+    "rolesub_attend_values",
 )
 
 
@@ -93,6 +94,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rolesub_full_transpose.argtypes = [I32, ctypes.c_int, P, P, P]
     lib.rolesub_full_rotate_pack.argtypes = [P, ctypes.c_int, P, P, P, P, P, I64, P, P, P, SZ, P]
     lib.rolesub_full_values.argtypes = [P, ctypes.c_int, P, P, P, P, I64, P, P, SZ, P]
+    lib.rolesub_attend_values.argtypes = [P, ctypes.c_int, I32, P, P, P, ctypes.c_float, P, ctypes.c_int, P]
     for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_rotate_pack",
                "rolesub_attend"):
         getattr(lib, fn).restype = ctypes.c_int
@@ -433,3 +435,17 @@ def full_values(R, mask, offsets, Vp, S: int, H: int, workspace=None, out=None, 
         ctypes.byref(dims), _code(Vp), _ptr(R, Vp.dtype), _ptr(mask), _ptr(offsets, torch.int32), _ptr(Vp),
         cap, _ptr(Vh, Vp.dtype), _ptr(workspace), workspace.numel(), _stream(stream)))
     return Vh
+
+
+def attend_values(q, k, V, scale: float = 0.0, out_dtype=None, out=None, stream=None):
+    """Attention over plain head-major values V [B,H,T,dh] (the full-width
+    routing space's rebuilt values). Returns [B,Tq,H,dh]."""
+    B, Tq, H, dh = q.shape
+    T = k.shape[1]
+    od = out.dtype if out is not None else (out_dtype or q.dtype)
+    o = torch.empty((B, Tq, H, dh), dtype=od, device=q.device) if out is None else out
+    dims = Dims(B, T, H, dh, 1, 0)
+    _check("rolesub_attend_values", load().rolesub_attend_values(
+        ctypes.byref(dims), _code(q), Tq, _ptr(q), _ptr(k, q.dtype), _ptr(V, q.dtype), ctypes.c_float(scale),
+        _ptr(o), _code(o), _stream(stream)))
+    return o

@@ -201,3 +201,16 @@ def test_full_width_validation(lib):
     assert lib.rolesub_full_transpose(128, rs.BF16, FAKE, FAKE, None) == 1
     assert lib.rolesub_full_transpose(128, rs.F32, FAKE, ctypes.c_void_p(0x10000000), None) == 2
     assert lib.rolesub_full_transpose(0, rs.BF16, None, None, None) == 0
+
+
+def test_attend_values_validation(lib):
+    d = rs.Dims(2, 9, 4, 128, 1, 0)
+    assert lib.rolesub_attend_values(ctypes.byref(d), rs.F32, 4, FAKE, FAKE, FAKE, ctypes.c_float(0.0), FAKE,
+                                     rs.F32, None) == 2
+    assert lib.rolesub_attend_values(ctypes.byref(rs.Dims(2, 9, 4, 96, 1, 0)), rs.BF16, 4, FAKE, FAKE, FAKE,
+                                     ctypes.c_float(0.0), FAKE, rs.F32, None) == 2
+    assert lib.rolesub_attend_values(ctypes.byref(d), rs.BF16, 4, FAKE, None, FAKE, ctypes.c_float(0.0), FAKE,
+                                     rs.F32, None) == 1
+    assert lib.rolesub_attend_values(ctypes.byref(d), rs.BF16, 0, None, None, None, ctypes.c_float(0.0), None,
+                                     rs.F32, None) == 0
+    assert lib.rolesub_attend_values(None, rs.BF16, 4, FAKE, FAKE, FAKE, ctypes.c_float(0.0), FAKE, rs.F32, None) == 1

@@ -865,3 +865,21 @@ def test_full_width_with_role_driven_budgets_and_repeatable():
     torch.cuda.synchronize()
     for a, b_ in zip(first, (bufs.offsets, bufs.Vp, bufs.Vh, bufs.out)):
         assert torch.equal(a, b_)
+
+
+@pytest.mark.parametrize("B,T,Tq,H,dh,out_dtype", [(2, 81, 56, 8, 128, torch.bfloat16), (3, 200, 70, 4, 128, torch.float32),
+                                                   (2, 37, 9, 4, 64, torch.float32)])
+def test_attend_values_is_textbook_attention(B, T, Tq, H, dh, out_dtype):
+    """Attention over plain head-major values (the full-width path's last step)
+    against the oracle with every group kept, where the routed value is v."""
+    rng = np.random.default_rng(T + dh)
+    q = synth.round_to(rng.standard_normal((B, Tq, H, dh)), "bf16")
+    k = synth.round_to(rng.standard_normal((B, T, H, dh)), "bf16")
+    v = synth.round_to(rng.standard_normal((B, T, H, dh)), "bf16")
+    Vh = _dev_bf16(np.ascontiguousarray(v.transpose(0, 2, 1, 3)))
+    got = host(rs.attend_values(_dev_bf16(q), _dev_bf16(k), Vh, out_dtype=out_dtype))
+    R = np.eye(H * dh)
+    want = O.attend_full_plain(q, k, v, np.full((B, T), 1, np.uint32), R, 1)
+    err = max_rel(got, want)
+    _say(f"attend_values B={B} T={T} Tq={Tq} H={H} dh={dh}: max rel err {err:.2e}")
+    assert err <= TOL["bf16"]          # bf16 inputs; P enters the matrix cores in bf16
