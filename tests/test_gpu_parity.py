@@ -883,3 +883,21 @@ def test_attend_values_is_textbook_attention(B, T, Tq, H, dh, out_dtype):
     err = max_rel(got, want)
     _say(f"attend_values B={B} T={T} Tq={Tq} H={H} dh={dh}: max rel err {err:.2e}")
     assert err <= TOL["bf16"]          # bf16 inputs; P enters the matrix cores in bf16
+
+
+def test_full_rotate_pack_never_writes_past_capacity():
+    w = synth.workload(7).replace(B=1)
+    R, v, mask = _full_case(w, 1, 95, ["mixed"])
+    S, ds = w.G, w.ds
+    want_off, want_Vp = O.pack_full(v, mask, R, S, w.T * S)
+    need = int(want_off[0, -1])
+    cap = need // 2
+    big = torch.full((1, need + 8, ds), 7.0, dtype=torch.bfloat16, device=DEV)    # sentinel past cap
+    Rd = _dev_bf16(R)
+    off = torch.empty((1, w.T + 1), dtype=torch.int32, device=DEV)
+    rs.full_rotate_pack(_dev_bf16(v), rs.full_transpose(Rd), put_mask(mask), S, cap, out=(off, big[:, :cap]))
+    torch.cuda.synchronize()
+    got = host(big)
+    assert np.array_equal(host(off), want_off)                   # offsets still count every kept group
+    assert np.all(got[0, cap:] == 7.0)                           # nothing at or past the capacity
+    assert max_rel(got[0, :cap], want_Vp[0, :cap]) <= TOL["bf16"]
