@@ -61,8 +61,10 @@ def stage_bytes(w, sum_k: int) -> dict:
     them (rotation and pack fused: v read once, only kept groups written)."""
     e = 2 if w.dtype == "bf16" else 4
     route_w = (w.Hr * w.router_in + w.C * w.d + w.G * w.Hr + w.C * w.d_e) * e
+    # with given logits the selection reads them instead of running the router
+    route_in = 4 * w.B * w.T * w.G if w.scores_in else w.B * w.T * w.d * e + route_w
     return {
-        "route": w.B * w.T * w.d * e + route_w + 4 * w.B * w.T * (w.G + 2),
+        "route": route_in + 4 * w.B * w.T * (w.G + 2),
         "rotate_pack": w.B * w.T * w.H * w.dh * e + w.H * w.dh * w.dh * e
                        + w.B * sum_k * w.ds * w.H * e + 8 * w.B * w.T,
         "attend": attend_bytes(w, sum_k, e),
@@ -74,14 +76,15 @@ def _source_hash() -> str:
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
 
 
-def _traffic(launches_bytes_hint):
+def _traffic(workload_name):
     """HBM traffic per attention launch from committed rocprofv3 counter runs,
-    or None when absent or taken on a different kernel source."""
+    or None when absent, taken on a different kernel source or on another
+    workload."""
     try:
         t = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if t.get("k_attend_sha256_16") != _source_hash():
+    if t.get("k_attend_sha256_16") != _source_hash() or not str(t.get("workload", "")).startswith(workload_name):
         return None
     return t.get("bytes_per_launch")
 
@@ -727,12 +730,13 @@ def main():
                    "keep": {"vis": w.k_vis, "lang": w.k_lang, "prop": w.k_prop}
                    if w.mode == 0 else {"threshold": w.tau, "kmin": w.kmin, "kmax": w.kmax},
                    "budgets": "role-driven per-token allocation within each type (priority w^T a)"
-                   if args.allocation else "fixed per type",
+                   if args.allocation else ("fixed per type" if w.mode == 0 else
+                                            "threshold on given logits (selection only)"),
                    "value_counts": "query tokens x layers per second (B*Tq*L / step time)",
                    "graphs": not args.eager},
         "roofline": {"kernel": "rolesub_attend (k_attend_bf16)", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": _traffic(a_bytes),
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": _traffic(w.name),
                      "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": att_ms * 1e3},
         "detail": {"attend_query_tokens_per_s": w.B * w.Tq / (att_ms * 1e-3),
                    "layers_per_s": w.L / (ms_step * 1e-3),
