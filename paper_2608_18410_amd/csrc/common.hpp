@@ -97,6 +97,46 @@ __device__ __forceinline__ bool key_equal(float a, float b) {
   return (a == b) || (__builtin_isnan(a) && __builtin_isnan(b));
 }
 
+// The same order as an unsigned integer: order_key(a) > order_key(b) exactly
+// when key_above(a, b), and equal keys exactly when key_equal(a, b). Sign and
+// magnitude become one monotone code (negatives bit-flipped, positives with
+// the top bit set); every NaN maps to 0, below -inf's code.
+__device__ __forceinline__ uint32_t order_key(float x) {
+  uint32_t u = x == 0.f ? 0u : __float_as_uint(x);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return __builtin_isnan(x) ? 0u : u;
+}
+
+// Top-K of the first G of NP scores, in the order above, as a bit mask. Each
+// unordered pair s < t is compared once: s wins when its key is at least t's
+// (equal keys go to the lower index), and the loser's rank (the number of
+// groups ranked before it) goes up by one. Entries past G get key 0 and lose
+// to every real group, which sits at a lower index; rank[s] starts at the
+// number of later entries and drops by one per later entry s beats.
+template <int NP>
+__device__ __forceinline__ uint32_t top_k_pairs(const float* g, int G, int K) {
+  uint32_t key[NP];
+  int rank[NP];
+#pragma unroll
+  for (int s = 0; s < NP; ++s) {
+    key[s] = s < G ? order_key(g[s]) : 0u;
+    rank[s] = NP - 1 - s;
+  }
+#pragma unroll
+  for (int s = 0; s < NP; ++s) {
+#pragma unroll
+    for (int t = s + 1; t < NP; ++t) {
+      const int c = key[s] >= key[t];
+      rank[t] += c;
+      rank[s] -= c;
+    }
+  }
+  uint32_t m = 0;
+#pragma unroll
+  for (int s = 0; s < NP; ++s) m |= static_cast<uint32_t>((s < G) & (rank[s] < K)) << s;
+  return m;
+}
+
 // Number of groups kept by one token (Sec. 3.5).
 __device__ __forceinline__ int budget_k(int mode, const int* k_by_type, int type, float tau,
                                         int kmin, int kmax, int G, int n_above) {

@@ -45,18 +45,7 @@ __device__ __forceinline__ u64 block_sum(u64 x, u64* slot) {
 // the lower group index, -0 equal to +0, NaN last) as a bit mask.
 template <int GP>
 __device__ __forceinline__ uint32_t top_k_mask(const float (&g)[GP], int G, int K) {
-  uint32_t msk = 0;
-#pragma unroll
-  for (int s = 0; s < GP; ++s) {
-    int rank = 0;
-#pragma unroll
-    for (int u = 0; u < GP; ++u) {
-      const bool before = key_above(g[u], g[s]) || (u < s && key_equal(g[u], g[s]));
-      rank += static_cast<int>(u < G && before);
-    }
-    msk |= static_cast<uint32_t>((s < G) & (rank < K)) << s;
-  }
-  return msk;
+  return top_k_pairs<GP>(g, G, K);
 }
 
 template <int GP>

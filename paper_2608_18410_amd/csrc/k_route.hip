@@ -335,22 +335,6 @@ __global__ __launch_bounds__(256) void k_route_proj(RouteParams p) {
   }
 }
 
-// Rank-based selection of one token's groups from scores held in registers.
-__device__ __forceinline__ uint32_t select_from(const float* g, int G, int K) {
-  uint32_t m = 0;
-#pragma unroll
-  for (int s = 0; s < 32; ++s) {
-    if (s < G) {
-      int rank = 0;
-#pragma unroll
-      for (int t = 0; t < 32; ++t)
-        if (t < G) rank += key_above(g[t], g[s]) || (t < s && key_equal(g[t], g[s]));
-      if (rank < K) m |= 1u << s;
-    }
-  }
-  return m;
-}
-
 __device__ __forceinline__ void write_selection(const RouteParams& p, size_t tok, uint32_t m) {
   p.mask[tok] = m;
   if (p.count) p.count[tok] = static_cast<uint8_t>(__popc(m));
@@ -364,10 +348,12 @@ __device__ __forceinline__ void write_selection(const RouteParams& p, size_t tok
 }
 
 // Full selection for one token whose G scores sit in registers of one thread.
+// NP >= G bounds the unrolled loops.
+template <int NP>
 __device__ __forceinline__ uint32_t select_token(const RouteParams& p, const float* g, int type) {
   int n_above = 0;
 #pragma unroll
-  for (int s = 0; s < 32; ++s)
+  for (int s = 0; s < NP; ++s)
     if (s < p.G) n_above += g[s] > p.tau;
   const int K = budget_k(p.mode, p.k_by_type, type, p.tau, p.kmin, p.kmax, p.G, n_above);
   if (p.mode == 1 && K == n_above) {
@@ -375,40 +361,97 @@ __device__ __forceinline__ uint32_t select_token(const RouteParams& p, const flo
     // so the top-K set is exactly the groups above the threshold.
     uint32_t m = 0;
 #pragma unroll
-    for (int s = 0; s < 32; ++s)
+    for (int s = 0; s < NP; ++s)
       if (s < p.G && g[s] > p.tau) m |= 1u << s;
     return m;
   }
-  return select_from(g, p.G, K);
+  return top_k_pairs<NP>(g, p.G, K);
 }
 
 // ---------------------------------------------------------------------------
-// Selection only, from given scores. One thread per token.
-__global__ __launch_bounds__(256) void k_select(RouteParams p) {
+// Selection only, from given scores. A one-wave workgroup takes kSelTok
+// consecutive tokens: their scores are read (and copied to scores_out) with
+// consecutive lanes on consecutive 16-byte pieces, all of a lane's pieces in
+// flight together, staged in LDS with a row stride of G + 1 floats (odd, so
+// one token per lane reads its row without bank conflicts), ranked one token
+// per lane, and the idx bytes are staged in LDS and written out in 16-byte
+// pieces. Reading a token's G scores per lane directly would put consecutive
+// lanes G * 4 bytes apart. Small workgroups keep many in flight per CU. The
+// ranking is vector-ALU bound (a wave runs it when any of its tokens needs
+// it); NP >= G sizes its unrolled pairs, and the occupancy hint keeps the
+// register count where no spills occur.
+constexpr int kSelTok = 64;
+constexpr int kSelPieces = kSelTok * 32 / 4 / kSelTok;  // 16-byte score pieces per lane at G = 32
+
+__device__ __forceinline__ bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; }
+
+template <int NP>
+__global__ __launch_bounds__(kSelTok) __attribute__((amdgpu_waves_per_eu(NP == 32 ? 3 : 5))) void k_select(RouteParams p) {
+  __shared__ __attribute__((aligned(16))) float sg[kSelTok * 33];  // scores, then the idx bytes
+  uint8_t* sidx = reinterpret_cast<uint8_t*>(sg);
   const size_t N = static_cast<size_t>(p.B) * p.T;
-  const size_t tok = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (tok >= N) return;
-  float g[32];
-  const float* src = p.scores_in + tok * p.G;
-  if ((p.G & 3) == 0) {
+  const size_t tok0 = static_cast<size_t>(blockIdx.x) * kSelTok;
+  const int tid = threadIdx.x, G = p.G;
+  const int ntok = static_cast<int>(N - tok0 < kSelTok ? N - tok0 : kSelTok);
+  const int nval = ntok * G;
+  const float* src = p.scores_in + tok0 * G;
+  float* dst = p.scores_out ? p.scores_out + tok0 * G : nullptr;
+  const bool vec = (G & 3) == 0 && aligned16(p.scores_in) && (!dst || aligned16(p.scores_out));
+  if (vec) {
+    // tok0 * G * 4 bytes is a multiple of 16; at most kSelPieces pieces per lane
+    f32x4 v[kSelPieces];
 #pragma unroll
-    for (int s = 0; s < 32; s += 4) {
-      if (s < p.G) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(src + s);
-        g[s] = v[0]; g[s + 1] = v[1]; g[s + 2] = v[2]; g[s + 3] = v[3];
-      } else {
-        g[s] = g[s + 1] = g[s + 2] = g[s + 3] = 0.f;
+    for (int i = 0; i < kSelPieces; ++i) {
+      const int q = tid + i * kSelTok;
+      if (4 * q < nval) v[i] = *reinterpret_cast<const f32x4*>(src + 4 * q);
+    }
+#pragma unroll
+    for (int i = 0; i < kSelPieces; ++i) {
+      const int q = tid + i * kSelTok;
+      if (4 * q < nval) {
+        if (dst) *reinterpret_cast<f32x4*>(dst + 4 * q) = v[i];
+        const int t = (4 * q) / G, s0 = 4 * q - t * G;  // the 4 values share a token (G % 4 == 0)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sg[t * (G + 1) + s0 + j] = v[i][j];
       }
     }
   } else {
-#pragma unroll
-    for (int s = 0; s < 32; ++s) g[s] = s < p.G ? src[s] : 0.f;
+    for (int e = tid; e < nval; e += kSelTok) {
+      const float x = src[e];
+      if (dst) dst[e] = x;
+      const int t = e / G;
+      sg[t * (G + 1) + (e - t * G)] = x;
+    }
   }
-  const uint32_t m = select_token(p, g, p.types ? p.types[tok] : 0);
-  write_selection(p, tok, m);
-  if (p.scores_out) {
-    float* dst = p.scores_out + tok * p.G;
-    for (int s = 0; s < p.G; ++s) dst[s] = src[s];
+  __syncthreads();
+  const bool valid = tid < ntok;
+  float g[NP];
+#pragma unroll
+  for (int s = 0; s < NP; ++s) g[s] = (valid && s < G) ? sg[tid * (G + 1) + s] : 0.f;
+  const size_t tok = tok0 + tid;
+  uint32_t m = 0;
+  if (valid) {
+    m = select_token<NP>(p, g, p.types ? p.types[tok] : 0);
+    p.mask[tok] = m;
+    if (p.count) p.count[tok] = static_cast<uint8_t>(__popc(m));
+  }
+  if (p.idx) {
+    __syncthreads();  // every lane has its scores in registers before sidx overwrites them
+    if (valid) {
+      uint8_t* row = sidx + tid * G;
+      int r = 0;
+      for (int s = 0; s < G; ++s)
+        if ((m >> s) & 1u) row[r++] = static_cast<uint8_t>(s);
+      for (; r < G; ++r) row[r] = 0xFF;
+    }
+    __syncthreads();
+    // tok0 * G bytes is a multiple of 64: 16-byte pieces, then the tail
+    const int nb = ntok * G;
+    uint8_t* out = p.idx + tok0 * G;
+    const int nv = aligned16(p.idx) ? nb / 16 : 0;
+    for (int q = tid; q < nv; q += kSelTok)
+      *reinterpret_cast<u32x4*>(out + 16 * q) = *reinterpret_cast<const u32x4*>(sidx + 16 * q);
+    for (int e = nv * 16 + tid; e < nb; e += kSelTok) out[e] = sidx[e];
   }
 }
 
@@ -490,7 +533,7 @@ __global__ __launch_bounds__(256) void k_route_generic(RouteParams p) {
     float g[32];
 #pragma unroll
     for (int s = 0; s < 32; ++s) g[s] = s < G ? gam[s] : 0.f;
-    if (p.mask) write_selection(p, tok, select_token(p, g, p.types[tok]));
+    if (p.mask) write_selection(p, tok, select_token<32>(p, g, p.types[tok]));
     if (p.scores_out)
       for (int s = 0; s < G; ++s) p.scores_out[tok * G + s] = gam[s];
   }
@@ -904,7 +947,10 @@ size_t route_generic_shm(int d, int G, int C, int Hr, int kind) {
 hipError_t launch_select(const RouteParams& p, hipStream_t s) {
   const size_t ntok = static_cast<size_t>(p.B) * p.T;
   if (ntok == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_select, dim3(static_cast<unsigned>((ntok + 255) / 256)), dim3(256), 0, s, p);
+  const dim3 grid(static_cast<unsigned>((ntok + kSelTok - 1) / kSelTok));
+  if (p.G <= 8) hipLaunchKernelGGL(k_select<8>, grid, dim3(kSelTok), 0, s, p);
+  else if (p.G <= 16) hipLaunchKernelGGL(k_select<16>, grid, dim3(kSelTok), 0, s, p);
+  else hipLaunchKernelGGL(k_select<32>, grid, dim3(kSelTok), 0, s, p);
   return hipGetLastError();
 }
 

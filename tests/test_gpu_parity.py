@@ -82,6 +82,34 @@ def test_select_threshold_clamps(G, kmin, kmax):
     _check_selection(scores, types, bu, G, O.THRESHOLD, (0, 0, 0, 0), 0.0, kmin, kmax)
 
 
+@pytest.mark.parametrize("G,fo,bo", [(16, 1, 3), (32, 2, 1), (16, 0, 0)])
+def test_select_unaligned_buffers(G, fo, bo):
+    """Scores and idx buffers starting fo floats / bo bytes past a 16-byte
+    boundary, with a ragged last workgroup (T = 300)."""
+    r = np.random.default_rng(100 + G + fo)
+    B, T = 1, 300
+    n = B * T * G
+    scores = r.standard_normal((B, T, G)).astype(np.float32)
+    types = r.integers(0, 4, size=(B, T)).astype(np.uint8)
+    kbt = (1, 3, G // 2, G)
+    base_in = torch.zeros(n + 4, dtype=torch.float32, device=DEV)
+    base_out = torch.zeros(n + 4, dtype=torch.float32, device=DEV)
+    base_idx = torch.zeros(n + 16, dtype=torch.uint8, device=DEV)
+    s_in = base_in[fo:fo + n].view(B, T, G)
+    s_in.copy_(put(scores, torch.float32))
+    out = {"scores": base_out[fo:fo + n].view(B, T, G), "idx": base_idx[bo:bo + n].view(B, T, G)}
+    res = rs.route(put_u8(types), rs.make_budget(rs.TOPK, kbt), G, scores_in=s_in, out=out)
+    torch.cuda.synchronize()
+    want = O.select_groups(scores, O.group_budget(scores, types, O.TOPK, kbt, G, 0.0, 0, 0))
+    assert np.array_equal(host_mask(res["mask"]), want)
+    idx, _ = O.mask_to_idx(want, G)
+    assert np.array_equal(host(res["idx"]), idx)
+    assert np.array_equal(host(res["scores"]).view(np.uint32), scores.view(np.uint32))
+    # nothing written around the views
+    assert not host(base_out[:fo]).any() and not host(base_out[fo + n:]).any()
+    assert not host(base_idx[:bo]).any() and not host(base_idx[bo + n:]).any()
+
+
 # ----------------------------------------------------------------------------
 # Pack: bit-exact
 # ----------------------------------------------------------------------------
