@@ -66,13 +66,15 @@ template <int DH, int VM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k_attend_bf16(AttendParams p) {
   // 32-token tiles at DH = 128 (shorter per-tile chains, 140 registers); 64 at
   // DH = 64 so that every thread has a value item per tile
-  constexpr int TK = DH == 128 ? 32 : 64, MT = DH / 16, KS = DH / 32, KLD = DH + 8, ZLD = TK / 2 + 4;
+  constexpr int TK = DH == 128 ? 32 : 64, MT = DH / 16, KS = DH / 32, KLD = DH + 8, ZLD = TK / 2 + 2;
   constexpr int NM2 = TK / 16, NHF = TK / 32;  // 16-token score blocks, 32-token P.V steps
   constexpr int NKP = TK * DH / 8 / 256;          // 16-byte K pieces per thread per tile
   constexpr int NVI = (TK / 2) * (DH / 8) / 256;  // (token pair, 8-dim chunk) items per thread
   // R_h has its own LDS region, filled by buffer->LDS DMA at the start so its
   // load overlaps the key loop; rows are unpadded with 16-byte chunks
-  // XOR-swizzled by row (conflict-free fragment reads). The output staging
+  // XOR-swizzled by row. The Z~^T tile's row stride of TK/2 + 2 dwords keeps
+  // both its 4-byte writes and its 8-byte fragment reads free of bank
+  // conflicts (a stride of TK/2 + 4 made both two-way). The output staging
   // reuses R_h and the tile buffers after the back-rotation. About 51 KB of
   // LDS at DH = 128: three workgroups per CU.
   constexpr int RBY = DH * 2, RCH = RBY / 16;  // bytes and 16-byte chunks per R_h row
@@ -177,6 +179,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       kreg[r] = bload16(r_k, oob_unless(t < T, t * kstride + 16u * c8));
     }
   };
+  // Item it = (token pair pp, 8-dim chunk cc). Bits 0 and 1 of cc are swapped
+  // against the lane order so that the two chunks written by one 32-lane
+  // half-wave land 8 tile rows apart (distinct banks, see store_tile).
+  auto item_of = [](int it, int& pp, int& cc) {
+    pp = it % (TK / 2);
+    const int gi = it / (TK / 2);
+    cc = (gi & ~3) | ((gi & 1) << 1) | ((gi >> 1) & 1);
+  };
   // packed groups of 2 tokens x 8 dims for each item, addressed through the LDS masks/offsets
   u32x4 vA[NVI][2], vB[NVI][2];
   const int64_t cap = p.cap;
@@ -191,8 +201,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   auto load_v = [&](u32x4 (&vreg)[NVI][2], int t0, int slot) {
 #pragma unroll
     for (int r = 0; r < NVI; ++r) {
-      const int it = tid + 256 * r;
-      const int pp = it % (TK / 2), cc = it / (TK / 2);
+      int pp, cc;
+      item_of(tid + 256 * r, pp, cc);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const int tl = 2 * pp + e;
@@ -224,13 +234,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     }
 #pragma unroll
     for (int r = 0; r < NVI; ++r) {
-      const int it = tid + 256 * r;
-      const int pp = it % (TK / 2), cc = it / (TK / 2);
-      uint32_t* zc = Zt + 8 * cc * ZLD + pp;
+      int pp, cc;
+      item_of(tid + 256 * r, pp, cc);
+      // dim 32a + 8b + c sits in tile row 32a + 4b + (c % 4) + 16 (c / 4), so
+      // that the P.V accumulator of lane quarter g4 holds dims 32ks + 8g4 ..
+      // + 7 for each ks (one 16-byte R_h chunk in the back-rotation)
+      uint32_t* zc = Zt + (32 * (cc >> 2) + 4 * (cc & 3)) * ZLD + pp;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        zc[(2 * j) * ZLD] = (vreg[r][0][j] & 0xFFFFu) | (vreg[r][1][j] << 16);
-        zc[(2 * j + 1) * ZLD] = (vreg[r][0][j] >> 16) | (vreg[r][1][j] & 0xFFFF0000u);
+        const int row = 2 * (j & 1) + 16 * (j >> 1);  // dims 2j, 2j + 1 of the chunk
+        zc[row * ZLD] = (vreg[r][0][j] & 0xFFFFu) | (vreg[r][1][j] << 16);
+        zc[(row + 1) * ZLD] = (vreg[r][0][j] >> 16) | (vreg[r][1][j] & 0xFFFF0000u);
       }
     }
   };
@@ -396,21 +410,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   for (int m = 0; m < MT; ++m) {
     o[m] = f32x4{0.f, 0.f, 0.f, 0.f};
     if constexpr (DENSE) {
-      // no rotation: the normalised accumulator, which holds dims
-      // 16m + 4 g4 + i like the rotated result (the P.V order pairs acc[2ks]
-      // with dims 32ks + 4 g4.. and acc[2ks+1] with 32ks + 16 + 4 g4..)
+      // no rotation: the normalised accumulator, dims 32(m/2) + 8 g4 +
+      // 4(m%2) + i (the tile row order), placed accordingly when staged
       o[m] = acc[m] * inv;
       continue;
     }
-    // row 16m + l16, elements 32ks + 4g4 .. +3 and 32ks + 16 + 4g4 .. +3:
-    // byte 8*(g4 & 1) of chunks 4ks + g4/2 and 4ks + 2 + g4/2
+    // A fragment: R_h row 16m + l16 at the dims of ub[ks], 32ks + 8g4 .. + 7:
+    // one 16-byte chunk, 4ks + g4
     const int row = 16 * m + l16;
-    const char* rr = Rs + row * RBY + 8 * (g4 & 1);
+    const char* rr = Rs + row * RBY;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const u32x2 lo = *reinterpret_cast<const u32x2*>(rr + 16 * ((4 * ks + (g4 >> 1)) ^ (row % RCH)));
-      const u32x2 hi = *reinterpret_cast<const u32x2*>(rr + 16 * ((4 * ks + 2 + (g4 >> 1)) ^ (row % RCH)));
-      const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
+      const u32x4 av = *reinterpret_cast<const u32x4*>(rr + 16 * ((4 * ks + g4) ^ (row % RCH)));
       o[m] = mfma_16x16x32(__builtin_bit_cast(bf16x8, av), ub[ks], o[m]);
     }
   }
@@ -429,8 +440,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   if (p.out_f32) {
     constexpr int NC = DH / 4;  // 16-byte chunks per f32 row
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
-      *reinterpret_cast<f32x4*>(stg + l16 * (DH * 4) + 16 * ((4 * m + g4) ^ l16)) = o[m];
+    for (int m = 0; m < MT; ++m) {
+      // 16-byte chunk of o[m]: dims 16m + 4g4 .. (rotated) or the tile row order (dense)
+      const int c = DENSE ? 8 * (m >> 1) + 2 * g4 + (m & 1) : 4 * m + g4;
+      *reinterpret_cast<f32x4*>(stg + l16 * (DH * 4) + 16 * (c ^ l16)) = o[m];
+    }
 #pragma unroll
     for (int i = 0; i < 16 * NC / 64; ++i) {
       const int u = 64 * i + lane, r = u / NC, c = u % NC;
@@ -446,7 +460,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       ov[1] = static_cast<bf16>(o[m][1]);
       ov[2] = static_cast<bf16>(o[m][2]);
       ov[3] = static_cast<bf16>(o[m][3]);
-      *reinterpret_cast<bf16x4*>(stg + l16 * (DH * 2) + 16 * ((2 * m + (g4 >> 1)) ^ (l16 % NC)) + 8 * (g4 & 1)) = ov;
+      // 16-byte chunk and 8-byte half of o[m] (see the f32 case)
+      const int c = DENSE ? 4 * (m >> 1) + g4 : 2 * m + (g4 >> 1), hf = DENSE ? (m & 1) : (g4 & 1);
+      *reinterpret_cast<bf16x4*>(stg + l16 * (DH * 2) + 16 * (c ^ (l16 % NC)) + 8 * hf) = ov;
     }
 #pragma unroll
     for (int i = 0; i < 16 * NC / 64; ++i) {
