@@ -60,6 +60,11 @@ __device__ __forceinline__ void sched_reads_ahead() {
 //          the output is the normalised accumulator itself
 constexpr int kWide = 0, kDs4 = 1, kDs2 = 2, kDense = 3;
 
+template <bool B>
+struct Flag {
+  static constexpr bool value = B;
+};
+
 // Three waves per SIMD (three workgroups per CU): the register budget is
 // capped at 168 so that occupancy, not just the pipeline, hides latency.
 template <int DH, int VM>
@@ -225,13 +230,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
       }
     }
   };
-  auto store_tile = [&](const u32x4 (&kreg)[NKP], const u32x4 (&vreg)[NVI][2]) {
+  auto store_k = [&](const u32x4 (&kreg)[NKP]) {
 #pragma unroll
     for (int r = 0; r < NKP; ++r) {
       const int pc = tid + 256 * r;
       const int row = pc / (DH / 8), c8 = pc % (DH / 8);
       *reinterpret_cast<u32x4*>(Ks + row * KLD + 8 * c8) = kreg[r];
     }
+  };
+  auto store_v = [&](const u32x4 (&vreg)[NVI][2]) {
 #pragma unroll
     for (int r = 0; r < NVI; ++r) {
       int pp, cc;
@@ -247,6 +254,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
         zc[(row + 1) * ZLD] = (vreg[r][0][j] >> 16) | (vreg[r][1][j] & 0xFFFF0000u);
       }
     }
+  };
+  auto store_tile = [&](const u32x4 (&kreg)[NKP], const u32x4 (&vreg)[NVI][2]) {
+    store_k(kreg);
+    store_v(vreg);
   };
 
   // ---- pipeline: the operands of tiles i+1 and i+2 are in flight while
@@ -290,8 +301,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   // overwrites slot 0 with tile 2's metadata
   __syncthreads();
 
-  auto step = [&](int t0, int slot, u32x4 (&kreg)[NKP], u32x4 (&vreg)[NVI][2], uint32_t& mreg, int32_t& oreg) {
-    store_tile(kreg, vreg);
+  // SPLIT (the first tile only): its packed groups were requested one
+  // metadata round trip after its keys, so the keys go to LDS first and the
+  // scores and softmax are computed while the groups are still in flight;
+  // the groups are stored (and the next loads into their registers issued)
+  // just before P.V, behind one more barrier.
+  auto step = [&](auto split, int t0, int slot, u32x4 (&kreg)[NKP], u32x4 (&vreg)[NVI][2], uint32_t& mreg,
+                  int32_t& oreg) {
+    constexpr bool SPLIT = decltype(split)::value;
+    if constexpr (SPLIT) store_k(kreg);
+    else store_tile(kreg, vreg);
     if (tid < TK) {  // masks/offsets of tile t0 + 2*TK into this tile's slot
       s_mask[slot][tid] = mreg & gm;
       s_off[slot][tid] = oreg;
@@ -301,7 +320,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
     // memory access), so there is no branch here: a branch around the loads
     // makes the compiler wait on every outstanding load at its join
     load_k(kreg, t0 + 2 * TK);
-    load_v(vreg, t0 + 2 * TK, slot);
+    if constexpr (!SPLIT) load_v(vreg, t0 + 2 * TK, slot);
     load_meta(t0 + 4 * TK, mreg, oreg);
 
     // ---- S^T = K Q^T (rows: tile tokens 16*m2 + 4*g4 + i; column: this lane's query)
@@ -363,6 +382,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
         pb[m2 >> 1][4 * (m2 & 1) + i] = static_cast<bf16>(pr);
       }
     l_run += psum;
+    if constexpr (SPLIT) {
+      store_v(vreg);
+      load_v(vreg, t0 + 2 * TK, slot);
+      __syncthreads();
+    }
     // ---- O^T += Z~^T P^T, one MFMA per 32 tokens
     {
       u32x4 zf[MT * NHF];
@@ -384,9 +408,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   };
   // prefix self-attention: keys past this block's last query are all masked
   const int t_stop = p.causal ? min(T, qb * 64 + 64) : T;
-  for (int t0 = 0; t0 < t_stop; t0 += 2 * TK) {
-    step(t0, 0, kA, vA, mA, oA);
-    step(t0 + TK, 1, kB, vB, mB, oB);
+  // t_stop >= 1 (T >= 1): the first pair always runs, with no branch around it
+  step(Flag<true>{}, 0, 0, kA, vA, mA, oA);
+  step(Flag<false>{}, TK, 1, kB, vB, mB, oB);
+  for (int t0 = 2 * TK; t0 < t_stop; t0 += 2 * TK) {
+    step(Flag<false>{}, t0, 0, kA, vA, mA, oA);
+    step(Flag<false>{}, t0 + TK, 1, kB, vB, mB, oB);
   }
 
   // ---- R_h has landed (its DMA was issued before every other load; the loop
