@@ -245,6 +245,9 @@ def _attend_case(w, B, T, Tq, H, dh, G, counts=None, out_dtype=None, seed=0):
     (1, 2, 33, 3, 4, 128, 4),          # f32, head dim 128
     (3, 301, 70, 20, 4, 128, 8),       # runs of 3 samples per workgroup, last run shorter
     (3, 150, 40, 9, 8, 64, 16),        # one tile per sample: every tile starts and ends one
+    (3, 2, 5, 3, 4, 128, 8),           # fewer tokens than one tile, one partial query block
+    (5, 2, 31, 17, 8, 128, 32),        # one token short of a tile, 4-dim groups
+    (3, 1, 1, 1, 4, 64, 8),            # a single token and a single query
 ])
 def test_attend(cid, B, T, Tq, H, dh, G):
     w = synth.workload(cid)
@@ -896,7 +899,8 @@ def test_full_width_with_role_driven_budgets_and_repeatable():
 
 
 @pytest.mark.parametrize("B,T,Tq,H,dh,out_dtype", [(2, 81, 56, 8, 128, torch.bfloat16), (3, 200, 70, 4, 128, torch.float32),
-                                                   (2, 37, 9, 4, 64, torch.float32)])
+                                                   (2, 37, 9, 4, 64, torch.float32), (2, 1, 5, 2, 128, torch.bfloat16),
+                                                   (1, 32, 1, 3, 128, torch.bfloat16)])
 def test_attend_values_is_textbook_attention(B, T, Tq, H, dh, out_dtype):
     """Attention over plain head-major values (the full-width path's last step)
     against the oracle with every group kept, where the routed value is v."""
