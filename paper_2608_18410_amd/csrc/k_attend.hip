@@ -37,7 +37,8 @@ __device__ __forceinline__ void sched_reads_ahead() {
 // dim 64):
 //   * K tile (TK x DH) -> LDS, shared by the four waves;
 //   * the tile's packed groups -> a zero-filled, transposed LDS tile
-//     Zt[dim][token] (token pairs packed in one dword);
+//     Zt[row][token] (token pairs packed in one dword), its rows the dims in
+//     the permuted order that store_v describes;
 //   * S^T = K Q^T on MFMA (queries are the B operand held in registers), so
 //     each lane owns one query column and TK/4 token rows;
 //   * online softmax per query: in-lane, then 2 cross-lane steps, against a
