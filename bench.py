@@ -517,7 +517,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the path shards by prefix or head with no exchange; see the design notes)",
+              "(the path would shard by prefix or by head, with no exchange between GPUs)",
               file=sys.stderr)
         sys.exit(2)
 
