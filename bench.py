@@ -90,26 +90,32 @@ def _traffic(workload_name):
 
 
 def cpu_baseline(w, budget_s: float = 12.0, allocation: bool = False) -> dict:
-    """The float64 oracle (test infrastructure) on whole prefixes of layer 0."""
+    """The float64 oracle (test infrastructure) on whole prefixes, layer 0 first
+    and further layers while the time budget lasts."""
     import oracle as O
     import synth
     from threadpoolctl import threadpool_info
 
-    wt = synth.layer_weights(w, 0)
-    wpri = synth.priority_weights(w, 0) if allocation else None
     cap = sum(n * min(k, w.G) for n, k in zip(w.type_counts(), w.k_by_type))
-    done, spent = 0, 0.0
-    while spent < budget_s and done < w.B:
-        a = synth.sample_activations(w, 0, done)
-        t0 = time.perf_counter()
-        O.pipeline(a["h"][None], a["q"][None], a["k"][None], a["v"][None], w.types(), wt, w.mode,
-                   w.k_by_type, w.G, w.tau, w.kmin, w.kmax, cap=cap, w_pri=wpri)
-        spent += time.perf_counter() - t0
-        done += 1
+    done, spent, layer = 0, 0.0, 0
+    while spent < budget_s and layer < w.L:
+        wt = synth.layer_weights(w, layer)
+        wpri = synth.priority_weights(w, layer) if allocation else None
+        b = 0
+        while spent < budget_s and b < w.B:
+            a = synth.sample_activations(w, layer, b)
+            t0 = time.perf_counter()
+            O.pipeline(a["h"][None], a["q"][None], a["k"][None], a["v"][None], w.types(), wt, w.mode,
+                       w.k_by_type, w.G, w.tau, w.kmin, w.kmax, cap=cap, w_pri=wpri)
+            spent += time.perf_counter() - t0
+            done += 1
+            b += 1
+        layer += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": done * w.Tq / spent, "unit": "query-tokens/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"layer 0, prefixes 0..{done - 1} of {w.B}: route->"
+            "sample": f"{done} (layer, prefix) pairs, layers 0..{layer - 1} of {w.L} with {w.B} prefixes "
+                      f"each (the last layer possibly partial): route->"
                       f"{'allocate->' if allocation else ''}rotate->pack->attend in float64 "
                       f"({spent:.1f} s); BLAS pool {threads} threads, Python loops on one core"}
 
