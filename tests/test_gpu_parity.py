@@ -82,7 +82,7 @@ def test_select_threshold_clamps(G, kmin, kmax):
     _check_selection(scores, types, bu, G, O.THRESHOLD, (0, 0, 0, 0), 0.0, kmin, kmax)
 
 
-@pytest.mark.parametrize("G,fo,bo", [(16, 1, 3), (32, 2, 1), (16, 0, 0)])
+@pytest.mark.parametrize("G,fo,bo", [(16, 1, 3), (32, 2, 1), (16, 0, 0), (5, 1, 2), (5, 0, 0)])
 def test_select_unaligned_buffers(G, fo, bo):
     """Scores and idx buffers starting fo floats / bo bytes past a 16-byte
     boundary, with a ragged last workgroup (T = 300)."""
