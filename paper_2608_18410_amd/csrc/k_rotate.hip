@@ -224,7 +224,10 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       constexpr int NQ = 16 * DH * 2 / U;  // units of a fully kept tile
       const int lsu = lds + 1 - __builtin_ctz(U);  // log2(units per slot)
       const int nunit = nslot << lsu;
-#pragma unroll
+      // unrolled by 4 only: fully unrolled, the 8 rounds of 8-byte units (G = 32)
+      // kept every round's address live and cost a wave per SIMD (188
+      // registers against 146)
+#pragma unroll 4
       for (int q0 = 0; q0 < NQ; q0 += 64) {
         const int q = q0 + lane;
         const int ls = min(q >> lsu, NSLOT - 1);
