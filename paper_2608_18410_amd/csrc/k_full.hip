@@ -350,11 +350,15 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     return k0 >= dv ? dv : (kn < dv ? kn : dv);
   };
   const int k_first = tile_or == 0 ? dv : static_cast<int>(__builtin_ctz(tile_or)) * ds;
-  // active steps: a multiple of NS = 4 (ds is a multiple of 128: at least 4
-  // steps per group). Eight sets for the rotation were measured slower (two
-  // workgroups per CU instead of four).
+  // active steps: a multiple of 4 (ds is a multiple of 128: at least 4 steps
+  // per group), which NS divides. Eight sets for the rotation were measured
+  // slower (two workgroups per CU instead of four); the values product uses
+  // two (three workgroups per CU instead of two, about 3 % faster than four).
   const int nsteps = MODE == 0 ? dv / kBK : __popc(tile_or) * (ds / kBK);
 
+  // the loop body covers NS steps and picks the LDS buffer by step parity:
+  // NS must be even and divide the step count
+  static_assert(NS == 2 || NS == 4, "operand sets: even and a divisor of 4");
   f32x4 acc[MI][4];
 #pragma unroll
   for (int i = 0; i < MI; ++i)
@@ -493,7 +497,7 @@ hipError_t launch_full(const FullParams& p, int mode, hipStream_t s) {
     hipLaunchKernelGGL(k_full_prep<false>, gprep, dim3(256), shm_vals, s, p);
     const unsigned ntn = static_cast<unsigned>(p.dv / kBN);
     const unsigned nmt = static_cast<unsigned>((rows + kBM1 - 1) / kBM1);
-    hipLaunchKernelGGL((k_full_gemm<1, kBM1, 4>), dim3(ntn * nmt), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((k_full_gemm<1, kBM1, 2>), dim3(ntn * nmt), dim3(256), 0, s, p);
   }
   return hipGetLastError();
 }
