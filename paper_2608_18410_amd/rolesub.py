@@ -133,6 +133,40 @@ def _ptr(t, dtype=None):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _fmt(shape):
+    return "[" + ", ".join("*" if x is None else str(int(x)) for x in shape) + "]"
+
+
+def _need(name, t, shape, dtype=None):
+    """Check a tensor argument's shape (None: any extent) and dtype on the host,
+    before anything is launched: the library receives bare pointers and would
+    otherwise read or write past a wrongly sized buffer."""
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor, got {type(t).__name__}")
+    if t.dim() != len(shape) or any(s is not None and int(s) != int(x) for s, x in zip(shape, t.shape)):
+        raise ValueError(f"{name}: expected shape {_fmt(shape)}, got {list(t.shape)}")
+    if dtype is not None:
+        ok = dtype if isinstance(dtype, tuple) else (dtype,)
+        if t.dtype not in ok:
+            raise TypeError(f"{name}: expected dtype {' or '.join(str(d) for d in ok)}, got {t.dtype}")
+
+
+_MASK = (torch.int32, torch.uint32)
+
+
+def _same_device(*ts):
+    devs = {t.device for t in ts if isinstance(t, torch.Tensor)}
+    if len(devs) > 1:
+        raise ValueError(f"tensors on different devices: {sorted(str(d) for d in devs)}")
+
+
+def _need_workspace(t):
+    if t is not None:
+        _need("workspace", t, (None,), torch.uint8)
+
+
 def _stream(stream=None):
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
@@ -166,6 +200,20 @@ class Router:
             setattr(r, name, _ptr(t).value)
         return r
 
+    def check(self, d: int, G: int, dtype) -> None:
+        """Weight shapes against the hidden size d and G groups (row-major [out][in])."""
+        t, C = self.tensors, self.C
+        if self.kind == MLP2:
+            shapes = dict(W_r=(C, d), b_r=(C,), E=(C, self.d_e), W1=(self.Hr, 2 * d + self.d_e), b1=(self.Hr,),
+                          W2=(G, self.Hr), b2=(G,))
+        else:
+            shapes = dict(W_tok=(G, d), b_tok=(G,), W_r=(C, d), b_r=(C,), W_role=(G, C), W_lang=(G, d),
+                          b_lang=(G,))
+        for name, shape in shapes.items():
+            if name not in t:
+                raise ValueError(f"router: missing {name}")
+            _need(f"router.{name}", t[name], shape, dtype)
+
     @staticmethod
     def mlp2(W_r, b_r, E, W1, b1, W2, b2) -> "Router":
         return Router(MLP2, W_r.shape[0], dict(W_r=W_r, b_r=b_r, E=E, W1=W1, b1=b1, W2=W2, b2=b2),
@@ -184,7 +232,11 @@ class Router:
 
 def rotate_values(v: torch.Tensor, R: torch.Tensor, out: torch.Tensor | None = None, stream=None):
     """z = R_h^T v per head. v [B,T,H,dh], R [H,dh,dh]."""
+    _need("v", v, (None, None, None, None))
     B, T, H, dh = v.shape
+    _need("R", R, (H, dh, dh), v.dtype)
+    _need("out", out, (B, T, H, dh), v.dtype)
+    _same_device(v, R, out)
     z = torch.empty_like(v) if out is None else out
     dims = Dims(B, T, H, dh, 1, 0)
     _check("rolesub_rotate_values", load().rolesub_rotate_values(
@@ -202,11 +254,21 @@ def route(token_type: torch.Tensor, budget: Budget, G: int, h: torch.Tensor | No
           router: Router | None = None, scores_in: torch.Tensor | None = None, *,
           want_scores=True, want_idx=True, want_count=True, workspace=None, out=None, stream=None):
     """Routing scores and group selection. Returns dict(mask, idx, count, scores)."""
+    _need("token_type", token_type, (None, None), torch.uint8)
     B, T = token_type.shape
     dev = token_type.device
+    _need("h", h, (B, T, None), (torch.float32, torch.bfloat16))
     d = 0 if h is None else h.shape[2]
     dtype = torch.float32 if h is None else h.dtype
+    _need("scores_in", scores_in, (B, T, G), torch.float32)
+    if router is not None and h is not None:
+        router.check(d, G, dtype)
     o = out or {}
+    for name, shape, dt in (("mask", (B, T), _MASK), ("idx", (B, T, G), torch.uint8),
+                            ("count", (B, T), torch.uint8), ("scores", (B, T, G), torch.float32)):
+        _need(f"out[{name!r}]", o.get(name), shape, dt)
+    _need_workspace(workspace)
+    _same_device(token_type, h, scores_in, workspace, *o.values())
 
     def buf(name, shape, dtype, want=True):
         if not want:
@@ -236,8 +298,14 @@ def route(token_type: torch.Tensor, budget: Budget, G: int, h: torch.Tensor | No
 def pack_kv(z: torch.Tensor, mask: torch.Tensor, G: int, cap: int, budget: Budget | None = None,
             type_counts=None, out=None, stream=None):
     """Compact group-indexed cache. Returns (offsets [B,T+1] int32, Vp [B,H,cap,ds])."""
+    _need("z", z, (None, None, None, None))
     B, T, H, dh = z.shape
     ds = dh // G
+    _need("mask", mask, (B, T), _MASK)
+    if out is not None:
+        _need("offsets", out[0], (B, T + 1), torch.int32)
+        _need("Vp", out[1], (B, H, cap, ds), z.dtype)
+    _same_device(z, mask, *(out or ()))
     offsets = torch.empty((B, T + 1), dtype=torch.int32, device=z.device) if out is None else out[0]
     Vp = torch.empty((B, H, cap, ds), dtype=z.dtype, device=z.device) if out is None else out[1]
     dims = Dims(B, T, H, dh, G, 0)
@@ -251,8 +319,15 @@ def pack_kv(z: torch.Tensor, mask: torch.Tensor, G: int, cap: int, budget: Budge
 def rotate_pack(v: torch.Tensor, R: torch.Tensor, mask: torch.Tensor, G: int, cap: int,
                 budget: Budget | None = None, type_counts=None, out=None, stream=None):
     """Rotation and pack in one pass (z is not materialised). Returns (offsets, Vp)."""
+    _need("v", v, (None, None, None, None))
     B, T, H, dh = v.shape
     ds = dh // G
+    _need("R", R, (H, dh, dh), v.dtype)
+    _need("mask", mask, (B, T), _MASK)
+    if out is not None:
+        _need("offsets", out[0], (B, T + 1), torch.int32)
+        _need("Vp", out[1], (B, H, cap, ds), v.dtype)
+    _same_device(v, R, mask, *(out or ()))
     offsets = torch.empty((B, T + 1), dtype=torch.int32, device=v.device) if out is None else out[0]
     Vp = torch.empty((B, H, cap, ds), dtype=v.dtype, device=v.device) if out is None else out[1]
     dims = Dims(B, T, H, dh, G, 0)
@@ -266,9 +341,17 @@ def rotate_pack(v: torch.Tensor, R: torch.Tensor, mask: torch.Tensor, G: int, ca
 
 def attend(q, k, mask, offsets, Vp, R, G: int, scale: float = 0.0, out_dtype=None, out=None, stream=None):
     """Attention with full q, k over the packed routed values; returns [B,Tq,H,dh]."""
+    _need("q", q, (None, None, None, None))
     B, Tq, H, dh = q.shape
+    _need("k", k, (B, None, H, dh), q.dtype)
     T = k.shape[1]
+    _need("Vp", Vp, (B, H, None, dh // max(G, 1)), q.dtype)
     cap = Vp.shape[2]
+    _need("mask", mask, (B, T), _MASK)
+    _need("offsets", offsets, (B, T + 1), torch.int32)
+    _need("R", R, (H, dh, dh), q.dtype)
+    _need("out", out, (B, Tq, H, dh), (torch.float32, torch.bfloat16))
+    _same_device(q, k, mask, offsets, Vp, R, out)
     odt = q.dtype if out_dtype is None else out_dtype
     o = torch.empty((B, Tq, H, dh), dtype=odt, device=q.device) if out is None else out
     dims = Dims(B, T, H, dh, G, 0)
@@ -282,8 +365,16 @@ def attend(q, k, mask, offsets, Vp, R, G: int, scale: float = 0.0, out_dtype=Non
 def attend_causal(q, k, mask, offsets, Vp, R, G: int, scale: float = 0.0, out_dtype=None, out=None, stream=None):
     """Prefix self-attention over the packed routed values (query t sees keys
     0..t); q and k are [B,T,H,dh]; returns [B,T,H,dh]."""
+    _need("q", q, (None, None, None, None))
     B, T, H, dh = q.shape
+    _need("k", k, (B, T, H, dh), q.dtype)
+    _need("Vp", Vp, (B, H, None, dh // max(G, 1)), q.dtype)
     cap = Vp.shape[2]
+    _need("mask", mask, (B, T), _MASK)
+    _need("offsets", offsets, (B, T + 1), torch.int32)
+    _need("R", R, (H, dh, dh), q.dtype)
+    _need("out", out, (B, T, H, dh), (torch.float32, torch.bfloat16))
+    _same_device(q, k, mask, offsets, Vp, R, out)
     odt = q.dtype if out_dtype is None else out_dtype
     o = torch.empty((B, T, H, dh), dtype=odt, device=q.device) if out is None else out
     dims = Dims(B, T, H, dh, G, 0)
@@ -297,8 +388,13 @@ def attend_causal(q, k, mask, offsets, Vp, R, G: int, scale: float = 0.0, out_dt
 def retain_tokens(scores, seg_len, seg_keep, out=None, stream=None):
     """Per sample and per segment of consecutive tokens, the indices of the
     seg_keep highest-scoring tokens (int32 [B, sum(seg_keep)])."""
+    _need("scores", scores, (None, None), torch.float32)
     B, N = scores.shape
     n = len(seg_len)
+    if len(seg_keep) != n:
+        raise ValueError(f"seg_keep has {len(seg_keep)} entries for {n} segments")
+    _need("out", out, (B, int(sum(seg_keep))), torch.int32)
+    _same_device(scores, out)
     lens = (ctypes.c_int32 * n)(*[int(x) for x in seg_len])
     keeps = (ctypes.c_int32 * n)(*[int(x) for x in seg_keep])
     K = int(sum(seg_keep))
@@ -310,8 +406,13 @@ def retain_tokens(scores, seg_len, seg_keep, out=None, stream=None):
 
 def gather_tokens(x, idx, out=None, stream=None):
     """Rows x[b, idx[b, j]] of a [B, N, ...] tensor (the retained prefix)."""
+    if not isinstance(x, torch.Tensor) or x.dim() < 2:
+        raise ValueError("x: expected a [B, N, ...] tensor")
     B, N = x.shape[:2]
+    _need("idx", idx, (B, None), torch.int32)
     K = idx.shape[1]
+    _need("out", out, (B, K) + tuple(x.shape[2:]), x.dtype)
+    _same_device(x, idx, out)
     o = torch.empty((B, K) + tuple(x.shape[2:]), dtype=x.dtype, device=x.device) if out is None else out
     row_bytes = x[0, 0].numel() * x.element_size() if N else 0
     _check("rolesub_gather_tokens", load().rolesub_gather_tokens(
@@ -323,9 +424,16 @@ def allocate_groups(priority, token_type, k_by_type, G: int, scores=None, *, wan
                     want_count=True, out=None, stream=None):
     """Role-driven within-type group budgets K_i from token priorities, and with
     scores the Top-K_i selection on them. Returns dict(k, mask, idx, count)."""
+    _need("token_type", token_type, (None, None), torch.uint8)
     B, T = token_type.shape
     dev = token_type.device
+    _need("priority", priority, (B, T), torch.float32)
+    _need("scores", scores, (B, T, G), torch.float32)
     o = out or {}
+    for name, shape, dt in (("k", (B, T), torch.uint8), ("mask", (B, T), _MASK), ("idx", (B, T, G), torch.uint8),
+                            ("count", (B, T), torch.uint8)):
+        _need(f"out[{name!r}]", o.get(name), shape, dt)
+    _same_device(token_type, priority, scores, *o.values())
 
     def buf(name, shape, dtype, want=True):
         if not want:
@@ -356,10 +464,20 @@ def route_allocate(token_type, k_by_type, G: int, h, router: Router, w_pri, *, w
     """Routing with role-driven budgets: scores, priorities p = w_pri^T a, the
     allocated K_i and the Top-K_i selection. Returns dict(mask, idx, count, k,
     scores, priority)."""
+    _need("token_type", token_type, (None, None), torch.uint8)
     B, T = token_type.shape
     dev = token_type.device
+    _need("h", h, (B, T, None), (torch.float32, torch.bfloat16))
     d = h.shape[2]
+    router.check(d, G, h.dtype)
+    _need("w_pri", w_pri, (router.C,), h.dtype)
     o = out or {}
+    for name, shape, dt in (("mask", (B, T), _MASK), ("idx", (B, T, G), torch.uint8), ("count", (B, T), torch.uint8),
+                            ("k", (B, T), torch.uint8), ("scores", (B, T, G), torch.float32),
+                            ("priority", (B, T), torch.float32)):
+        _need(f"out[{name!r}]", o.get(name), shape, dt)
+    _need_workspace(workspace)
+    _same_device(token_type, h, w_pri, workspace, *o.values())
 
     def buf(name, shape, dtype, want=True):
         if not want:
@@ -395,7 +513,11 @@ def full_workspace_size(B, T, S) -> int:
 
 def full_transpose(R, out=None, stream=None):
     """R^T of a frozen [d_v, d_v] rotation (the layout full_rotate_pack takes)."""
+    _need("R", R, (None, None))
     n = R.shape[0]
+    _need("R", R, (n, n))
+    _need("out", out, (n, n), R.dtype)
+    _same_device(R, out)
     Rt = torch.empty_like(R) if out is None else out
     _check("rolesub_full_transpose", load().rolesub_full_transpose(n, _code(R), _ptr(R), _ptr(Rt, R.dtype),
                                                                    _stream(stream)))
@@ -405,8 +527,16 @@ def full_transpose(R, out=None, stream=None):
 def full_rotate_pack(v, Rt, mask, S: int, cap: int, budget: Budget | None = None, type_counts=None,
                      workspace=None, out=None, stream=None):
     """Full-width cache: (offsets [B,T+1] int32, Vp [B,cap,d_v/S])."""
+    _need("v", v, (None, None, None, None))
     B, T, H, dh = v.shape
     dv = H * dh
+    _need("Rt", Rt, (dv, dv), v.dtype)
+    _need("mask", mask, (B, T), _MASK)
+    if out is not None:
+        _need("offsets", out[0], (B, T + 1), torch.int32)
+        _need("Vp", out[1], (B, cap, dv // max(S, 1)), v.dtype)
+    _need_workspace(workspace)
+    _same_device(v, Rt, mask, workspace, *(out or ()))
     if out is None:
         out = (torch.empty((B, T + 1), dtype=torch.int32, device=v.device),
                torch.empty((B, cap, dv // S), dtype=v.dtype, device=v.device))
@@ -424,9 +554,18 @@ def full_rotate_pack(v, Rt, mask, S: int, cap: int, budget: Budget | None = None
 
 def full_values(R, mask, offsets, Vp, S: int, H: int, workspace=None, out=None, stream=None):
     """Routed values [B,H,T,dh] (head-major) from the full-width cache."""
+    _need("Vp", Vp, (None, None, None))
     B, cap, ds = Vp.shape
+    _need("offsets", offsets, (B, None), torch.int32)
     T = offsets.shape[1] - 1
+    if H < 1 or (ds * S) % H:
+        raise ValueError(f"d_v = {ds * S} does not split into {H} heads")
     dh = ds * S // H
+    _need("R", R, (ds * S, ds * S), Vp.dtype)
+    _need("mask", mask, (B, T), _MASK)
+    _need("out", out, (B, H, T, dh), Vp.dtype)
+    _need_workspace(workspace)
+    _same_device(Vp, offsets, R, mask, out, workspace)
     Vh = torch.empty((B, H, T, dh), dtype=Vp.dtype, device=Vp.device) if out is None else out
     if workspace is None:
         workspace = torch.empty(max(full_workspace_size(B, T, S), 1), dtype=torch.uint8, device=Vp.device)
@@ -440,8 +579,13 @@ def full_values(R, mask, offsets, Vp, S: int, H: int, workspace=None, out=None, 
 def attend_values(q, k, V, scale: float = 0.0, out_dtype=None, out=None, stream=None):
     """Attention over plain head-major values V [B,H,T,dh] (the full-width
     routing space's rebuilt values). Returns [B,Tq,H,dh]."""
+    _need("q", q, (None, None, None, None))
     B, Tq, H, dh = q.shape
+    _need("k", k, (B, None, H, dh), q.dtype)
     T = k.shape[1]
+    _need("V", V, (B, H, T, dh), q.dtype)
+    _need("out", out, (B, Tq, H, dh), (torch.float32, torch.bfloat16))
+    _same_device(q, k, V, out)
     od = out.dtype if out is not None else (out_dtype or q.dtype)
     o = torch.empty((B, Tq, H, dh), dtype=od, device=q.device) if out is None else out
     dims = Dims(B, T, H, dh, 1, 0)

@@ -217,7 +217,7 @@ def test_rotate_pack_fused(cid, B, T, H, dh, G):
 # Attention over the packed cache
 # ----------------------------------------------------------------------------
 
-def _attend_case(w, B, T, Tq, H, dh, G, counts=None, out_dtype=None, seed=0):
+def _attend_case(w, B, T, Tq, H, dh, G, counts=None, out_dtype=None, seed=0, scale=None):
     w = w.replace(B=B, n_vis=T, n_lang=0, n_prop=0, Tq=Tq, H=H, dh=dh, G=G)
     dt = tdtype(w)
     acts = [synth.sample_activations(w, seed, b, ("q", "k")) for b in range(B)]
@@ -228,10 +228,11 @@ def _attend_case(w, B, T, Tq, H, dh, G, counts=None, out_dtype=None, seed=0):
     R = synth.layer_weights(w, seed)["R"]
     cap = T * G
     off, Vp = rs.pack_kv(put(z, dt), put_mask(m), G, cap)
-    out = rs.attend(put(q, dt), put(k, dt), put_mask(m), off, Vp, put(R, dt), G, out_dtype=out_dtype)
+    out = rs.attend(put(q, dt), put(k, dt), put_mask(m), off, Vp, put(R, dt), G, out_dtype=out_dtype,
+                    scale=0.0 if scale is None else scale)
     torch.cuda.synchronize()
     o_ref, Vp_ref = O.pack(z, m, G, cap)
-    ref = O.attend_packed(q, k, m, o_ref, Vp_ref, R, G)
+    ref = O.attend_packed(q, k, m, o_ref, Vp_ref, R, G, scale=scale)
     return host(out), ref, (q, k, z, m, R)
 
 
@@ -258,7 +259,7 @@ def test_attend(cid, B, T, Tq, H, dh, G):
     assert err <= TOL[w.dtype]
 
 
-def _attend_causal_case(w, B, T, H, dh, G, counts=None, out_dtype=None, seed=0):
+def _attend_causal_case(w, B, T, H, dh, G, counts=None, out_dtype=None, seed=0, scale=None):
     w = w.replace(B=B, n_vis=T, n_lang=0, n_prop=0, Tq=T, H=H, dh=dh, G=G)
     dt = tdtype(w)
     acts = [synth.sample_activations(w, seed, b, ("q", "k")) for b in range(B)]
@@ -269,10 +270,11 @@ def _attend_causal_case(w, B, T, H, dh, G, counts=None, out_dtype=None, seed=0):
     R = synth.layer_weights(w, seed)["R"]
     cap = T * G
     off, Vp = rs.pack_kv(put(z, dt), put_mask(m), G, cap)
-    out = rs.attend_causal(put(q, dt), put(k, dt), put_mask(m), off, Vp, put(R, dt), G, out_dtype=out_dtype)
+    out = rs.attend_causal(put(q, dt), put(k, dt), put_mask(m), off, Vp, put(R, dt), G, out_dtype=out_dtype,
+                           scale=0.0 if scale is None else scale)
     torch.cuda.synchronize()
     o_ref, Vp_ref = O.pack(z, m, G, cap)
-    ref = O.attend_packed_causal(q, k, m, o_ref, Vp_ref, R, G)
+    ref = O.attend_packed_causal(q, k, m, o_ref, Vp_ref, R, G, scale=scale)
     return host(out), ref
 
 
@@ -295,6 +297,35 @@ def test_attend_causal(cid, B, T, H, dh, G):
     got, ref = _attend_causal_case(w, B, T, H, dh, G, counts=counts)
     err = max_rel(got, ref)
     _say(f"attend_causal {w.dtype} B={B} T={T} H={H} dh={dh} G={G}: max rel err {err:.2e}")
+    assert err <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("cid,B,T,Tq,H,dh,G,scale", [
+    (2, 2, 177, 56, 8, 128, 8, 0.25),          # matrix cores, a stated positive scale
+    (2, 2, 177, 56, 8, 128, 8, -0.0625),       # negative scale: scores of the opposite sign
+    (5, 2, 90, 20, 4, 128, 32, -0.3),          # 4-dim groups
+    (3, 2, 97, 20, 8, 64, 8, 0.5),             # head dim 64
+    (1, 1, 80, 8, 4, 64, 8, -0.2),             # f32 (vector kernel)
+])
+def test_attend_explicit_scale(cid, B, T, Tq, H, dh, G, scale):
+    w = synth.workload(cid)
+    counts = np.random.default_rng(T + 3).integers(0, G + 1, size=T)
+    got, ref, _ = _attend_case(w, B, T, Tq, H, dh, G, counts=counts, scale=scale)
+    err = max_rel(got, ref)
+    _say(f"attend scale={scale} {w.dtype} B={B} T={T} Tq={Tq} dh={dh} G={G}: max rel err {err:.2e}")
+    assert err <= TOL[w.dtype]
+    # the default (1/sqrt(dh)) gives a different result: the scale is really applied
+    base, _, _ = _attend_case(w, B, T, Tq, H, dh, G, counts=counts)
+    assert max_rel(got, base) > 10 * TOL[w.dtype]
+
+
+@pytest.mark.parametrize("cid,scale", [(2, -0.125), (2, 0.3), (1, -0.4)])
+def test_attend_causal_explicit_scale(cid, scale):
+    w = synth.workload(cid)
+    counts = np.random.default_rng(11).integers(1, 9, size=70)
+    got, ref = _attend_causal_case(w, 2, 70, 4, 128 if cid == 2 else 64, 8, counts=counts, scale=scale)
+    err = max_rel(got, ref)
+    _say(f"attend_causal scale={scale} {w.dtype}: max rel err {err:.2e}")
     assert err <= TOL[w.dtype]
 
 
@@ -461,9 +492,20 @@ def _route_allocate_check(w, B, router, wpri_np, prio_ref, score_ref, label):
     lo_kept = np.where(bits == 1, sc, np.inf).min(-1)
     hi_drop = np.where(bits == 0, sc, -np.inf).max(-1)
     assert np.all(lo_kept >= hi_drop)
+    # bit for bit: the oracle's allocation on the GPU's own float32 priorities
+    # (integer arithmetic after an exact quantisation), then its Top-K_i on the
+    # GPU's own scores, on every token
+    want_k = O.allocate_groups(host(r["priority"]), types, kby, w.G)
+    assert np.array_equal(k, want_k), f"{int(np.sum(k != want_k))} budgets differ"
+    want = O.select_groups(sc, want_k)
+    assert np.array_equal(mask, want)
+    idx, cnt = O.mask_to_idx(want, w.G)
+    assert np.array_equal(host(r["count"]), cnt) and np.array_equal(host(r["idx"]), idx)
+    # end to end: budgets from the oracle's float64 priorities (a last-bit
+    # difference in a priority may move one group, so this is reported)
     agree = float(np.mean(k == O.allocate_groups(prio_ref(h).astype(np.float32), types, kby, w.G)))
     _say(f"route_allocate {label}: priority max rel err {perr:.2e}, scores {serr:.2e}; "
-         f"K equal to the oracle's on {100 * agree:.1f}% of tokens")
+         f"K equal to the oracle's from its own priorities on {100 * agree:.1f}% of tokens")
     assert perr <= 1e-4 and serr <= 1e-4
 
 
@@ -529,6 +571,24 @@ def test_attend_no_groups_is_zero_and_all_groups_is_standard_attention():
 # Router end to end (scores from h)
 # ----------------------------------------------------------------------------
 
+def _exact_selection_on_own_scores(w, types, got_scores, got_mask, got_count=None, got_idx=None, K=None):
+    """The selection the GPU made, bit for bit on every token: the oracle's
+    Top-K_i run on the GPU's own float32 scores (exactly upcast) must give the
+    GPU's masks, counts and kept-group lists. K defaults to the budget rule on
+    those scores (fixed per-type budgets, or the threshold count)."""
+    if K is None:
+        K = O.group_budget(got_scores, types, w.mode, w.k_by_type, w.G, w.tau, w.kmin, w.kmax)
+    want = O.select_groups(got_scores, K)
+    bad = int(np.sum(got_mask != want))
+    assert bad == 0, f"{bad} tokens select other groups than the oracle on the GPU's own scores"
+    if got_count is not None or got_idx is not None:
+        idx, cnt = O.mask_to_idx(want, w.G)
+        if got_count is not None:
+            assert np.array_equal(got_count, cnt)
+        if got_idx is not None:
+            assert np.array_equal(got_idx, idx)
+    return want
+
 def _route_check(w, h, types, router, wt_or_scores_fn, label):
     dt = tdtype(w)
     budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
@@ -548,8 +608,13 @@ def _route_check(w, h, types, router, wt_or_scores_fn, label):
          f"{n_near} near-margin tokens of {safe.size}; mismatches on safe tokens "
          f"{int(np.sum((got != want) & safe))}")
     assert serr <= 1e-4
+    # (i) bit-exact on every token against the oracle's selection on the GPU's scores
+    _exact_selection_on_own_scores(w, types, got_scores, got, host(r["count"]), host(r["idx"]))
+    # (ii) end to end against the oracle's own float64 scores, wherever the margin decides
     assert np.array_equal(got[safe], want[safe])
     assert np.array_equal(host(r["count"])[safe], O.popcount(want)[safe])
+    idx_ref, _ = O.mask_to_idx(want, w.G)
+    assert np.array_equal(host(r["idx"])[safe], idx_ref[safe])
     return r
 
 
@@ -595,6 +660,92 @@ def test_route_additive(dtype):
     _route_check(w, h, types, router, ref, f"additive {dtype}")
 
 
+def _tie_router_weights(w, wt, variant):
+    """Router weights built so that the fused ranking meets exact ties: pairs of
+    identical W2 rows with equal biases give bitwise-equal group scores (every
+    group's sum runs through the same operations), zero rows give zero scores;
+    'nonfinite' adds +inf, -inf and NaN biases. G = 32 (threshold budgets):
+    most groups pushed below the threshold, so many tokens keep one group by
+    the lower clamp and it is chosen among the tied zero groups."""
+    wt = dict(wt)
+    W2, b2 = wt["W2"].astype(np.float32).copy(), wt["b2"].astype(np.float32).copy()
+    if w.G == 8:
+        W2[1], b2[1] = W2[0], b2[0]
+        W2[3], b2[3] = W2[2], b2[2]
+        W2[5], b2[5] = 0.0, -0.0
+        W2[6], b2[6] = 0.0, 0.0
+        if variant == "nonfinite":
+            W2[4], b2[4] = 0.0, np.inf
+            b2[6] = -np.inf
+            b2[7] = np.nan
+    else:
+        b2 = synth.round_to(b2.astype(np.float64) - 4.0, "bf16").astype(np.float32)
+        W2[0:4] = 0.0
+        b2[0:4] = np.array([-0.0, 0.0, -0.0, 0.0], np.float32)
+        for a, c in ((4, 5), (8, 9), (12, 13)):
+            W2[c], b2[c] = W2[a], b2[a]
+    wt["W2"], wt["b2"] = W2, b2
+    return wt
+
+
+def _split_ties(scores, K):
+    """Tokens whose K-th and (K+1)-th highest scores are equal (-0 = +0): the
+    cut runs through a tie, so only the lower-index rule decides."""
+    s = np.where(np.isnan(scores), -np.inf, scores.astype(np.float64))
+    s = np.sort(s, axis=-1)[..., ::-1]
+    G = s.shape[-1]
+    inner = (K > 0) & (K < G)
+    kk = np.clip(K, 1, G - 1)
+    a = np.take_along_axis(s, (kk - 1)[..., None], -1)[..., 0]
+    b = np.take_along_axis(s, kk[..., None], -1)[..., 0]
+    return inner & (a == b)
+
+
+@pytest.mark.parametrize("cid,B,variant", [(3, 4, "ties"), (2, 1, "ties"), (3, 2, "nonfinite"), (5, 2, "ties")])
+def test_route_mlp2_forced_ties(cid, B, variant):
+    w = synth.workload(cid).replace(B=B)
+    wt = _tie_router_weights(w, synth.layer_weights(w, 0), variant)
+    h = np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(B)])
+    types = stack_types(w, B)
+    budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
+    r = rs.route(put_u8(types), budget, w.G, h=put(h, torch.bfloat16), router=router_tensors(wt, torch.bfloat16))
+    torch.cuda.synchronize()
+    got_scores = host(r["scores"])
+    ref = O.router_mlp2(h, types, wt["W_r"], wt["b_r"], wt["E"], wt["W1"], wt["b1"], wt["W2"], wt["b2"])
+    fin = np.isfinite(ref)
+    for f in (np.isnan, np.isposinf, np.isneginf):
+        assert np.array_equal(f(got_scores), f(ref))
+    serr = max_rel(got_scores[fin], ref[fin])
+    assert serr <= 1e-4
+    K = O.group_budget(got_scores, types, w.mode, w.k_by_type, w.G, w.tau, w.kmin, w.kmax)
+    got = host_mask(r["mask"])
+    _exact_selection_on_own_scores(w, types, got_scores, got, host(r["count"]), host(r["idx"]), K=K)
+    split = _split_ties(got_scores, K)
+    if w.G == 8:
+        kept = (got[..., None] >> np.arange(8, dtype=np.uint32)) & 1
+        zero_split = int(np.sum(kept[..., 5] != kept[..., 6])) if variant == "ties" else 0
+        dup_split = int(np.sum((kept[..., 0] != kept[..., 1]) | (kept[..., 2] != kept[..., 3])))
+        _say(f"forced ties workload {cid} {variant}: score err {serr:.1e}; {int(split.sum())} tokens cut "
+             f"through a tie, duplicated pair split on {dup_split}, zero pair split on {zero_split}")
+        assert split.sum() > 0 and dup_split > 0
+        if variant == "ties":
+            assert zero_split > 0
+            # the lower index of a split pair is the kept one
+            assert np.all(kept[..., 1] <= kept[..., 0]) and np.all(kept[..., 3] <= kept[..., 2])
+            assert np.all(kept[..., 6] <= kept[..., 5])
+        else:
+            assert np.all(kept[..., 4] == 1)                                   # +inf always kept
+            vis = types == O.VIS                                               # K = 2: NaN and -inf never kept
+            assert np.all(kept[..., 7][vis] == 0) and np.all(kept[..., 6][vis] == 0)
+    else:
+        one = K == 1
+        n_zero_pick = int(np.sum(one & (host(r["count"]) == 1) & ((got & 0xF) != 0)))
+        _say(f"forced ties workload {cid}: score err {serr:.1e}; {int(one.sum())} tokens keep one group, "
+             f"{n_zero_pick} of them one of the tied zero groups")
+        assert n_zero_pick > 0
+        assert np.all((got[one & ((got & 0xF) != 0)] & 0xF) == 1)             # group 0 of the tied zeros
+
+
 def test_route_sample_without_language_tokens():
     w = synth.workload(3).replace(B=2)
     wt = synth.layer_weights(w, 0)
@@ -634,24 +785,34 @@ def _check_sample(w, layer, b, bufs, wt, cap, scores=None):
                                    wt["W2"], wt["b2"])
     else:
         ref_scores = scores[None]
-    ref = O.pipeline(h, q, k, v, w.types(), wt, w.mode, w.k_by_type, w.G, w.tau, w.kmin, w.kmax,
-                     scores=ref_scores, cap=cap)
+    run = lambda sc: O.pipeline(h, q, k, v, w.types(), wt, w.mode, w.k_by_type, w.G, w.tau, w.kmin, w.kmax,
+                                scores=sc, cap=cap)
+    ref = run(ref_scores)
     got_mask = host_mask(bufs.mask[b:b + 1])
     got_scores = host(bufs.scores[b:b + 1])
+    if scores is not None:
+        assert np.array_equal(got_scores.view(np.uint32), ref_scores.astype(np.float32).view(np.uint32))
+    # (i) the selection on the GPU's own scores, bit for bit on every token
+    _exact_selection_on_own_scores(w, w.types()[None], got_scores, got_mask, host(bufs.count[b:b + 1]),
+                                   host(bufs.idx[b:b + 1]))
+    # (ii) against the oracle's float64 scores wherever the margin decides
     abs_err = float(np.max(np.abs(got_scores - ref_scores)))
     margin = decisive_margin(ref_scores, ref["K"], w.tau if w.mode == O.THRESHOLD else None)
     safe = margin > 8 * abs_err if scores is None else np.ones_like(margin, dtype=bool)
     assert np.array_equal(got_mask[safe], ref["mask"][safe])
     flips = int(np.sum(got_mask != ref["mask"]))
+    if flips:
+        # a near-margin token chose differently: the rest of the path is checked
+        # on the GPU's selection (exact on its scores, asserted above)
+        ref = run(got_scores)
+    assert np.array_equal(host(bufs.offsets[b:b + 1]), ref["offsets"])
+    n = int(ref["offsets"][0, -1])
+    vp_err = max_rel(host(bufs.Vp[b:b + 1, :, :n]), ref["Vp"][:, :, :n]) if n else 0.0
     out_err = max_rel(host(bufs.out[b:b + 1]), ref["out"])
-    vp_err = 0.0
-    if flips == 0:
-        assert np.array_equal(host(bufs.offsets[b:b + 1]), ref["offsets"])
-        n = int(ref["offsets"][0, -1])
-        vp_err = max_rel(host(bufs.Vp[b:b + 1, :, :n]), ref["Vp"][:, :, :n])
     _say(f"  layer {layer} sample {b}: mask flips {flips} (near-margin {int(np.sum(~safe))}), "
          f"packed cache err {vp_err:.2e}, out err {out_err:.2e}")
     assert vp_err <= TOL[w.dtype] and out_err <= TOL[w.dtype]
+    return flips
 
 
 @pytest.mark.parametrize("cid", [1, 2, 3])
@@ -665,14 +826,15 @@ def test_pipeline_small_workloads(cid):
 
 
 @pytest.mark.parametrize("layer", [0, 31])
-def test_pipeline_stack_full_batch_sampled(layer):
-    """The 32-layer, batch-64 workload at full size; the oracle checks sampled prefixes."""
+def test_pipeline_stack_full_batch(layer):
+    """The 32-layer, batch-64 workload at full size in the bench's launch
+    configuration; the oracle checks every prefix of the batch."""
     w = synth.workload(4)
     _say(f"pipeline workload 4 layer {layer}, B={w.B}")
     acts = layer_on_device(w, layer)
     bufs, wt, cap = _run_gpu_layer(w, layer, acts, stack_types(w))
-    for b in (0, 17, 63):
-        _check_sample(w, layer, b, bufs, wt, cap)
+    flips = sum(_check_sample(w, layer, b, bufs, wt, cap) for b in range(w.B))
+    _say(f"workload 4 layer {layer}: {flips} near-margin mask flips over {w.B * w.T} tokens")
     cnt = host(bufs.count)
     assert np.all(cnt[:, :w.n_vis] == w.k_vis) and np.all(cnt[:, w.n_vis:w.n_vis + w.n_lang] == w.k_lang)
     assert np.all(host(bufs.offsets)[:, -1] == cap)
@@ -693,11 +855,17 @@ def test_pipeline_stress_full_batch_sampled():
     acts = layer_on_device(w, 0, need_h=False)
     scores = np.stack([synth.sample_scores(w, 0, b) for b in range(w.B)])
     bufs, wt, cap = _run_gpu_layer(w, 0, acts, stack_types(w), scores_in=put(scores, torch.float32))
-    for b in (0, 77, 127):
-        _check_sample(w, 0, b, bufs, wt, cap, scores=scores[b])
+    # selection and cache offsets of every prefix, bit for bit
     K = O.group_budget(scores, stack_types(w), O.THRESHOLD, w.k_by_type, w.G, 0.0, 1, 32)
+    want = O.select_groups(scores, K)
+    assert np.array_equal(host_mask(bufs.mask), want)
     assert np.array_equal(host(bufs.count).astype(np.int64), K)
-    assert np.array_equal(host(bufs.offsets)[:, -1], K.sum(axis=1))
+    off = np.zeros((w.B, w.T + 1), dtype=np.int64)
+    off[:, 1:] = np.cumsum(K, axis=1)
+    assert np.array_equal(host(bufs.offsets), off)
+    # packed cache and attention on sampled prefixes (the oracle takes ~5 s per prefix)
+    for b in (0, 19, 38, 57, 77, 96, 115, 127):
+        _check_sample(w, 0, b, bufs, wt, cap, scores=scores[b])
 
 
 # ----------------------------------------------------------------------------
