@@ -146,6 +146,31 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype,
                              void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * rolesub_route_noalloc: rolesub_route without a workspace argument, for
+ * callers that cannot allocate device memory (code under stream capture,
+ * serving loops that forbid allocation). Same arguments, results and kernels
+ * as rolesub_route; the route workspace is a file-scope device array of
+ * ROLESUB_ROUTE_NOALLOC_MAX_BYTES that each device holds until the process
+ * ends (its address is looked up once per device, with that device current).
+ * Nothing is allocated or freed, by the library or any routine it calls.
+ *   - Calls whose rolesub_route_workspace_size() exceeds the maximum return
+ *     ROLESUB_ERR_UNSUPPORTED before anything is enqueued (with d = 4096 that
+ *     is about B > 400 samples).
+ *   - stream must belong to the current device (else ROLESUB_ERR_INVALID_ARG).
+ *   - Every call on one device shares that device's array and overwrites it
+ *     (every byte the kernels read is written earlier in the same call, so
+ *     nothing needs clearing): calls that may overlap on one device, e.g. on
+ *     two streams without ordering between them, race and must not be issued.
+ *   - With scores_in the array is not used.
+ * ------------------------------------------------------------------------ */
+#define ROLESUB_ROUTE_NOALLOC_MAX_BYTES (8u << 20)
+rolesub_status rolesub_route_noalloc(const rolesub_dims* dims, rolesub_dtype dtype,
+                                     const rolesub_router* router, const rolesub_budget* budget,
+                                     const void* h, const uint8_t* token_type, const float* scores_in,
+                                     float* scores_out, uint32_t* mask, uint8_t* idx, uint8_t* count,
+                                     void* stream);
+
+/* ---------------------------------------------------------------------------
  * rolesub_pack_kv: the compact group-indexed value cache, i.e. the kept
  * groups of z~ = M z (Sec. 3.2).
  *   offsets[b,i] = sum_{j<i} popcount(mask[b,j] & (2^G-1)); offsets[b,T] = total

@@ -8,5 +8,5 @@ from .rolesub import (  # noqa: F401
     Router, RouterDesc, RolesubError, attend, attend_causal, load, make_budget, pack_kv, rotate_values, route,
     rotate_pack, route_workspace_size, status_name, retain_tokens, gather_tokens, allocate_groups,
     route_allocate, route_allocate_workspace_size, full_workspace_size, full_transpose, full_rotate_pack,
-    full_values, attend_values,
+    full_values, attend_values, route_noalloc, ROUTE_NOALLOC_MAX_BYTES,
 )

@@ -4,12 +4,19 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "launch.hpp"
 #include "rolesub.h"
 
 using namespace rolesub;
+
+// Route workspace of rolesub_route_noalloc, for callers that cannot allocate
+// device memory. Each device holds its own copy for the life of the process.
+// In host code this name is only a stand-in for the symbol: kernels and
+// copies take the device address that hipGetSymbolAddress returns for it.
+__device__ __align__(256) char scratch[ROLESUB_ROUTE_NOALLOC_MAX_BYTES];
 
 namespace {
 
@@ -172,6 +179,39 @@ rolesub_status setup_router(const char* fn, const rolesub_dims* dims, rolesub_dt
   return ROLESUB_OK;
 }
 
+// Device address of the current device's copy of `scratch`, looked up once
+// per device (with that device current) and kept. The caller's stream must
+// belong to the current device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+rolesub_status scratch_on_current_device(const char* fn, hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return from_hip(e, fn);
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(ROLESUB_ERR_UNSUPPORTED, "%s: device %d is beyond the %d supported", fn, dev, kMaxDevices);
+  if (stream) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return from_hip(e, fn);
+    if (sdev != dev)
+      return fail(ROLESUB_ERR_INVALID_ARG, "%s: the stream belongs to device %d, the current device is %d", fn,
+                  static_cast<int>(sdev), dev);
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return from_hip(e, fn);
+    if (!ptr) return fail(ROLESUB_ERR_HIP, "%s: no device address for the scratch array", fn);
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return ROLESUB_OK;
+}
+
 rolesub_status check_alloc(const char* fn, int32_t B, int32_t T, int32_t G, const int32_t* k_by_type) {
   if (B < 0 || T < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: need B >= 0, T >= 0", fn);
   if (G < 1 || G > 32) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: G=%d groups not supported (1..32)", fn, G);
@@ -249,6 +289,66 @@ rolesub_status full_setup(const char* fn, const rolesub_dims* dims, rolesub_dtyp
 
 }  // namespace
 
+namespace {
+
+// rolesub_route and rolesub_route_noalloc: with use_scratch the workspace is
+// this device's `scratch` array (no allocation anywhere on the path).
+rolesub_status route_impl(const char* fn, const rolesub_dims* dims, rolesub_dtype dtype,
+                          const rolesub_router* router, const rolesub_budget* budget, const void* h,
+                          const uint8_t* token_type, const float* scores_in, float* scores_out, uint32_t* mask,
+                          uint8_t* idx, uint8_t* count, void* workspace, size_t ws_bytes, bool use_scratch,
+                          void* stream) {
+  if (!dims) return fail(ROLESUB_ERR_INVALID_ARG, "%s: dims is NULL", fn);
+  if (dims->B < 0 || dims->T < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: need B >= 0, T >= 0", fn);
+  rolesub_status st = check_groups(dims, fn, false);
+  if (st) return st;
+  if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+  st = check_budget(budget, dims->G, fn);
+  if (st) return st;
+  const size_t ntok = static_cast<size_t>(dims->B) * dims->T;
+  if (ntok == 0) return ROLESUB_OK;
+  if (ntok > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
+  if (!mask) return fail(ROLESUB_ERR_INVALID_ARG, "%s: mask must be non-NULL", fn);
+  const bool need_types = budget->mode == ROLESUB_BUDGET_TOPK || scores_in == nullptr;
+  if (need_types && !token_type)
+    return fail(ROLESUB_ERR_INVALID_ARG, "%s: token_type must be non-NULL", fn);
+
+  RouteParams p = {};
+  p.B = dims->B;
+  p.T = dims->T;
+  p.d = dims->d;
+  p.G = dims->G;
+  p.types = token_type;
+  p.mode = budget->mode;
+  for (int t = 0; t < 4; ++t) p.k_by_type[t] = budget->k_by_type[t];
+  p.tau = budget->tau;
+  p.kmin = budget->kmin;
+  p.kmax = budget->kmax;
+  p.scores_in = scores_in;
+  p.scores_out = scores_out;
+  p.mask = mask;
+  p.idx = idx;
+  p.count = count;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (scores_in) return from_hip(launch_select(p, s), fn);
+
+  if (!router) return fail(ROLESUB_ERR_INVALID_ARG, "%s: router is NULL and no scores_in given", fn);
+  if (use_scratch) {
+    const size_t need = route_ws_bytes(dims, router);
+    if (need > ROLESUB_ROUTE_NOALLOC_MAX_BYTES)
+      return fail(ROLESUB_ERR_UNSUPPORTED, "%s: needs %zu bytes of route workspace, above the %zu bytes it holds", fn,
+                  need, static_cast<size_t>(ROLESUB_ROUTE_NOALLOC_MAX_BYTES));
+    st = scratch_on_current_device(fn, s, &workspace);
+    if (st) return st;
+    ws_bytes = ROLESUB_ROUTE_NOALLOC_MAX_BYTES;
+  }
+  st = setup_router(fn, dims, dtype, router, h, workspace, ws_bytes, p);
+  if (st) return st;
+  return from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* rolesub_status_str(rolesub_status s) {
@@ -293,45 +393,16 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype, cons
                              const rolesub_budget* budget, const void* h, const uint8_t* token_type,
                              const float* scores_in, float* scores_out, uint32_t* mask, uint8_t* idx,
                              uint8_t* count, void* workspace, size_t ws_bytes, void* stream) {
-  const char* fn = "rolesub_route";
-  if (!dims) return fail(ROLESUB_ERR_INVALID_ARG, "%s: dims is NULL", fn);
-  if (dims->B < 0 || dims->T < 0) return fail(ROLESUB_ERR_INVALID_ARG, "%s: need B >= 0, T >= 0", fn);
-  rolesub_status st = check_groups(dims, fn, false);
-  if (st) return st;
-  if (!valid_dtype(dtype)) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
-  st = check_budget(budget, dims->G, fn);
-  if (st) return st;
-  const size_t ntok = static_cast<size_t>(dims->B) * dims->T;
-  if (ntok == 0) return ROLESUB_OK;
-  if (ntok > 0x7FFFFFFF) return fail(ROLESUB_ERR_UNSUPPORTED, "%s: B*T too large", fn);
-  if (!mask) return fail(ROLESUB_ERR_INVALID_ARG, "%s: mask must be non-NULL", fn);
-  const bool need_types = budget->mode == ROLESUB_BUDGET_TOPK || scores_in == nullptr;
-  if (need_types && !token_type)
-    return fail(ROLESUB_ERR_INVALID_ARG, "%s: token_type must be non-NULL", fn);
+  return route_impl("rolesub_route", dims, dtype, router, budget, h, token_type, scores_in, scores_out, mask, idx,
+                    count, workspace, ws_bytes, false, stream);
+}
 
-  RouteParams p = {};
-  p.B = dims->B;
-  p.T = dims->T;
-  p.d = dims->d;
-  p.G = dims->G;
-  p.types = token_type;
-  p.mode = budget->mode;
-  for (int t = 0; t < 4; ++t) p.k_by_type[t] = budget->k_by_type[t];
-  p.tau = budget->tau;
-  p.kmin = budget->kmin;
-  p.kmax = budget->kmax;
-  p.scores_in = scores_in;
-  p.scores_out = scores_out;
-  p.mask = mask;
-  p.idx = idx;
-  p.count = count;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (scores_in) return from_hip(launch_select(p, s), fn);
-
-  if (!router) return fail(ROLESUB_ERR_INVALID_ARG, "%s: router is NULL and no scores_in given", fn);
-  st = setup_router(fn, dims, dtype, router, h, workspace, ws_bytes, p);
-  if (st) return st;
-  return from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
+rolesub_status rolesub_route_noalloc(const rolesub_dims* dims, rolesub_dtype dtype, const rolesub_router* router,
+                                     const rolesub_budget* budget, const void* h, const uint8_t* token_type,
+                                     const float* scores_in, float* scores_out, uint32_t* mask, uint8_t* idx,
+                                     uint8_t* count, void* stream) {
+  return route_impl("rolesub_route_noalloc", dims, dtype, router, budget, h, token_type, scores_in, scores_out,
+                    mask, idx, count, nullptr, 0, true, stream);
 }
 
 rolesub_status rolesub_allocate_groups(int32_t B, int32_t T, int32_t G, const int32_t* k_by_type,

@@ -27,8 +27,9 @@ EXPORTS = (
     "rolesub_attend_causal", "rolesub_retain_tokens", "rolesub_gather_tokens",
     "rolesub_allocate_groups", "rolesub_route_allocate_workspace_size", "rolesub_route_allocate",
     "rolesub_full_workspace_size", "rolesub_full_transpose", "rolesub_full_rotate_pack", "rolesub_full_values",
-    "rolesub_attend_values",
+    "rolesub_attend_values", "rolesub_route_noalloc",
 )
+ROUTE_NOALLOC_MAX_BYTES = 8 << 20
 
 
 class RolesubError(RuntimeError):
@@ -76,6 +77,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rolesub_route_workspace_size.argtypes = [P, P]
     lib.rolesub_route_workspace_size.restype = SZ
     lib.rolesub_route.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.rolesub_route_noalloc.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P]
     lib.rolesub_pack_kv.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, I64, P]
     lib.rolesub_rotate_pack.argtypes = [P, ctypes.c_int, P, P, P, P, P, P, P, I64, P]
     lib.rolesub_attend_workspace_size.argtypes = [P, I32]
@@ -95,8 +97,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rolesub_full_rotate_pack.argtypes = [P, ctypes.c_int, P, P, P, P, P, I64, P, P, P, SZ, P]
     lib.rolesub_full_values.argtypes = [P, ctypes.c_int, P, P, P, P, I64, P, P, SZ, P]
     lib.rolesub_attend_values.argtypes = [P, ctypes.c_int, I32, P, P, P, ctypes.c_float, P, ctypes.c_int, P]
-    for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_pack_kv", "rolesub_rotate_pack",
-               "rolesub_attend"):
+    for fn in ("rolesub_rotate_values", "rolesub_route", "rolesub_route_noalloc", "rolesub_pack_kv",
+               "rolesub_rotate_pack", "rolesub_attend"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -293,6 +295,35 @@ def route(token_type: torch.Tensor, budget: Budget, G: int, h: torch.Tensor | No
         _ptr(h), _ptr(token_type, torch.uint8), _ptr(scores_in, torch.float32), _ptr(sco),
         _ptr(mask), _ptr(idx), _ptr(cnt), ws_ptr, ws_bytes, _stream(stream)))
     return {"mask": mask, "idx": idx, "count": cnt, "scores": sco}
+
+
+def route_noalloc(token_type: torch.Tensor, budget: Budget, G: int, h: torch.Tensor | None = None,
+                  router: Router | None = None, scores_in: torch.Tensor | None = None, *, out, stream=None):
+    """rolesub_route with the library's own fixed device scratch as workspace:
+    the call allocates nothing. Every output buffer comes from the caller
+    (out: dict with mask [B,T] int32 and optionally idx, count, scores)."""
+    _need("token_type", token_type, (None, None), torch.uint8)
+    B, T = token_type.shape
+    _need("h", h, (B, T, None), (torch.float32, torch.bfloat16))
+    d = 0 if h is None else h.shape[2]
+    dtype = torch.float32 if h is None else h.dtype
+    _need("scores_in", scores_in, (B, T, G), torch.float32)
+    if router is not None and h is not None:
+        router.check(d, G, dtype)
+    if "mask" not in out:
+        raise ValueError("out['mask'] is required")
+    for name, shape, dt in (("mask", (B, T), _MASK), ("idx", (B, T, G), torch.uint8),
+                            ("count", (B, T), torch.uint8), ("scores", (B, T, G), torch.float32)):
+        _need(f"out[{name!r}]", out.get(name), shape, dt)
+    _same_device(token_type, h, scores_in, *out.values())
+    dims = Dims(B, T, 1, 64, G, d)
+    desc = router.desc() if router is not None else None
+    _check("rolesub_route_noalloc", load().rolesub_route_noalloc(
+        ctypes.byref(dims), F32 if dtype == torch.float32 else BF16,
+        ctypes.byref(desc) if desc is not None else None, ctypes.byref(budget),
+        _ptr(h), _ptr(token_type, torch.uint8), _ptr(scores_in, torch.float32), _ptr(out.get("scores")),
+        _ptr(out["mask"]), _ptr(out.get("idx")), _ptr(out.get("count")), _stream(stream)))
+    return out
 
 
 def pack_kv(z: torch.Tensor, mask: torch.Tensor, G: int, cap: int, budget: Budget | None = None,

@@ -64,6 +64,30 @@ def test_rotate_validation(lib):
     assert lib.rolesub_rotate_values(ctypes.byref(d0), rs.BF16, None, None, None, None) == 0
 
 
+def test_route_noalloc_validation(lib):
+    """The no-alloc route call validates like rolesub_route and refuses a
+    route workspace beyond its fixed device array before any device call."""
+    d = _dims(G=8)
+    bad_k = rs.make_budget(rs.TOPK, (9, 1, 8, 8))
+    assert lib.rolesub_route_noalloc(ctypes.byref(d), rs.BF16, None, ctypes.byref(bad_k), FAKE, FAKE, FAKE,
+                                     None, FAKE, None, None, None) == 1
+    assert "rolesub_route_noalloc" in _last() and "k_by_type" in _last()
+    ok = rs.make_budget(rs.TOPK, (4, 6, 8, 8))
+    assert lib.rolesub_route_noalloc(None, rs.BF16, None, ctypes.byref(ok), FAKE, FAKE, FAKE,
+                                     None, FAKE, None, None, None) == 1
+    assert lib.rolesub_route_noalloc(ctypes.byref(d), rs.BF16, None, ctypes.byref(ok), FAKE, FAKE, None,
+                                     None, FAKE, None, None, None) == 1                 # no router, no scores
+    big = _dims(B=600, T=1, G=8, d=4096)
+    desc = rs.RouterDesc()
+    desc.kind, desc.C, desc.d_e, desc.Hr = rs.MLP2, 8, 128, 128
+    for n in ("W_r", "b_r", "E", "W1", "b1", "W2", "b2"):
+        setattr(desc, n, 0x1000)
+    assert lib.rolesub_route_workspace_size(ctypes.byref(big), ctypes.byref(desc)) > rs.ROUTE_NOALLOC_MAX_BYTES
+    assert lib.rolesub_route_noalloc(ctypes.byref(big), rs.BF16, ctypes.byref(desc), ctypes.byref(ok), FAKE, FAKE,
+                                     None, None, FAKE, None, None, None) == 2
+    assert "above the" in _last()
+
+
 def test_route_validation(lib):
     d = _dims(G=8)
     bad_k = rs.make_budget(rs.TOPK, (9, 1, 8, 8))
