@@ -154,8 +154,8 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype,
  * ends (its address is looked up once per device, with that device current).
  * Nothing is allocated or freed, by the library or any routine it calls.
  *   - Calls whose rolesub_route_workspace_size() exceeds the maximum return
- *     ROLESUB_ERR_UNSUPPORTED before anything is enqueued (with d = 4096 that
- *     is about B > 400 samples).
+ *     ROLESUB_ERR_UNSUPPORTED before anything is enqueued (with d = 4096 and
+ *     Hr = 128: more than 333 samples).
  *   - stream must belong to the current device (else ROLESUB_ERR_INVALID_ARG).
  *   - Every call on one device shares that device's array and overwrites it
  *     (every byte the kernels read is written earlier in the same call, so
