@@ -47,28 +47,73 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_hbm_traffic.json")
 
 
-def attend_bytes(w, sum_k: int, out_esize: int) -> int:
+def attend_bytes(w, sum_k: int, out_esize: int, total_k: int | None = None) -> int:
     """Algorithmic HBM bytes of one attention call: q, k, packed values,
-    mask + offsets, output, rotations (everything read or written once)."""
+    mask + offsets, output, rotations (everything read or written once).
+    sum_k: kept groups per sample; total_k (if given): over the whole batch."""
     e = 2 if w.dtype == "bf16" else 4
-    per = (w.Tq * w.H * w.dh * e + w.T * w.H * w.dh * e + sum_k * w.ds * w.H * e + 8 * w.T
-           + w.Tq * w.H * w.dh * out_esize)
-    return w.B * per + w.H * w.dh * w.dh * e
+    tot = w.B * sum_k if total_k is None else total_k
+    per = (w.Tq * w.H * w.dh * e + w.T * w.H * w.dh * e + 8 * w.T + w.Tq * w.H * w.dh * out_esize)
+    return w.B * per + tot * w.ds * w.H * e + w.H * w.dh * w.dh * e
 
 
-def stage_bytes(w, sum_k: int) -> dict:
+def stage_bytes(w, sum_k: int, total_k: int | None = None) -> dict:
     """Algorithmic HBM bytes per layer call of each stage as the step runs
     them (rotation and pack fused: v read once, only kept groups written)."""
     e = 2 if w.dtype == "bf16" else 4
+    tot = w.B * sum_k if total_k is None else total_k
     route_w = (w.Hr * w.router_in + w.C * w.d + w.G * w.Hr + w.C * w.d_e) * e
     # with given logits the selection reads them instead of running the router
     route_in = 4 * w.B * w.T * w.G if w.scores_in else w.B * w.T * w.d * e + route_w
     return {
         "route": route_in + 4 * w.B * w.T * (w.G + 2),
         "rotate_pack": w.B * w.T * w.H * w.dh * e + w.H * w.dh * w.dh * e
-                       + w.B * sum_k * w.ds * w.H * e + 8 * w.B * w.T,
-        "attend": attend_bytes(w, sum_k, e),
+                       + tot * w.ds * w.H * e + 8 * w.B * w.T,
+        "attend": attend_bytes(w, sum_k, e, total_k),
     }
+
+
+def dist(xs) -> dict:
+    """median and 10th / 90th percentiles of a list of timings."""
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median": float(np.median(a)), "p10": float(np.percentile(a, 10)),
+            "p90": float(np.percentile(a, 90)), "n": int(a.size)}
+
+
+def timed_replays(fn, reps: int, per: int = 1) -> list:
+    """HIP events on the current stream around each of `reps` calls of fn;
+    returns the time per unit (fn does `per` units) of each call, in us."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    fn()
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(reps):
+        fn()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    return [ev[i].elapsed_time(ev[i + 1]) * 1e3 / per for i in range(reps)]
+
+
+def copy_rate(nbytes: int = 1 << 30, reps: int = 20) -> dict:
+    """A plain device-to-device copy of nbytes (read + written once), the
+    achievable streaming rate on this GPU in the same run."""
+    import torch
+    src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    us = timed_replays(lambda: dst.copy_(src), reps)
+    gbs = [2 * nbytes / (u * 1e-6) / 1e9 for u in us]
+    del src, dst
+    return {"bytes_read": nbytes, "bytes_written": nbytes, "GBs": dist(gbs), "kernel": "torch copy_ (HIP)"}
+
+
+def _blas_threads() -> int:
+    from threadpoolctl import threadpool_info
+    return max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+
+
+def _cores() -> dict:
+    return {"nproc": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
 
 
 def _source_hash() -> str:
@@ -94,10 +139,12 @@ def cpu_baseline(w, budget_s: float = 12.0, allocation: bool = False) -> dict:
     and further layers while the time budget lasts."""
     import oracle as O
     import synth
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_limits
 
+    cores = _cores()
     cap = sum(n * min(k, w.G) for n, k in zip(w.type_counts(), w.k_by_type))
     done, spent, layer = 0, 0.0, 0
+    lim = threadpool_limits(limits=cores["affinity"], user_api="blas")
     while spent < budget_s and layer < w.L:
         wt = synth.layer_weights(w, layer)
         wpri = synth.priority_weights(w, layer) if allocation else None
@@ -111,13 +158,42 @@ def cpu_baseline(w, budget_s: float = 12.0, allocation: bool = False) -> dict:
             done += 1
             b += 1
         layer += 1
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": done * w.Tq / spent, "unit": "query-tokens/s", "cores": int(threads),
-            "kind": "oracle",
+    threads = _blas_threads()
+    lim.restore_original_limits()
+    single = {} if allocation else cpu_single_thread()
+    return {"value": done * w.Tq / spent, "unit": "query-tokens/s", "cores": int(min(threads, cores["affinity"])),
+            "kind": "oracle", "nproc": cores["nproc"], "affinity_cores": cores["affinity"], "blas_threads": threads,
             "sample": f"{done} (layer, prefix) pairs, layers 0..{layer - 1} of {w.L} with {w.B} prefixes "
                       f"each (the last layer possibly partial): route->"
                       f"{'allocate->' if allocation else ''}rotate->pack->attend in float64 "
-                      f"({spent:.1f} s); BLAS pool {threads} threads, Python loops on one core"}
+                      f"({spent:.1f} s); BLAS pool {threads} threads, Python loops on one core",
+            "single_thread": single}
+
+
+def cpu_single_thread(budget_s: float = 3.0) -> dict:
+    """The oracle's whole layer on the tiny f32 and the one-layer 7B workloads
+    with one BLAS thread (query tokens per second)."""
+    import oracle as O
+    import synth
+    from threadpoolctl import threadpool_limits
+
+    out = {}
+    with threadpool_limits(limits=1, user_api="blas"):
+        for cid in (1, 2):
+            w = synth.workload(cid)
+            wt = synth.layer_weights(w, 0)
+            cap = sum(n * min(k, w.G) for n, k in zip(w.type_counts(), w.k_by_type))
+            a = synth.sample_activations(w, 0, 0)
+            done, spent = 0, 0.0
+            while spent < budget_s or done == 0:
+                t0 = time.perf_counter()
+                O.pipeline(a["h"][None], a["q"][None], a["k"][None], a["v"][None], w.types(), wt, w.mode,
+                           w.k_by_type, w.G, w.tau, w.kmin, w.kmax, cap=cap)
+                spent += time.perf_counter() - t0
+                done += 1
+            out[w.name] = {"value": done * w.Tq / spent, "unit": "query-tokens/s", "calls": done,
+                           "seconds": round(spent, 2)}
+    return out
 
 
 def causal_flops(w) -> float:
@@ -325,6 +401,149 @@ def full_width(args, w):
     print(json.dumps(line), flush=True)
 
 
+def _graph(fn):
+    """fn's launches captured once into a HIP graph; returns its replay."""
+    import torch
+    stream = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        fn()
+    return g.replay
+
+
+def stress_stages(reps: int = 50) -> dict:
+    """The G = 32 stress workload at full size (128 prefixes x 2048 tokens,
+    64 queries, 4-dim groups, threshold budgets on given logits): selection,
+    rotate + pack and attention, each captured in a graph and replayed
+    `reps` times with an event around every replay."""
+    import torch
+
+    import paper_2608_18410_amd as rs
+    import synth
+    from paper_2608_18410_amd.pipeline import pack_capacity
+
+    w = synth.workload(5)
+    dev, dt = torch.device("cuda:0"), torch.bfloat16
+    g = torch.Generator(device=dev)
+    g.manual_seed(w.seed)
+    q = torch.randn((w.B, w.Tq, w.H, w.dh), generator=g, device=dev, dtype=dt)
+    k = torch.randn((w.B, w.T, w.H, w.dh), generator=g, device=dev, dtype=dt)
+    v = torch.randn((w.B, w.T, w.H, w.dh), generator=g, device=dev, dtype=dt)
+    R = torch.from_numpy(synth.layer_weights(w, 0)["R"]).to(dev).to(dt)
+    scores = torch.from_numpy(np.stack([synth.sample_scores(w, 0, b) for b in range(w.B)])).to(dev)
+    types = torch.from_numpy(np.broadcast_to(w.types(), (w.B, w.T)).copy()).to(dev)
+    budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
+    cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
+    sel = {"mask": torch.empty((w.B, w.T), dtype=torch.int32, device=dev),
+           "idx": torch.empty((w.B, w.T, w.G), dtype=torch.uint8, device=dev),
+           "count": torch.empty((w.B, w.T), dtype=torch.uint8, device=dev),
+           "scores": torch.empty((w.B, w.T, w.G), dtype=torch.float32, device=dev)}
+    offsets = torch.empty((w.B, w.T + 1), dtype=torch.int32, device=dev)
+    Vp = torch.empty((w.B, w.H, cap, w.ds), dtype=dt, device=dev)
+    out = torch.empty((w.B, w.Tq, w.H, w.dh), dtype=dt, device=dev)
+    f_sel = lambda: rs.route(types, budget, w.G, scores_in=scores, out=sel)
+    f_rp = lambda: rs.rotate_pack(v, R, sel["mask"], w.G, cap, out=(offsets, Vp))
+    f_att = lambda: rs.attend(q, k, sel["mask"], offsets, Vp, R, w.G, out=out)
+
+    def f_step():
+        f_sel()
+        f_rp()
+        f_att()
+
+    f_step()
+    torch.cuda.synchronize()
+    total_k = int(offsets[:, -1].sum().item())
+    by = stage_bytes(w, total_k // w.B, total_k)
+    res = {"workload": w.name, "prefixes": w.B, "kv_tokens": w.T, "queries": w.Tq, "groups": w.G,
+           "kept_groups_per_prefix": total_k / w.B, "inputs": "device-seeded Gaussian q, k, v; seeded logits"}
+    for name, fn, key in (("select", f_sel, "route"), ("rotate_pack", f_rp, "rotate_pack"),
+                          ("attend", f_att, "attend"), ("step", f_step, None)):
+        us = timed_replays(_graph(fn), reps)
+        mean = float(np.mean(us))
+        r = {"us": dist(us), "avg_us": mean}
+        nb = sum(by.values()) if key is None else by[key]
+        gbs = nb / (mean * 1e-6) / 1e9
+        r.update({"algorithmic_bytes": nb, "GBs": gbs, "frac_of_peak": gbs / HBM_PEAK_GBS})
+        res[name] = r
+    res["attend_query_tokens_per_s"] = w.B * w.Tq / (res["attend"]["avg_us"] * 1e-6)
+    del q, k, v, Vp
+    torch.cuda.empty_cache()
+    return res
+
+
+def small_layer_calls(cid: int, min_bytes: float = 1.1e9, reps: int = 50) -> dict:
+    """One 7B-shape layer call (route -> rotate + pack -> attend) of a small
+    workload, per call: cold, cycling through enough distinct copies of every
+    input (own activations, router weights and rotations) that together exceed
+    the 256 MB memory-side cache, and hot (attention repeated on one copy)."""
+    import torch
+
+    import paper_2608_18410_amd as rs
+    import synth
+    from paper_2608_18410_amd.pipeline import LayerBuffers, pack_capacity, run_layer
+
+    w = synth.workload(cid)
+    dev, dt = torch.device("cuda:0"), torch.bfloat16
+    g = torch.Generator(device=dev)
+    g.manual_seed(100 + cid)
+    rnd = lambda shape, std=1.0: (torch.randn(shape, generator=g, device=dev, dtype=torch.float32) * std).to(dt)
+    budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
+    cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
+    types = torch.from_numpy(np.broadcast_to(w.types(), (w.B, w.T)).copy()).to(dev)
+    fin = w.router_in
+    per_copy = 2 * (w.B * w.T * (w.d + 2 * w.H * w.dh) + w.B * w.Tq * w.H * w.dh + w.Hr * fin + w.H * w.dh * w.dh)
+    n = max(8, int(np.ceil(min_bytes / per_copy)))
+    copies = []
+    for _ in range(n):
+        router = rs.Router.mlp2(rnd((w.C, w.d), w.d ** -0.5), rnd((w.C,), w.d ** -0.5), rnd((w.C, w.d_e)),
+                                rnd((w.Hr, fin), fin ** -0.5), rnd((w.Hr,), fin ** -0.5),
+                                rnd((w.G, w.Hr), w.Hr ** -0.5), rnd((w.G,), w.Hr ** -0.5))
+        bufs = LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, dt, device=dev, with_z=False,
+                                     ws_bytes=rs.route_workspace_size(w.B, w.T, w.G, w.d, router))
+        copies.append(dict(h=rnd((w.B, w.T, w.d)), q=rnd((w.B, w.Tq, w.H, w.dh)), k=rnd((w.B, w.T, w.H, w.dh)),
+                           v=rnd((w.B, w.T, w.H, w.dh)), R=rnd((w.H, w.dh, w.dh), w.dh ** -0.5), router=router,
+                           bufs=bufs))
+
+    def layer(c):
+        run_layer(c["h"], c["q"], c["k"], c["v"], types, c["R"], budget, w.G, c["bufs"], router=c["router"],
+                  type_counts=w.type_counts(), fused=True)
+
+    def att(c):
+        b = c["bufs"]
+        rs.attend(c["q"], c["k"], b.mask, b.offsets, b.Vp, c["R"], w.G, out=b.out)
+
+    for c in copies:
+        layer(c)
+    torch.cuda.synchronize()
+    total_k = int(copies[0]["bufs"].offsets[:, -1].sum().item())
+    by = stage_bytes(w, total_k // w.B, total_k)
+    res = {"workload": w.name, "prefixes": w.B, "kv_tokens": w.T, "copies_cycled": n,
+           "bytes_cycled": n * per_copy, "inputs": "device-seeded Gaussian activations and weights"}
+    for name, fn in (("layer_cold", lambda: [layer(c) for c in copies]),
+                     ("attend_cold", lambda: [att(c) for c in copies]),
+                     ("attend_hot", lambda: [att(copies[0]) for _ in copies])):
+        us = timed_replays(_graph(fn), reps, per=n)
+        mean = float(np.mean(us))
+        nb = sum(by.values()) if name == "layer_cold" else by["attend"]
+        gbs = nb / (mean * 1e-6) / 1e9
+        res[name] = {"us_per_call": dist(us), "avg_us": mean, "algorithmic_bytes": nb, "GBs": gbs,
+                     "frac_of_peak": gbs / HBM_PEAK_GBS}
+    res["note"] = ("latency-bound: a call moves a few MB (tens of MB at batch 16); hot = inputs resident in the "
+                   "memory-side cache")
+    del copies
+    torch.cuda.empty_cache()
+    return res
+
+
+def other_workloads(args) -> dict:
+    """The stress workload's stages and the small workloads' per-call times."""
+    import synth
+    out = {synth.workload(5).name: stress_stages()}
+    for cid in (2, 3):
+        out[synth.workload(cid).name] = small_layer_calls(cid)
+    return {"other_workloads": out}
+
+
 def prefix_attention(args, w):
     """Prefix self-attention (rolesub_attend_causal) at the 7B-stack layer shape:
     every prefix token is a query and sees the keys before it; masks carry the
@@ -509,6 +728,8 @@ def main():
     ap.add_argument("--workload", type=int, default=4, help="workload id (4: 32-layer 7B stack)")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the other workloads (G = 32 stress, one-layer and batch-16 shapes) after the step")
     ap.add_argument("--eager", action="store_true", help="issue the calls directly, no HIP graphs")
     ap.add_argument("--prefix-attention", action="store_true",
                     help="time prefix self-attention (rolesub_attend_causal) at the same shape instead")
@@ -656,33 +877,30 @@ def main():
     if not torch.equal(layers[-1]["bufs"].out, eager_out):
         raise RuntimeError("graph replay output differs from the eager pass")
 
-    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # K timed steps back to back, an event after each (the mean is the
+    # reported step time; the spread comes from the same events)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    t_start.record()
-    for _ in range(args.steps):
+    ev[0].record()
+    for i in range(args.steps):
         step()
-    t_end.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    ms_step = t_start.elapsed_time(t_end) / args.steps
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms_step = ev[0].elapsed_time(ev[-1]) / args.steps
 
-    # Attention kernel duration: HIP events on the launch stream around
-    # back-to-back replays of the attention calls of every layer (same inputs
-    # as the last step), divided by the number of launches; this includes the
-    # short dispatch gaps between consecutive kernels of one graph.
-    reps = max(2, args.steps // 4)
-    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    att_all()
-    torch.cuda.synchronize()
-    a0.record()
-    for _ in range(reps):
-        att_all()
-    a1.record()
-    torch.cuda.synchronize()
-    att_ms = a0.elapsed_time(a1) / (reps * len(layers))
+    # Attention kernel duration: HIP events on the launch stream around each
+    # of >= 50 back-to-back replays of the attention calls of every layer
+    # (same inputs as the last step), divided by the number of launches; this
+    # includes the short dispatch gaps between consecutive kernels of one graph.
+    reps = max(50, args.steps)
+    att_us = timed_replays(att_all, reps, per=len(layers))
+    att_ms = float(np.mean(att_us)) / 1e3
     if not torch.equal(layers[-1]["bufs"].out, eager_out):
         raise RuntimeError("attention replay output differs from the eager pass")
 
     alloc_us = None
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     if args.allocation:
         # the allocation + selection kernel alone: the same call on the step's
         # own priorities and scores (it rewrites identical budgets and masks)
@@ -707,8 +925,9 @@ def main():
         torch.cuda.synchronize()
         alloc_us = a0.elapsed_time(a1) / (reps * len(layers)) * 1e3
 
-    sum_k = int(layers[0]["bufs"].offsets[:, -1].sum().item()) // w.B
-    per_stage = stage_bytes(w, sum_k)
+    total_k = int(layers[0]["bufs"].offsets[:, -1].sum().item())
+    sum_k = total_k // w.B
+    per_stage = stage_bytes(w, sum_k, total_k)
     if args.allocation:
         # over the fixed-budget route: scores read again, priorities written
         # and read, token types and the budgets K_i
@@ -716,6 +935,11 @@ def main():
     a_bytes = per_stage["attend"]
     achieved = a_bytes / (att_ms * 1e-3) / 1e9
     value = w.B * w.Tq * w.L / (ms_step * 1e-3)
+    extra = {}
+    if not args.no_extra and not args.allocation and w.name == synth.workload(4).name:
+        extra = other_workloads(args)
+    copy = copy_rate()
+    copy_gbs = copy["GBs"]["median"]
 
     line = {
         "metric": ALLOC_METRIC if args.allocation else METRIC,
@@ -743,12 +967,17 @@ def main():
         "roofline": {"kernel": "rolesub_attend (k_attend_bf16)", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": _traffic(w.name),
-                     "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": att_ms * 1e3},
-        "detail": {"attend_query_tokens_per_s": w.B * w.Tq / (att_ms * 1e-3),
+                     "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": att_ms * 1e3,
+                     "launch_us": dist(att_us), "copy_GBs_same_run": copy_gbs,
+                     "frac_of_copy": achieved / copy_gbs},
+        "detail": {"step_ms": dist(step_ms),
+                   "copy": copy,
+                   "attend_query_tokens_per_s": w.B * w.Tq / (att_ms * 1e-3),
                    "layers_per_s": w.L / (ms_step * 1e-3),
                    "allocate_select_us_per_layer": alloc_us,
                    "stage_algorithmic_bytes": per_stage,
-                   "step_algorithmic_GBs": w.L * sum(per_stage.values()) / (ms_step * 1e-3) / 1e9},
+                   "step_algorithmic_GBs": w.L * sum(per_stage.values()) / (ms_step * 1e-3) / 1e9,
+                   **extra},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, allocation=args.allocation)

@@ -149,6 +149,53 @@ __device__ __forceinline__ int budget_k(int mode, const int* k_by_type, int type
   return k < G ? k : G;
 }
 
+// Pairwise combination with the lane 16 (or 32) positions away, i.e.
+// x op (x of lane l ^ 16): v_permlane16_swap / v_permlane32_swap exchange the
+// 16-lane rows (32-lane halves) of two copies of x in one VALU instruction,
+// leaving each lane with {x, partner} in some order; op is commutative, so the
+// result is bitwise that of the operands in either order (a cross-lane
+// shuffle goes through the LDS crossbar and costs an LDS round trip).
+__device__ __forceinline__ void swap16(uint32_t x, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  a = r[0];
+  b = r[1];
+}
+__device__ __forceinline__ void swap32(uint32_t x, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  a = r[0];
+  b = r[1];
+}
+__device__ __forceinline__ float add_xor16(float x) {
+  uint32_t a, b;
+  swap16(__float_as_uint(x), a, b);
+  return __uint_as_float(a) + __uint_as_float(b);
+}
+__device__ __forceinline__ float add_xor32(float x) {
+  uint32_t a, b;
+  swap32(__float_as_uint(x), a, b);
+  return __uint_as_float(a) + __uint_as_float(b);
+}
+__device__ __forceinline__ float max_xor16(float x) {
+  uint32_t a, b;
+  swap16(__float_as_uint(x), a, b);
+  return fmaxf(__uint_as_float(a), __uint_as_float(b));
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  uint32_t a, b;
+  swap32(__float_as_uint(x), a, b);
+  return fmaxf(__uint_as_float(a), __uint_as_float(b));
+}
+__device__ __forceinline__ uint32_t or_xor16(uint32_t x) {
+  uint32_t a, b;
+  swap16(x, a, b);
+  return a | b;
+}
+__device__ __forceinline__ uint32_t or_xor32(uint32_t x) {
+  uint32_t a, b;
+  swap32(x, a, b);
+  return a | b;
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, kWave);

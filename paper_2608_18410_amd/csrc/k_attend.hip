@@ -362,8 +362,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
           mx = fmaxf(mx, s[m2][i]);
         }
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    mx = max_xor32(max_xor16(mx));
     const float m_cand = fmaxf(m_run, mx * sl2);  // sl2 >= 0
     if (__builtin_amdgcn_ballot_w64(m_cand > m_run + kSlack) != 0) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_cand);  // 0 on the first tile
@@ -422,8 +421,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
   wait_vmcnt<0>();
   __syncthreads();
   // ---- normalise and rotate back: O^T = R_h U^T
-  float lsum = l_run + __shfl_xor(l_run, 16, kWave);
-  lsum += __shfl_xor(lsum, 32, kWave);
+  const float lsum = add_xor32(add_xor16(l_run));
   const float inv = 1.f / lsum;
   bf16x8 ub[KS];
 #pragma unroll

@@ -760,8 +760,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
     ex[i] = c < C ? lg : -INFINITY;
     mx = fmaxf(mx, ex[i]);
   }
-  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  mx = max_xor32(max_xor16(mx));
   float sm = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -769,8 +768,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
     ex[i] = (4 * g4 + i < C) ? e : 0.f;
     sm += ex[i];
   }
-  sm += __shfl_xor(sm, 16, kWave);
-  sm += __shfl_xor(sm, 32, kWave);
+  sm = add_xor32(add_xor16(sm));
   const float isum = 1.f / sm;
   float a[16];  // role mixture weights; zero past C
 #pragma unroll
@@ -827,8 +825,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
   int n_above = 0;
 #pragma unroll
   for (int s = 0; s < GP; ++s) {
-    gam[s] += __shfl_xor(gam[s], 16, kWave);
-    gam[s] += __shfl_xor(gam[s], 32, kWave);
+    gam[s] = add_xor32(add_xor16(gam[s]));
     gam[s] += b2s[s];
     n_above += static_cast<int>((s < G) & (gam[s] > p.tau));
   }
@@ -862,8 +859,7 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
         rank += static_cast<int>((t < G) & (key_above(gam[t], mine[u]) | ((t < s) & key_equal(gam[t], mine[u]))));
       msk |= static_cast<uint32_t>((s < G) & (rank < K)) << s;
     }
-    msk |= __shfl_xor(msk, 16, kWave);
-    msk |= __shfl_xor(msk, 32, kWave);
+    msk = or_xor32(or_xor16(msk));
   }
   if (valid) {
     if (p.scores_out) {
