@@ -41,9 +41,9 @@ __global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
   __shared__ float s_part[4][64 * VEC];
   const int ncb = (p.d + 64 * VEC - 1) / (64 * VEC);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  if (PCB && blockIdx.x >= static_cast<unsigned>(p.B * ncb)) {
-    // F[j][c] = W1[j, d : d+d_e] . E[c]; d_e a multiple of 8, rows 16-byte aligned
-    const int e = (blockIdx.x - p.B * ncb) * 256 + tid;
+  // F[j][c] = W1[j, d : d+d_e] . E[c] (entry e = j*C + c); d_e a multiple of
+  // 8, rows 16-byte aligned
+  auto fold_F = [&](int e) {
     const int j = e / p.C, c = e - j * p.C;
     const bool ok = j < p.Hr;
     const uint32_t W1s = 2u * p.d + p.d_e;
@@ -52,17 +52,18 @@ __global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
     const uint32_t ow = (static_cast<uint32_t>(j) * W1s + p.d) * sizeof(T);
     const uint32_t oe = static_cast<uint32_t>(c * p.d_e) * sizeof(T);
     float acc = 0.f;
-    for (int m0 = 0; m0 < p.d_e; m0 += 8 * VEC) {
-      u32x4 wv[8], ev[8];
+    // 16 loads of each operand in flight: one round trip for d_e <= 16*VEC
+    for (int m0 = 0; m0 < p.d_e; m0 += 16 * VEC) {
+      u32x4 wv[16], ev[16];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 16; ++u) {
         const bool in = ok && m0 + u * VEC < p.d_e;
         const uint32_t m = static_cast<uint32_t>(m0 + u * VEC) * sizeof(T);
         wv[u] = bload16(r_w, oob_unless(in, ow + m));
         ev[u] = bload16(r_e, oob_unless(in, oe + m));
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 16; ++u) {
         const T* a = reinterpret_cast<const T*>(&wv[u]);
         const T* x = reinterpret_cast<const T*>(&ev[u]);
 #pragma unroll
@@ -70,26 +71,15 @@ __global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
       }
     }
     if (ok) p.F[j * p.C + c] = acc;
+  };
+  if (PCB && blockIdx.x >= static_cast<unsigned>(p.B * ncb)) {
+    fold_F((blockIdx.x - p.B * ncb) * 256 + tid);
     return;
   }
   const int b = blockIdx.x / ncb, cb = blockIdx.x % ncb;
   const uint8_t* ty = p.types + static_cast<size_t>(b) * p.T;
   const int col = cb * 64 * VEC + lane * VEC;
-  // PCB: the language-term weights this block needs (Hr <= 128 rows of its
-  // 64*VEC columns) are requested first, so they arrive during the pooling
   u32x4 wraw[PCB ? 2 : 1][16];
-  if constexpr (PCB) {
-    const uint32_t W1s = 2u * p.d + p.d_e;
-    const rsrc_t r_w = make_rsrc(p.W1, static_cast<uint32_t>(p.Hr) * W1s * sizeof(T));
-    const uint32_t ol = static_cast<uint32_t>(p.d + p.d_e + col) * sizeof(T);
-#pragma unroll
-    for (int jb = 0; jb < 2; ++jb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int j = 64 * jb + 16 * w + i;
-        wraw[jb][i] = bload16(r_w, oob_unless(j < p.Hr, static_cast<uint32_t>(j) * W1s * sizeof(T) + ol));
-      }
-  }
   const bool vec = (p.d % VEC) == 0;
   const T* hsample = static_cast<const T*>(p.h) + static_cast<size_t>(b) * p.T * p.d;
   const rsrc_t r_h = make_rsrc(hsample, static_cast<uint32_t>(p.T) * p.d * sizeof(T));
@@ -137,6 +127,22 @@ __global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
           if (col + e < p.d) acc[e] += tof(hsample[static_cast<size_t>(s_rows[i]) * p.d + col + e]);
     }
     __syncthreads();
+  }
+  if constexpr (PCB) {
+    // The language-term weights this block needs (Hr <= 128 rows of its
+    // 64*VEC columns), requested after the row loads: loads of a wave
+    // complete in issue order, so requested first (128 KB per block) they
+    // held back the token types and language rows behind them.
+    const uint32_t W1s = 2u * p.d + p.d_e;
+    const rsrc_t r_w = make_rsrc(p.W1, static_cast<uint32_t>(p.Hr) * W1s * sizeof(T));
+    const uint32_t ol = static_cast<uint32_t>(p.d + p.d_e + col) * sizeof(T);
+#pragma unroll
+    for (int jb = 0; jb < 2; ++jb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int j = 64 * jb + 16 * w + i;
+        wraw[jb][i] = bload16(r_w, oob_unless(j < p.Hr, static_cast<uint32_t>(j) * W1s * sizeof(T) + ol));
+      }
   }
 #pragma unroll
   for (int e = 0; e < VEC; ++e) s_part[w][lane * VEC + e] = acc[e];
