@@ -544,6 +544,42 @@ def other_workloads(args) -> dict:
     return {"other_workloads": out}
 
 
+def full_width_probe(reps: int = 6):
+    """The full-width layer calls at the 7B full-width shape (64 prefixes of
+    81 tokens: 32 visual keeping 4 of 16 groups, 48 language and 1 proprio in
+    value space; d_v = 4096), every call repeated on the same inputs."""
+    import torch
+
+    import paper_2608_18410_amd as rs
+    import synth
+    from paper_2608_18410_amd.pipeline import FullWidthBuffers, run_full_layer
+
+    w = synth.workload(6)
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(w.seed)
+    rng = np.random.default_rng(w.seed)
+    R = (torch.randn(w.dv, w.dv, device=dev, generator=g) / w.dv ** 0.5).bfloat16()
+    Rt = rs.full_transpose(R)
+    q = torch.randn(w.B, w.Tq, w.H, w.dh, device=dev, generator=g).bfloat16()
+    k = torch.randn(w.B, w.T, w.H, w.dh, device=dev, generator=g).bfloat16()
+    v = torch.randn(w.B, w.T, w.H, w.dh, device=dev, generator=g).bfloat16()
+    S = w.G
+    m = np.zeros((w.B, w.T), np.uint32)
+    for b in range(w.B):
+        for t in range(w.n_vis):
+            m[b, t] = int(np.sum(1 << rng.choice(S, w.k_vis, replace=False)))
+        m[b, w.n_vis:] = (1 << S) - 1
+    mask = torch.from_numpy(m.view(np.int32)).to(dev)
+    cap = sum(n * min(kk, S) for n, kk in zip(w.type_counts(), w.k_by_type))
+    bufs = FullWidthBuffers.allocate(w.B, w.T, w.H, w.dh, S, w.Tq, cap, torch.bfloat16, device=dev)
+    budget = rs.make_budget(rs.TOPK, w.k_by_type)
+    for _ in range(reps):
+        run_full_layer(q, k, v, mask, Rt, R, S, bufs, budget=budget, type_counts=w.type_counts())
+    torch.cuda.synchronize()
+    print(json.dumps({"full_width_probe_calls": reps, "workload": w.name}), flush=True)
+
+
 def prefix_attention(args, w):
     """Prefix self-attention (rolesub_attend_causal) at the 7B-stack layer shape:
     every prefix token is a query and sees the keys before it; masks carry the
@@ -741,6 +777,10 @@ def main():
                     help="time token retention + gather of the retained hidden states instead")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 4 times (counter calibration) and exit")
+    ap.add_argument("--full-width-probe", action="store_true",
+                    help="only run the full-width layer calls (rotate + pack, values, attention) 6 times at the "
+                         "7B full-width layer shape with a random, non-orthogonal R (for counter collection; "
+                         "the counts do not depend on R's values) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -767,6 +807,9 @@ def main():
         return
     rs.load()
     dev = torch.device("cuda:0")
+    if args.full_width_probe:
+        full_width_probe()
+        return
     w = synth.workload(args.workload)
     if args.layers:
         w = w.replace(L=args.layers)
