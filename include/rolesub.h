@@ -136,7 +136,8 @@ rolesub_status rolesub_rotate_values(const rolesub_dims* dims, rolesub_dtype dty
  *   idx        [B,T,G] uint8 or NULL: kept group ids ascending, then 0xFF.
  *   count      [B,T]   uint8 or NULL: K_i actually kept.
  *   workspace  device scratch of at least rolesub_route_workspace_size()
- *              bytes (may be NULL if that size is 0).
+ *              bytes (may be NULL if that size is 0). Nothing in it needs
+ *              clearing; calls sharing one workspace must not overlap.
  * ------------------------------------------------------------------------ */
 size_t rolesub_route_workspace_size(const rolesub_dims* dims, const rolesub_router* router);
 rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype,
@@ -148,8 +149,10 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype,
 /* ---------------------------------------------------------------------------
  * rolesub_route_noalloc: rolesub_route without a workspace argument, for
  * callers that cannot allocate device memory (code under stream capture,
- * serving loops that forbid allocation). Same arguments, results and kernels
- * as rolesub_route; the route workspace is a file-scope device array of
+ * serving loops that forbid allocation). Same arguments as rolesub_route and
+ * the same results, bit for bit (the bf16 MLP2 router runs as its single
+ * kernel here, which sums the same terms in the same order as the split-K
+ * form rolesub_route uses); the route workspace is a file-scope device array of
  * ROLESUB_ROUTE_NOALLOC_MAX_BYTES that each device holds until the process
  * ends (its address is looked up once per device, with that device current).
  * Nothing is allocated or freed, by the library or any routine it calls.

@@ -73,7 +73,14 @@ __global__ __launch_bounds__(256) void k_route_pool(RouteParams p) {
     if (ok) p.F[j * p.C + c] = acc;
   };
   if (PCB && blockIdx.x >= static_cast<unsigned>(p.B * ncb)) {
-    fold_F((blockIdx.x - p.B * ncb) * 256 + tid);
+    const int fb = blockIdx.x - p.B * ncb;
+    fold_F(fb * 256 + tid);
+    // the split-K router's per-tile counters start each call at zero
+    if (p.rcnt) {
+      const int ntiles = static_cast<int>((static_cast<size_t>(p.B) * p.T + kRouteSkTok - 1) / kRouteSkTok);
+      const int nfb = (p.Hr * p.C + 255) / 256;
+      for (int i = fb * 256 + tid; i < ntiles; i += nfb * 256) p.rcnt[i] = 0;
+    }
     return;
   }
   const int b = blockIdx.x / ncb, cb = blockIdx.x % ncb;
@@ -684,9 +691,9 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
     for (int u = 0; u < 7; ++u) issue_one(c, u);
   };
 
-  f32x4 acc[9];
+  f32x4 acc[9], acc_lo[9];
 #pragma unroll
-  for (int m = 0; m < 9; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int m = 0; m < 9; ++m) acc[m] = acc_lo[m] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
   for (int c = 0; c < kRtNB - 1; ++c) issue(c);
@@ -718,9 +725,20 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
       if (i % 3 == 1) issue_one(c + kRtNB - 1, i / 3);
     }
     issue_one(c + kRtNB - 1, 6);
+    // the two halves of the hidden size are summed separately and added at
+    // the end, as the split-K form does
+    if (c == nch / 2 - 1) {
+#pragma unroll
+      for (int m = 0; m < 9; ++m) {
+        acc_lo[m] = acc[m];
+        acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
   }
   wait_vmcnt<0>();  // trailing dummy loads land before the LDS is released
   __syncthreads();  // every wave is done with the ring
+#pragma unroll
+  for (int m = 0; m < 9; ++m) acc[m] = acc_lo[m] + acc[m];
 
   float* Fs = reinterpret_cast<float*>(ring);
   float* W2t = Fs + Hr * kFsStride;
@@ -879,6 +897,335 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
   }
 }
 
+// ---------------------------------------------------------------------------
+// Split-K form of the same router (language terms as column-block partials,
+// T >= 96, d a multiple of 128). A tile of 96 tokens is computed by two
+// workgroups of six waves (16 tokens each), each over one half of the hidden
+// size: a workgroup reads half of the weight panel (0.6 MB rather than
+// 1.2 MB per 64 tokens), and 64 prefixes of 177 tokens make 236 workgroups,
+// one per CU on almost every CU. Both halves store their partial products;
+// the second to finish (one atomic ticket per tile, nobody waits) adds the
+// other half's and runs the epilogue. The single kernel accumulates the two
+// halves separately too, so both give the same bits: every product, sum and
+// epilogue step is the same per token.
+constexpr int kSkW = 6, kSkNB = 4;
+constexpr int kSkHBytes = kRouteSkTok * 128, kSkStage = kRtWBytes + kSkHBytes;
+constexpr int kSkLoads = kRtRows / 8 + kRouteSkTok / 8;  // 1 KB wave-loads per stage (30: five per wave)
+static_assert(kSkLoads == 5 * kSkW, "stage loads split evenly over the waves");
+
+template <int GP>
+__global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int npcb) {
+  constexpr int Hr = 128, kW2Stride = GP + 4;
+  static_assert(Hr * (kFsStride + kW2Stride) * 4 <= kSkNB * kSkStage, "epilogue tiles fit the ring");
+  __shared__ __attribute__((aligned(16))) char ring[kSkNB * kSkStage];
+  __shared__ float b2s[GP], brs[16], wps[16];
+  __shared__ __attribute__((aligned(16))) float cbs[2][Hr];
+  __shared__ int s_ticket;
+  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
+  const int d = p.d, C = p.C, G = p.G;
+  const size_t W1s = 2 * static_cast<size_t>(d) + p.d_e;
+  const int tile = blockIdx.x >> 1, half = blockIdx.x & 1;
+
+  const int N = p.B * p.T;
+  const int tok0 = tile * kRouteSkTok;
+  const int tok = tok0 + 16 * w + l16;
+  const bool valid = tok < N;
+  const int nvalid = min(kRouteSkTok, N - tok0);
+  const int b = valid ? tok / p.T : 0;
+  const int type = p.types[valid ? tok : 0];
+
+  // epilogue operands, as in the single kernel (threads 0..255)
+  float fv[8] = {}, w2v[GP / 2] = {}, ps[8] = {}, b1v = 0.f;
+  const int b0 = tok0 / p.T;
+  if (tid < 256) {
+    const rsrc_t r_F = make_rsrc(p.F, static_cast<uint32_t>(Hr * C) * 4u);
+    const rsrc_t r_W2 = make_rsrc(p.W2, static_cast<uint32_t>(G * Hr) * 2u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = u * 256 + tid, j = e >> 4, c = e & 15;
+      fv[u] = __uint_as_float(bload4(r_F, c < C ? 4u * (j * C + c) : kOOB));
+    }
+#pragma unroll
+    for (int u = 0; u < GP / 2; ++u) {
+      const int e = u * 256 + tid, sg = e >> 7, j = e & 127;
+      const uint32_t x = bload4(r_W2, sg < G ? 4u * ((sg * Hr + j) >> 1) : kOOB);
+      w2v[u] = __uint_as_float((j & 1) ? (x & 0xffff0000u) : (x << 16));
+    }
+    const int bs = b0 + (tid >> 7), jj = tid & 127;
+    const rsrc_t r_p = make_rsrc(p.pcb, static_cast<uint32_t>(npcb * p.B * Hr) * 4u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      ps[u] = __uint_as_float(bload4(r_p, oob_unless(bs < p.B && u < npcb, 4u * ((u * p.B + bs) * Hr + jj))));
+    b1v = tof(static_cast<const bf16*>(p.b1)[jj]);
+    if (tid < GP) b2s[tid] = tid < G ? tof(static_cast<const bf16*>(p.b2)[tid]) : 0.f;
+    if (tid < 16) brs[tid] = tid < C ? tof(static_cast<const bf16*>(p.b_r)[tid]) : 0.f;
+    if (tid < 16) wps[tid] = (p.priority && tid < C) ? tof(static_cast<const bf16*>(p.w_pri)[tid]) : 0.f;
+  }
+
+  const rsrc_t r_h = make_rsrc(static_cast<const bf16*>(p.h) + static_cast<size_t>(tok0) * d,
+                               static_cast<uint32_t>(nvalid) * d * 2);
+  const rsrc_t r_w1 = make_rsrc(p.W1, static_cast<uint32_t>(Hr * W1s * 2));
+  const rsrc_t r_wr = make_rsrc(p.W_r, static_cast<uint32_t>(C) * d * 2);
+  const int nh = d / kRtKc / 2, cbase = half * nh;  // this half's chunks
+  const uint32_t ring_base = lds_addr(ring);
+
+  // This wave's wave-loads of a stage: j = w + 6u, u < 5. Load j < 18 brings
+  // weight rows 8j..8j+7 (W1 for j < 16, W_r rows for j = 16, 17), load
+  // j >= 18 token rows 8(j-18).. . Lane i carries row 8j + i/8, LDS piece
+  // i%8, global piece (i%8) ^ swizzle. u = 0, 1: W1 rows; u = 2: W1 rows for
+  // waves 0-3, W_r rows for waves 4-5; u = 3, 4: token rows.
+  uint32_t base_off[5];
+#pragma unroll
+  for (int u = 0; u < 5; ++u) {
+    const int jj = w + kSkW * u;
+    const int ri = lane >> 3, piece = lane & 7;
+    uint32_t off = kOOB;
+    if (jj < 16) {
+      const int r = 8 * jj + ri;
+      off = static_cast<uint32_t>((r * W1s + 8 * (piece ^ rt_swz(r))) * 2);
+    } else if (jj < 18) {
+      const int r = 8 * jj + ri, rr = r - Hr;
+      if (rr < C) off = static_cast<uint32_t>((rr * d + 8 * (piece ^ rt_swz(r))) * 2);
+    } else {
+      const int t = 8 * (jj - 18) + ri;
+      if (t < nvalid) off = static_cast<uint32_t>((t * d + 8 * (piece ^ rt_swz(t))) * 2);
+    }
+    base_off[u] = off;
+  }
+  auto issue_one = [&](int i, int u) {
+    const uint32_t sbase = ring_base + (i % kSkNB) * kSkStage;
+    const bool ok = i < nh;  // stages past this half are all-out-of-range dummies
+    const uint32_t kb = static_cast<uint32_t>(cbase + i) * kRtKc * 2;
+    const uint32_t off = (ok && base_off[u] != kOOB) ? base_off[u] + kb : kOOB;
+    const int jj = w + kSkW * u;
+    const uint32_t dst = sbase + (jj < 18 ? jj * 1024 : kRtWBytes + (jj - 18) * 1024);
+    if (u < 2) dma16(r_w1, off, dst);
+    else if (u == 2) {
+      if (w < 4) dma16(r_w1, off, dst);
+      else dma16(r_wr, off, dst);
+    } else dma16(r_h, off, dst);
+  };
+  auto issue = [&](int i) {
+#pragma unroll
+    for (int u = 0; u < 5; ++u) issue_one(i, u);
+  };
+
+  f32x4 acc[9];
+#pragma unroll
+  for (int m = 0; m < 9; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int i = 0; i < kSkNB - 1; ++i) issue(i);
+  for (int i = 0; i < nh; ++i) {
+    // stage i has landed once at most (kSkNB - 2) younger stages are pending
+    wait_vmcnt<5 * (kSkNB - 2)>();
+    __syncthreads();
+    const char* st = ring + (i % kSkNB) * kSkStage;
+    const int th = 16 * w + l16;
+    bf16x8 hb[2], af[2][9];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      hb[ks] = *reinterpret_cast<const bf16x8*>(st + kRtWBytes + th * 128 + 16 * ((4 * ks + g4) ^ rt_swz(th)));
+#pragma unroll
+      for (int m = 0; m < 9; ++m) {
+        const int r = 16 * m + l16;
+        af[ks][m] = *reinterpret_cast<const bf16x8*>(st + r * 128 + 16 * ((4 * ks + g4) ^ rt_swz(r)));
+      }
+    }
+    // the refill DMAs of stage i + kSkNB - 1 spread between the MFMAs
+#pragma unroll
+    for (int q = 0; q < 18; ++q) {
+      acc[q % 9] = mfma_16x16x32(af[q / 9][q % 9], hb[q / 9], acc[q % 9]);
+      if (q % 4 == 1) issue_one(i + kSkNB - 1, q / 4);
+    }
+  }
+  wait_vmcnt<0>();  // trailing dummy loads land before the LDS is released
+  __syncthreads();  // every wave is done with the ring
+
+  // Both halves store their partial products; the second to finish adds the
+  // other's (a + b: the same bits in either order) and completes the tile.
+  // The two workgroups of a tile may sit on different XCDs, whose L2 caches
+  // are not coherent with each other: the partials are written and read with
+  // system-scope cache bits (written through to memory, read past the
+  // caches), and the ticket is a system-scope atomic. No fence is needed for
+  // them, and none of the XCD's cached weights is written back or dropped.
+  constexpr int kSys = 1 | 16;  // sc0 | sc1: system scope
+  const uint32_t part_bytes = static_cast<uint32_t>(9 * kSkW * 64 * 16);
+  const size_t ntiles = (static_cast<size_t>(N) + kRouteSkTok - 1) / kRouteSkTok;
+  const rsrc_t r_part = make_rsrc(p.rpart, clamp_bytes(ntiles * 2 * static_cast<size_t>(part_bytes)));
+  {
+    const uint32_t o = static_cast<uint32_t>(blockIdx.x) * part_bytes + static_cast<uint32_t>(w * 64 + lane) * 16u;
+#pragma unroll
+    for (int m = 0; m < 9; ++m)
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[m]), r_part, o + m * kSkW * 64 * 16, 0, kSys);
+  }
+  wait_vmcnt<0>();  // this wave's partial has been written
+  __syncthreads();
+  if (tid == 0) s_ticket = __hip_atomic_fetch_add(p.rcnt + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __syncthreads();
+  if (s_ticket == 0) return;  // the other half completes the tile
+  {
+    const uint32_t o = static_cast<uint32_t>(blockIdx.x ^ 1) * part_bytes + static_cast<uint32_t>(w * 64 + lane) * 16u;
+#pragma unroll
+    for (int m = 0; m < 9; ++m)
+      acc[m] = acc[m] + __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                      r_part, static_cast<int>(o + m * kSkW * 64 * 16), 0, kSys));
+  }
+
+  float* Fs = reinterpret_cast<float*>(ring);
+  float* W2t = Fs + Hr * kFsStride;
+  if (tid < 256) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = u * 256 + tid;
+      Fs[(e >> 4) * kFsStride + (e & 15)] = fv[u];
+    }
+#pragma unroll
+    for (int u = 0; u < GP / 2; ++u) {
+      const int e = u * 256 + tid;
+      W2t[(e & 127) * kW2Stride + (e >> 7)] = w2v[u];
+    }
+    // partials added in block order; out-of-range ones read as zero
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) sum += ps[u];
+    cbs[tid >> 7][tid & 127] = sum + b1v;
+  }
+  __syncthreads();
+  float cbl[32];
+  {
+    const float* src = cbs[valid ? b - b0 : 0];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(src + 16 * m + 4 * g4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cbl[4 * m + i] = v[i];
+    }
+  }
+
+  // ---- epilogue: lanes l16, l16+16, l16+32, l16+48 hold token `tok`;
+  // lane quarter q = g4 owns hidden units 16m + 4q + i and role logits 4q + i.
+  float ex[4], mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = 4 * g4 + i;
+    const float lg = acc[8][i] + brs[c];
+    ex[i] = c < C ? lg : -INFINITY;
+    mx = fmaxf(mx, ex[i]);
+  }
+  mx = max_xor32(max_xor16(mx));
+  float sm = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float e = expf(ex[i] - mx);
+    ex[i] = (4 * g4 + i < C) ? e : 0.f;
+    sm += ex[i];
+  }
+  sm = add_xor32(add_xor16(sm));
+  const float isum = 1.f / sm;
+  float a[16];  // role mixture weights; zero past C
+#pragma unroll
+  for (int c = 0; c < 16; ++c) a[c] = __shfl(ex[c & 3], l16 + 16 * (c >> 2), kWave) * isum;
+  if (p.priority) {  // role priority w^T a (weights zero past C)
+    float pr = 0.f;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) pr = fmaf(wps[c], a[c], pr);
+    if (valid && g4 == 0) p.priority[tok] = pr;
+  }
+
+  // F a on the f32 matrix cores: the accumulator layout is that of a 16x16x4
+  // MFMA with A = F (rows 16m + t, roles k0 + q) and B = a (role k0 + q of the
+  // lane's token), so x += F a costs ceil(C / 4) MFMAs per 16 hidden units.
+  // Lane quarter q takes a[k0 + q] by a bitwise blend (a select chain on q
+  // would be turned into an indexed access and move a[] to scratch memory).
+  float ab[4];
+#pragma unroll
+  for (int k4 = 0; k4 < 4; ++k4) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v |= (g4 == q ? ~0u : 0u) & __float_as_uint(a[4 * k4 + q]);
+    ab[k4] = __uint_as_float(v);
+  }
+#pragma unroll
+  for (int k4 = 0; k4 < 4; ++k4) {
+    if (4 * k4 < C) {
+#pragma unroll
+      for (int m = 0; m < 8; ++m)
+        acc[m] = __builtin_amdgcn_mfma_f32_16x16x4f32(Fs[(16 * m + l16) * kFsStride + 4 * k4 + g4], ab[k4],
+                                                      acc[m], 0, 0, 0);
+    }
+  }
+  float gam[GP];
+#pragma unroll
+  for (int s = 0; s < GP; ++s) gam[s] = 0.f;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = 16 * m + 4 * g4 + i;
+      const float gl = gelu_exact(acc[m][i] + cbl[4 * m + i]);
+      const f32x4* wr = reinterpret_cast<const f32x4*>(W2t + j * kW2Stride);
+#pragma unroll
+      for (int s4 = 0; s4 < GP / 4; ++s4) {
+        const f32x4 w2 = wr[s4];
+        gam[4 * s4] += w2[0] * gl;
+        gam[4 * s4 + 1] += w2[1] * gl;
+        gam[4 * s4 + 2] += w2[2] * gl;
+        gam[4 * s4 + 3] += w2[3] * gl;
+      }
+    }
+  }
+  int n_above = 0;
+#pragma unroll
+  for (int s = 0; s < GP; ++s) {
+    gam[s] = add_xor32(add_xor16(gam[s]));
+    gam[s] += b2s[s];
+    n_above += static_cast<int>((s < G) & (gam[s] > p.tau));
+  }
+  // the four lanes of a token now hold bitwise-identical scores; lane quarter
+  // q ranks groups s = 4u + q
+  // (a bitwise blend: a select chain on q gets turned into an indexed access,
+  // which would move gam to scratch memory)
+  float mine[GP / 4];
+  uint32_t qsel[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) qsel[q] = g4 == q ? ~0u : 0u;
+#pragma unroll
+  for (int u = 0; u < GP / 4; ++u) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v |= qsel[q] & __float_as_uint(gam[4 * u + q]);
+    mine[u] = __uint_as_float(v);
+  }
+  const int K = budget_k(p.mode, p.k_by_type, type, p.tau, p.kmin, p.kmax, G, n_above);
+  uint32_t msk = 0;
+  if (p.mode == 1 && K == n_above) {
+#pragma unroll
+    for (int s = 0; s < GP; ++s) msk |= static_cast<uint32_t>((s < G) & (gam[s] > p.tau)) << s;
+  } else {
+#pragma unroll
+    for (int u = 0; u < GP / 4; ++u) {
+      const int s = 4 * u + g4;
+      int rank = 0;
+#pragma unroll
+      for (int t = 0; t < GP; ++t)
+        rank += static_cast<int>((t < G) & (key_above(gam[t], mine[u]) | ((t < s) & key_equal(gam[t], mine[u]))));
+      msk |= static_cast<uint32_t>((s < G) & (rank < K)) << s;
+    }
+    msk = or_xor32(or_xor16(msk));
+  }
+  if (valid) {
+    if (p.scores_out) {
+#pragma unroll
+      for (int u = 0; u < GP / 4; ++u) {
+        const int s = 4 * u + g4;
+        if (s < G) p.scores_out[static_cast<size_t>(tok) * G + s] = mine[u];
+      }
+    }
+    if (g4 == 0 && p.mask) write_selection(p, tok, msk);
+  }
+}
 }  // namespace
 
 hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s) {
@@ -918,7 +1265,12 @@ hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (mfma_ok) {
+  if (mfma_ok && ps && p.rpart && p.rcnt && p.T >= kRouteSkTok && p.d % (2 * kRtKc) == 0) {
+    const dim3 grid(static_cast<unsigned>(2 * route_sk_tiles(p.B, p.T)));
+    if (p.G <= 8) hipLaunchKernelGGL(k_route_mlp2_sk<8>, grid, dim3(64 * kSkW), 0, s, p, ncb);
+    else if (p.G <= 16) hipLaunchKernelGGL(k_route_mlp2_sk<16>, grid, dim3(64 * kSkW), 0, s, p, ncb);
+    else hipLaunchKernelGGL(k_route_mlp2_sk<32>, grid, dim3(64 * kSkW), 0, s, p, ncb);
+  } else if (mfma_ok) {
     const dim3 grid(static_cast<unsigned>((ntok + kRtTok - 1) / kRtTok));
     if (ps) {
       if (p.G <= 8) hipLaunchKernelGGL((k_route_mlp2_bf16<8, true>), grid, dim3(256), 0, s, p, ncb);

@@ -16,6 +16,8 @@ struct RouteParams {
   float* F;   // [Hr or G][C] folded role term (workspace)
   float* hbar;  // [B][d] pooled language state (workspace)
   float* pcb;   // [ncb][B][Hr] partial language terms per column block (bf16 MLP2; workspace)
+  float* rpart;  // split-K router: both halves' partial products per 96-token tile, or null (workspace)
+  int* rcnt;     // split-K router: finished halves per tile, zeroed by the pool kernel (workspace)
   int mode;
   int k_by_type[4];
   float tau;
@@ -41,6 +43,18 @@ inline size_t route_hbar_floats(int B, int d) { return static_cast<size_t>(B) * 
 // the number of partial language terms for any dtype
 inline size_t route_pcb_floats(int B, int d, int Hr, int kind) {
   return kind == 0 ? static_cast<size_t>((d + 255) / 256) * B * Hr : 0;
+}
+
+// Split-K form of the bf16 MLP2 router (Hr = 128): 96-token tiles, each
+// computed by two workgroups over half of the hidden size.
+constexpr int kRouteSkTok = 96;
+inline size_t route_sk_tiles(int B, int T) { return (static_cast<size_t>(B) * T + kRouteSkTok - 1) / kRouteSkTok; }
+// floats of both halves' partials (144 products per token) and ints of the tile counters
+inline size_t route_sk_part_floats(int B, int T, int Hr, int kind) {
+  return kind == 0 && Hr == 128 ? route_sk_tiles(B, T) * 2 * kRouteSkTok * 144 : 0;
+}
+inline size_t route_sk_cnt_ints(int B, int T, int Hr, int kind) {
+  return kind == 0 && Hr == 128 ? route_sk_tiles(B, T) : 0;
 }
 
 hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s);

@@ -108,19 +108,25 @@ rolesub_status check_capacity(const rolesub_dims* dims, const rolesub_budget* bu
   return ROLESUB_OK;
 }
 
-size_t route_ws_bytes(const rolesub_dims* d, const rolesub_router* r) {
+// Route workspace: cb, F, hbar and the partial language terms, then (with
+// split) the partial products and tile counters of the split-K router.
+size_t route_ws_bytes(const rolesub_dims* d, const rolesub_router* r, bool split = true) {
   if (!d || !r || d->B <= 0) return 0;
+  const int T = d->T > 0 ? d->T : 0;
   return align256(route_cb_floats(d->B, r->Hr, d->G, r->kind) * sizeof(float)) +
          align256(route_F_floats(r->Hr, d->G, r->C, r->kind) * sizeof(float)) +
          align256(route_hbar_floats(d->B, d->d > 0 ? d->d : 0) * sizeof(float)) +
-         align256(route_pcb_floats(d->B, d->d > 0 ? d->d : 0, r->Hr, r->kind) * sizeof(float));
+         align256(route_pcb_floats(d->B, d->d > 0 ? d->d : 0, r->Hr, r->kind) * sizeof(float)) +
+         (split ? align256(route_sk_part_floats(d->B, T, r->Hr, r->kind) * sizeof(float)) +
+                      align256(route_sk_cnt_ints(d->B, T, r->Hr, r->kind) * sizeof(int))
+                : 0);
 }
 
 // Checks the router and hidden states and fills the router part of p (B, T,
 // d, G already set); the route workspace sits at the start of `workspace`.
 rolesub_status setup_router(const char* fn, const rolesub_dims* dims, rolesub_dtype dtype,
                             const rolesub_router* router, const void* h, void* workspace, size_t ws_bytes,
-                            RouteParams& p) {
+                            RouteParams& p, bool split = true) {
   if (!h) return fail(ROLESUB_ERR_INVALID_ARG, "%s: h must be non-NULL", fn);
   if (dims->d < 1) return fail(ROLESUB_ERR_INVALID_ARG, "%s: hidden size d=%d", fn, dims->d);
   if (router->C < 1 || router->C > 64)
@@ -145,7 +151,7 @@ rolesub_status setup_router(const char* fn, const rolesub_dims* dims, rolesub_dt
   if (static_cast<size_t>(dims->T) * dims->d * esize(dtype) >= kMaxRegion ||
       static_cast<size_t>(router->Hr) * (2 * static_cast<size_t>(dims->d) + router->d_e) * esize(dtype) >= kMaxRegion)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: one sample's hidden states exceed 2 GiB", fn);
-  const size_t need = route_ws_bytes(dims, router);
+  const size_t need = route_ws_bytes(dims, router, split);
   if (ws_bytes < need || (need && !workspace))
     return fail(ROLESUB_ERR_INVALID_ARG, "%s: workspace of %zu bytes needed, %zu given", fn, need, ws_bytes);
 
@@ -176,6 +182,14 @@ rolesub_status setup_router(const char* fn, const rolesub_dims* dims, rolesub_dt
   p.F = reinterpret_cast<float*>(ws + off_F);
   p.hbar = reinterpret_cast<float*>(ws + off_h);
   p.pcb = reinterpret_cast<float*>(ws + off_p);
+  p.rpart = nullptr;
+  p.rcnt = nullptr;
+  if (split && route_sk_cnt_ints(p.B, p.T, p.Hr, p.kind)) {
+    const size_t off_s = off_p + align256(route_pcb_floats(p.B, p.d, p.Hr, p.kind) * sizeof(float));
+    const size_t off_c = off_s + align256(route_sk_part_floats(p.B, p.T, p.Hr, p.kind) * sizeof(float));
+    p.rpart = reinterpret_cast<float*>(ws + off_s);
+    p.rcnt = reinterpret_cast<int*>(ws + off_c);
+  }
   return ROLESUB_OK;
 }
 
@@ -333,8 +347,10 @@ rolesub_status route_impl(const char* fn, const rolesub_dims* dims, rolesub_dtyp
   if (scores_in) return from_hip(launch_select(p, s), fn);
 
   if (!router) return fail(ROLESUB_ERR_INVALID_ARG, "%s: router is NULL and no scores_in given", fn);
+  // the no-alloc call runs the single-kernel router (its array holds no
+  // split-K partials); both forms give bitwise-equal results
   if (use_scratch) {
-    const size_t need = route_ws_bytes(dims, router);
+    const size_t need = route_ws_bytes(dims, router, false);
     if (need > ROLESUB_ROUTE_NOALLOC_MAX_BYTES)
       return fail(ROLESUB_ERR_UNSUPPORTED, "%s: needs %zu bytes of route workspace, above the %zu bytes it holds", fn,
                   need, static_cast<size_t>(ROLESUB_ROUTE_NOALLOC_MAX_BYTES));
@@ -342,7 +358,7 @@ rolesub_status route_impl(const char* fn, const rolesub_dims* dims, rolesub_dtyp
     if (st) return st;
     ws_bytes = ROLESUB_ROUTE_NOALLOC_MAX_BYTES;
   }
-  st = setup_router(fn, dims, dtype, router, h, workspace, ws_bytes, p);
+  st = setup_router(fn, dims, dtype, router, h, workspace, ws_bytes, p, !use_scratch);
   if (st) return st;
   return from_hip(launch_route(p, dtype == ROLESUB_BF16, s), fn);
 }
