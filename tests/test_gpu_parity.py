@@ -645,6 +645,40 @@ def test_route_mlp2_launch_paths(B, d, Hr, n_vis, n_lang):
     _route_check(w, h, types, router_tensors(wt, torch.bfloat16), ref, f"mlp2 B={B} d={d} Hr={Hr} T={w.T}")
 
 
+# The split-K router (two workgroups per 96-token tile, T >= 96, d a multiple
+# of 128) against the single kernel, which the no-alloc call runs: the same
+# bits for every token, including tiles that end inside a sample or past the
+# last token, 16 and 32 groups, and a second call on the same workspace.
+@pytest.mark.parametrize("cid,B,n_vis,G", [(4, 3, 47, 8),      # T = 96: every tile is one whole sample
+                                           (4, 2, 48, 8),      # T = 97: tiles straddle samples
+                                           (4, 5, 151, 16),    # 16 groups, ragged last tile
+                                           (4, 2, 300, 32)])   # 32 groups
+def test_route_split_k_matches_single_kernel(cid, B, n_vis, G):
+    w = synth.workload(cid).replace(B=B, n_vis=n_vis, G=G, k_vis=min(4, G), k_lang=min(6, G), k_prop=min(8, G))
+    wt = synth.layer_weights(w, 0)
+    h = put(np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(B)]), torch.bfloat16)
+    types = put_u8(stack_types(w, B))
+    router = router_tensors(wt, torch.bfloat16)
+    budget = rs.make_budget(rs.TOPK, w.k_by_type)
+    ws = torch.empty(rs.route_workspace_size(B, w.T, G, w.d, router), dtype=torch.uint8, device=DEV)
+
+    def outs():
+        return {"mask": torch.full((B, w.T), -1, dtype=torch.int32, device=DEV),
+                "idx": torch.full((B, w.T, G), 7, dtype=torch.uint8, device=DEV),
+                "count": torch.full((B, w.T), 9, dtype=torch.uint8, device=DEV),
+                "scores": torch.full((B, w.T, G), float("nan"), dtype=torch.float32, device=DEV)}
+    _say(f"split-K router vs single kernel: B={B} T={w.T} G={G}")
+    a = rs.route(types, budget, G, h=h, router=router, workspace=ws, out=outs())
+    a2 = rs.route(types, budget, G, h=h, router=router, workspace=ws, out=outs())
+    b = rs.route_noalloc(types, budget, G, h=h, router=router, out=outs())
+    torch.cuda.synchronize()
+    for r in (a2, b):
+        for name in ("mask", "idx", "count"):
+            assert torch.equal(r[name], a[name]), name
+        assert np.array_equal(host(r["scores"]).view(np.uint32), host(a["scores"]).view(np.uint32))
+    assert int(host(a["count"]).sum()) > 0
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_route_additive(dtype):
     w = synth.workload(2).replace(B=2, dtype=dtype, d=512, G=16, C=6, n_vis=40, n_lang=9, n_prop=1,
