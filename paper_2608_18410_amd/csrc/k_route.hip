@@ -693,11 +693,9 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
 
   f32x4 acc[9], acc_lo[9];
 #pragma unroll
-  for (int m = 0; m < 9; ++m) acc[m] = acc_lo[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int m = 0; m < 9; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-#pragma unroll
-  for (int c = 0; c < kRtNB - 1; ++c) issue(c);
-  for (int c = 0; c < nch; ++c) {
+  auto step = [&](int c) {
     // chunk c has landed once at most (kRtNB - 2) younger stages are pending
     if (nld == 7) wait_vmcnt<7 * (kRtNB - 2)>();
     else wait_vmcnt<6 * (kRtNB - 2)>();
@@ -725,16 +723,21 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
       if (i % 3 == 1) issue_one(c + kRtNB - 1, i / 3);
     }
     issue_one(c + kRtNB - 1, 6);
-    // the two halves of the hidden size are summed separately and added at
-    // the end, as the split-K form does
-    if (c == nch / 2 - 1) {
+  };
+
 #pragma unroll
-      for (int m = 0; m < 9; ++m) {
-        acc_lo[m] = acc[m];
-        acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-    }
+  for (int c = 0; c < kRtNB - 1; ++c) issue(c);
+  // the two halves of the hidden size are summed separately and added at the
+  // end, as the split-K form does; one loop per half keeps the first half's
+  // sums out of the loop-carried state of the second
+  const int nlo = nch / 2;
+  for (int c = 0; c < nlo; ++c) step(c);
+#pragma unroll
+  for (int m = 0; m < 9; ++m) {
+    acc_lo[m] = acc[m];
+    acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  for (int c = nlo; c < nch; ++c) step(c);
   wait_vmcnt<0>();  // trailing dummy loads land before the LDS is released
   __syncthreads();  // every wave is done with the ring
 #pragma unroll
@@ -919,7 +922,7 @@ __global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int 
   static_assert(Hr * (kFsStride + kW2Stride) * 4 <= kSkNB * kSkStage, "epilogue tiles fit the ring");
   __shared__ __attribute__((aligned(16))) char ring[kSkNB * kSkStage];
   __shared__ float b2s[GP], brs[16], wps[16];
-  __shared__ __attribute__((aligned(16))) float cbs[2][Hr];
+  __shared__ __attribute__((aligned(16))) float cbs[kSkW / 2][Hr];
   __shared__ int s_ticket;
   const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
@@ -935,9 +938,18 @@ __global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int 
   const int b = valid ? tok / p.T : 0;
   const int type = p.types[valid ? tok : 0];
 
-  // epilogue operands, as in the single kernel (threads 0..255)
-  float fv[8] = {}, w2v[GP / 2] = {}, ps[8] = {}, b1v = 0.f;
+  // epilogue operands, as in the single kernel: F and W2 by threads 0..255,
+  // the language terms of the (at most three) samples the tile touches by all
+  float fv[8] = {}, w2v[GP / 2] = {}, ps[8] = {};
   const int b0 = tok0 / p.T;
+  {
+    const int bs = b0 + (tid >> 7), jj = tid & 127;
+    const rsrc_t r_p = make_rsrc(p.pcb, static_cast<uint32_t>(npcb * p.B * Hr) * 4u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      ps[u] = __uint_as_float(bload4(r_p, oob_unless(bs < p.B && u < npcb, 4u * ((u * p.B + bs) * Hr + jj))));
+  }
+  const float b1v = tof(static_cast<const bf16*>(p.b1)[tid & 127]);
   if (tid < 256) {
     const rsrc_t r_F = make_rsrc(p.F, static_cast<uint32_t>(Hr * C) * 4u);
     const rsrc_t r_W2 = make_rsrc(p.W2, static_cast<uint32_t>(G * Hr) * 2u);
@@ -952,12 +964,6 @@ __global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int 
       const uint32_t x = bload4(r_W2, sg < G ? 4u * ((sg * Hr + j) >> 1) : kOOB);
       w2v[u] = __uint_as_float((j & 1) ? (x & 0xffff0000u) : (x << 16));
     }
-    const int bs = b0 + (tid >> 7), jj = tid & 127;
-    const rsrc_t r_p = make_rsrc(p.pcb, static_cast<uint32_t>(npcb * p.B * Hr) * 4u);
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      ps[u] = __uint_as_float(bload4(r_p, oob_unless(bs < p.B && u < npcb, 4u * ((u * p.B + bs) * Hr + jj))));
-    b1v = tof(static_cast<const bf16*>(p.b1)[jj]);
     if (tid < GP) b2s[tid] = tid < G ? tof(static_cast<const bf16*>(p.b2)[tid]) : 0.f;
     if (tid < 16) brs[tid] = tid < C ? tof(static_cast<const bf16*>(p.b_r)[tid]) : 0.f;
     if (tid < 16) wps[tid] = (p.priority && tid < C) ? tof(static_cast<const bf16*>(p.w_pri)[tid]) : 0.f;
@@ -1086,6 +1092,8 @@ __global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int 
       const int e = u * 256 + tid;
       W2t[(e & 127) * kW2Stride + (e >> 7)] = w2v[u];
     }
+  }
+  {
     // partials added in block order; out-of-range ones read as zero
     float sum = 0.f;
 #pragma unroll
@@ -1265,7 +1273,7 @@ hipError_t launch_route(const RouteParams& p, bool bf16, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (mfma_ok && ps && p.rpart && p.rcnt && p.T >= kRouteSkTok && p.d % (2 * kRtKc) == 0) {
+  if (mfma_ok && ps && p.rpart && p.rcnt && p.T >= kRouteSkMinT && p.d % (2 * kRtKc) == 0) {
     const dim3 grid(static_cast<unsigned>(2 * route_sk_tiles(p.B, p.T)));
     if (p.G <= 8) hipLaunchKernelGGL(k_route_mlp2_sk<8>, grid, dim3(64 * kSkW), 0, s, p, ncb);
     else if (p.G <= 16) hipLaunchKernelGGL(k_route_mlp2_sk<16>, grid, dim3(64 * kSkW), 0, s, p, ncb);

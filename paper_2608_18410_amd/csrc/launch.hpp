@@ -48,6 +48,8 @@ inline size_t route_pcb_floats(int B, int d, int Hr, int kind) {
 // Split-K form of the bf16 MLP2 router (Hr = 128): 96-token tiles, each
 // computed by two workgroups over half of the hidden size.
 constexpr int kRouteSkTok = 96;
+// shortest prefix the split form takes: a tile then touches at most three samples
+constexpr int kRouteSkMinT = kRouteSkTok / 2;
 inline size_t route_sk_tiles(int B, int T) { return (static_cast<size_t>(B) * T + kRouteSkTok - 1) / kRouteSkTok; }
 // floats of both halves' partials (144 products per token) and ints of the tile counters
 inline size_t route_sk_part_floats(int B, int T, int Hr, int kind) {

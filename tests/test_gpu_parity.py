@@ -645,12 +645,15 @@ def test_route_mlp2_launch_paths(B, d, Hr, n_vis, n_lang):
     _route_check(w, h, types, router_tensors(wt, torch.bfloat16), ref, f"mlp2 B={B} d={d} Hr={Hr} T={w.T}")
 
 
-# The split-K router (two workgroups per 96-token tile, T >= 96, d a multiple
+# The split-K router (two workgroups per 96-token tile, T >= 48, d a multiple
 # of 128) against the single kernel, which the no-alloc call runs: the same
 # bits for every token, including tiles that end inside a sample or past the
-# last token, 16 and 32 groups, and a second call on the same workspace.
+# last token, tiles over three samples, 16 and 32 groups, and a second call on
+# the same workspace.
 @pytest.mark.parametrize("cid,B,n_vis,G", [(4, 3, 47, 8),      # T = 96: every tile is one whole sample
                                            (4, 2, 48, 8),      # T = 97: tiles straddle samples
+                                           (4, 5, 1, 8),       # T = 50: tiles over three samples
+                                           (4, 7, 32, 16),     # T = 81: the full-width prefix
                                            (4, 5, 151, 16),    # 16 groups, ragged last tile
                                            (4, 2, 300, 32)])   # 32 groups
 def test_route_split_k_matches_single_kernel(cid, B, n_vis, G):
