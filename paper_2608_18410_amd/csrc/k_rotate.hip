@@ -26,8 +26,12 @@ namespace {
 // the slots given by the offsets, so z never reaches memory; the tile then
 // holds the tile's slots in cache order and a slot -> token table. The copy
 // unit is 16 bytes (kPack16, ds >= 8), 8 bytes (kPack8, ds = 4) or 4 bytes
-// (kPack4, ds = 2), never wider than a slot.
+// (kPack4, ds = 2), never wider than a slot. The pack modes also form the
+// cache offsets of their run of tokens from the masks (an exclusive scan of
+// the kept counts within each sample), while R_h is being staged, and the
+// workgroups of head 0 write them out.
 enum RotOut { kZ = 0, kPack16 = 1, kPack8 = 2, kPack4 = 3 };
+constexpr int kRotMaxRun = 512;  // tokens per workgroup at most (two per thread)
 
 template <int DH>
 __device__ __forceinline__ int rt_chunk_swz(int j) {
@@ -46,11 +50,20 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
   __shared__ __attribute__((aligned(16))) bf16 Ost[4][16 * DH];  // per-wave output tile
   __shared__ uint8_t Otok[4][NSLOT];                           // slot -> token of the tile
   __shared__ int32_t Obase[4][PACK ? 16 : 1], Opre[4][PACK ? 16 : 1];
+  // PACK: exclusive scan of the kept counts over the run (< 2^16: at most
+  // 511 tokens of at most 32 groups); 16-bit entries keep three workgroups
+  // per CU within the LDS
+  __shared__ uint16_t Sexc[PACK ? kRotMaxRun : 1];
   const int H = p.H, ntok = p.ntok;
   int h, chunk;
   xcd_split(blockIdx.x, H, h, chunk);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, g4 = lane >> 4;
+  const int t_begin = chunk * p.tok_per_wg;
+  const int t_end = min(t_begin + p.tok_per_wg, ntok);
+  const uint32_t gm = p.G >= 32 ? 0xFFFFFFFFu : ((1u << p.G) - 1u);
   const bf16* Rh = static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH;
+  uint32_t mk0 = 0, mk1 = 0;
+  int cpre = 0, pre = 0;
   {
     // Transposed staging. An item is (row pair p, 8-column chunk jc): rows 2p
     // and 2p+1 of R_h are read 16 bytes each and written as 8 dwords
@@ -65,6 +78,17 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       const int pr = it % NPAIR, jc = it / NPAIR;
       lo[r] = *reinterpret_cast<const u32x4*>(Rh + (2 * pr) * DH + 8 * jc);
       hi[r] = *reinterpret_cast<const u32x4*>(Rh + (2 * pr + 1) * DH + 8 * jc);
+    }
+    // PACK: the masks of this thread's two tokens of the run (2 tid, 2 tid + 1)
+    // and the kept count of the earlier tokens of t_begin's sample, requested
+    // while R_h is in flight
+    if constexpr (PACK) {
+      const int ta = t_begin + 2 * tid;
+      mk0 = ta < t_end ? p.mask[ta] & gm : 0u;
+      mk1 = ta + 1 < t_end ? p.mask[ta + 1] & gm : 0u;
+      const int s0 = (t_begin / p.T) * p.T;
+#pragma unroll 4
+      for (int t = s0 + tid; t < t_begin; t += 256) cpre += __popc(p.mask[t] & gm);
     }
 #pragma unroll
     for (int r = 0; r < NI; ++r) {
@@ -82,10 +106,54 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       }
     }
   }
+  if constexpr (PACK) {
+    // Offsets of the run's tokens. With E(t) the exclusive scan of the kept
+    // counts over the run (from t_begin) and pre the kept count of t_begin's
+    // sample before t_begin, a token whose sample starts at or before
+    // t_begin has offset pre + E(t), one whose sample starts at ss inside the
+    // run E(t) - E(ss).
+    int* Sred = reinterpret_cast<int*>(Ost[0]);  // the output tiles are not in use yet
+    const int c0 = __popc(mk0), c1 = __popc(mk1);
+    int x = c0 + c1;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, kWave);
+      if (lane >= o) x += y;
+    }
+    int r = cpre;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) r += __shfl_xor(r, o, kWave);
+    if (lane == 63) Sred[w] = x;
+    if (lane == 0) Sred[4 + w] = r;
+    __syncthreads();
+    int e0 = x - c0 - c1;
+    for (int i = 0; i < w; ++i) e0 += Sred[i];
+    pre = Sred[4] + Sred[5] + Sred[6] + Sred[7];
+    const int T = p.T, ta = t_begin + 2 * tid;
+    const bool in0 = ta < t_end, in1 = ta + 1 < t_end;
+    if (in0) Sexc[2 * tid] = static_cast<uint16_t>(e0);
+    if (in1) Sexc[2 * tid + 1] = static_cast<uint16_t>(e0 + c0);
+    __syncthreads();
+    // offsets are [B][T+1]: token t at t + t/T, each sample's total after its
+    // last token; one workgroup per run writes them
+    if (h == 0) {
+      auto fin = [&](int t, int e) {
+        const int ss = (t / T) * T;
+        return ss <= t_begin ? pre + e : e - Sexc[ss - t_begin];
+      };
+      const int o0 = in0 ? fin(ta, e0) : 0, o1 = in1 ? fin(ta + 1, e0 + c0) : 0;
+      if (in0) {
+        p.offsets[ta + ta / T] = o0;
+        if (ta % T == T - 1) p.offsets[ta + ta / T + 1] = o0 + c0;
+      }
+      if (in1) {
+        p.offsets[ta + 1 + (ta + 1) / T] = o1;
+        if ((ta + 1) % T == T - 1) p.offsets[ta + 1 + (ta + 1) / T + 1] = o1 + c1;
+      }
+    }
+  }
   __syncthreads();
 
-  const int t_begin = chunk * p.tok_per_wg;
-  const int t_end = min(t_begin + p.tok_per_wg, ntok);
   // this workgroup's tokens of head h; rows past t_end load as zero
   const uint32_t tstride = static_cast<uint32_t>(H) * DH * 2;
   const rsrc_t r_v = make_rsrc(static_cast<const bf16*>(p.v) + (static_cast<size_t>(t_begin) * H + h) * DH,
@@ -95,9 +163,6 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
   // rotate only: this run's rows of z
   const rsrc_t r_z = make_rsrc(static_cast<bf16*>(p.z) + (static_cast<size_t>(t_begin) * H + h) * DH,
                                PACK ? 0u : static_cast<uint32_t>(t_end - t_begin - 1) * tstride + DH * 2);
-  // offsets are [B][T+1]: token (b, t) sits at b*(T+1)+t
-  const rsrc_t r_o = make_rsrc(p.offsets, PACK ? static_cast<uint32_t>(ntok + ntok / max(p.T, 1)) * 4u : 0u);
-  const uint32_t gm = p.G >= 32 ? 0xFFFFFFFFu : ((1u << p.G) - 1u);
   const int ds = DH / p.G;
   // G divides dh (a power of two), so ds is one too: shifts, no divisions
   const int lds = __builtin_ctz(ds);
@@ -123,7 +188,11 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
     x.off = 0;
     if constexpr (PACK) {
       x.mask = bload4(r_m, oob_unless(ok, 4u * (tok - t_begin)));
-      x.off = static_cast<int32_t>(bload4(r_o, oob_unless(ok, 4u * (tok + tok / p.T))));
+      // the token's offset from the run's scan (see the prologue)
+      const int ss = (tok / p.T) * p.T;
+      const int e = Sexc[min(tok - t_begin, kRotMaxRun - 1)];
+      const int es = Sexc[min(max(ss - t_begin, 0), kRotMaxRun - 1)];
+      x.off = ok ? (ss <= t_begin ? pre + e : e - es) : 0;
     }
   };
   auto process = [&](const Tile& x, int tt) {
@@ -307,7 +376,7 @@ int rotate_tokens_per_wg(int ntok, int H) {
   // Long token runs amortise staging R_h (32 KB at dh = 128, as much as 128
   // tokens of values); shorten them only while there would be fewer than
   // about 2.5 workgroups per CU (256 CUs) to spread the stream over.
-  int tpw = 512;
+  int tpw = kRotMaxRun;
   while (tpw > 64 && static_cast<long>((ntok + tpw - 1) / tpw) * H < 640) tpw >>= 1;
   return tpw;
 }
@@ -346,9 +415,17 @@ hipError_t launch_rotate(bool bf16, int ntok, int H, int dh, const void* v, cons
 }
 
 hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, const void* v, const void* R,
-                              const uint32_t* mask, const int32_t* offsets, void* Vp, int64_t cap,
+                              const uint32_t* mask, int32_t* offsets, void* Vp, int64_t cap,
                               hipStream_t s) {
   const int ntok = B * T;
+  if (B == 0) return hipSuccess;
+  const bool mfma = bf16 && (dh == 128 || dh == 64) && dh / G >= 2;
+  // the matrix-core kernel forms the offsets itself; otherwise (or when it
+  // does not run) they come first from their own kernel
+  if (!mfma || ntok == 0 || H == 0 || cap == 0) {
+    const hipError_t e = launch_pack_offsets(B, T, G, mask, offsets, s);
+    if (e != hipSuccess) return e;
+  }
   if (ntok == 0 || H == 0 || cap == 0) return hipSuccess;
   RotateParams p = {};
   p.ntok = ntok;
@@ -361,7 +438,7 @@ hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, con
   p.offsets = offsets;
   p.Vp = Vp;
   p.cap = cap;
-  if (bf16 && (dh == 128 || dh == 64) && dh / G >= 2) {
+  if (mfma) {
     p.tok_per_wg = rotate_tokens_per_wg(ntok, H);
     const dim3 grid(static_cast<unsigned>(((ntok + p.tok_per_wg - 1) / p.tok_per_wg) * H));
     // G <= 32, so 2-dim groups occur only at dh = 64

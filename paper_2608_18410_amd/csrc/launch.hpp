@@ -106,16 +106,16 @@ struct RotateParams {
   const void* R;
   void* z;                  // rotate only
   const uint32_t* mask;     // fused rotate + pack
-  const int32_t* offsets;
+  int32_t* offsets;         // written by the matrix-core kernel (head 0's workgroups)
   void* Vp;
   int64_t cap;
 };
 hipError_t launch_rotate(bool bf16, int ntok, int H, int dh, const void* v, const void* R, void* z,
                          hipStream_t s);
-// Fused rotation + pack. Offsets must already hold the exclusive scan of the
-// kept counts.
+// Fused rotation + pack; also writes the offsets (the exclusive scan of the
+// kept counts per sample).
 hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, const void* v, const void* R,
-                              const uint32_t* mask, const int32_t* offsets, void* Vp, int64_t cap,
+                              const uint32_t* mask, int32_t* offsets, void* Vp, int64_t cap,
                               hipStream_t s);
 hipError_t launch_pack_offsets(int B, int T, int G, const uint32_t* mask, int32_t* offsets, hipStream_t s);
 

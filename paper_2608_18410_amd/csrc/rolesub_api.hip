@@ -614,9 +614,6 @@ rolesub_status rolesub_rotate_pack(const rolesub_dims* dims, rolesub_dtype dtype
           esize(dtype) >= kMaxRegion)
     return fail(ROLESUB_ERR_UNSUPPORTED, "%s: packed cache too large", fn);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  rolesub_status r = from_hip(launch_pack_offsets(dims->B, dims->T, dims->G, mask, offsets, s), fn);
-  if (r) return r;
-  if (dims->T == 0) return ROLESUB_OK;
   return from_hip(launch_rotate_pack(dtype == ROLESUB_BF16, dims->B, dims->T, dims->H, dims->dh, dims->G, v, R,
                                      mask, offsets, Vp, cap_groups, s),
                   fn);
