@@ -26,10 +26,12 @@ namespace {
 // the slots given by the offsets, so z never reaches memory; the tile then
 // holds the tile's slots in cache order and a slot -> token table. The copy
 // unit is 16 bytes (kPack16, ds >= 8), 8 bytes (kPack8, ds = 4) or 4 bytes
-// (kPack4, ds = 2), never wider than a slot. The pack modes also form the
-// cache offsets of their run of tokens from the masks (an exclusive scan of
-// the kept counts within each sample), while R_h is being staged, and the
-// workgroups of head 0 write them out.
+// (kPack4, ds = 2), never wider than a slot. For prefixes of at most
+// kRotMaxRun tokens the pack modes also form the cache offsets of their run
+// of tokens from the masks (an exclusive scan of the kept counts within each
+// sample), while R_h is being staged, and the workgroups of head 0 write
+// them out; for longer prefixes (a run's sample may start thousands of
+// tokens earlier) they read offsets the scan kernel wrote (off_ready).
 enum RotOut { kZ = 0, kPack16 = 1, kPack8 = 2, kPack4 = 3 };
 constexpr int kRotMaxRun = 512;  // tokens per workgroup at most (two per thread)
 
@@ -62,6 +64,50 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
   const int t_end = min(t_begin + p.tok_per_wg, ntok);
   const uint32_t gm = p.G >= 32 ? 0xFFFFFFFFu : ((1u << p.G) - 1u);
   const bf16* Rh = static_cast<const bf16*>(p.R) + static_cast<size_t>(h) * DH * DH;
+  // this workgroup's tokens of head h; rows past t_end load as zero
+  const uint32_t tstride = static_cast<uint32_t>(H) * DH * 2;
+  const rsrc_t r_v = make_rsrc(static_cast<const bf16*>(p.v) + (static_cast<size_t>(t_begin) * H + h) * DH,
+                               static_cast<uint32_t>(t_end - t_begin - 1) * tstride + DH * 2);
+  // PACK: group masks and cache offsets of the run's tokens
+  const rsrc_t r_m = make_rsrc(p.mask + t_begin, static_cast<uint32_t>(t_end - t_begin) * 4u);
+  // rotate only: this run's rows of z
+  const rsrc_t r_z = make_rsrc(static_cast<bf16*>(p.z) + (static_cast<size_t>(t_begin) * H + h) * DH,
+                               PACK ? 0u : static_cast<uint32_t>(t_end - t_begin - 1) * tstride + DH * 2);
+  // off_ready: offsets are [B][T+1], token (b, t) at b*(T+1)+t
+  const rsrc_t r_o = make_rsrc(p.offsets, PACK && p.off_ready ? static_cast<uint32_t>(ntok + ntok / p.T) * 4u : 0u);
+  const int ds = DH / p.G;
+  // G divides dh (a power of two), so ds is one too: shifts, no divisions
+  const int lds = __builtin_ctz(ds);
+  const int cap32 = static_cast<int>(p.cap);  // < 2^31: the cache per (sample, head) is < 2 GiB
+
+  struct Tile {
+    bf16x8 v[KS];
+    uint32_t mask;
+    int32_t off;  // off_ready: the token's cache offset
+  };
+  // Loads are unconditional (rows past the run read as zeros through the
+  // buffer bounds): a branch around them makes later waits cover every
+  // outstanding memory operation.
+  auto load = [&](Tile& x, int tt) {
+    const int tok = tt + l16;
+    const bool ok = tok < t_end;
+    const uint32_t o = static_cast<uint32_t>(tok - t_begin) * tstride + 16u * g4;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) x.v[ks] = __builtin_bit_cast(bf16x8, bload16(r_v, oob_unless(ok, o + 64u * ks)));
+    x.mask = 0;
+    x.off = 0;
+    if constexpr (PACK) {
+      x.mask = bload4(r_m, oob_unless(ok, 4u * (tok - t_begin)));
+      x.off = static_cast<int32_t>(bload4(r_o, oob_unless(ok && p.off_ready, 4u * (tok + tok / p.T))));
+    }
+  };
+  // one tile in flight ahead of the one being processed (A and B alternate);
+  // the first is requested before R_h is staged, so that its round trip
+  // overlaps the staging
+  Tile A, B;
+  int t0 = t_begin + 16 * w;
+  load(A, t0);
+
   uint32_t mk0 = 0, mk1 = 0;
   int cpre = 0, pre = 0;
   {
@@ -82,7 +128,7 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
     // PACK: the masks of this thread's two tokens of the run (2 tid, 2 tid + 1)
     // and the kept count of the earlier tokens of t_begin's sample, requested
     // while R_h is in flight
-    if constexpr (PACK) {
+    if (PACK && !p.off_ready) {
       const int ta = t_begin + 2 * tid;
       mk0 = ta < t_end ? p.mask[ta] & gm : 0u;
       mk1 = ta + 1 < t_end ? p.mask[ta + 1] & gm : 0u;
@@ -106,7 +152,7 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       }
     }
   }
-  if constexpr (PACK) {
+  if (PACK && !p.off_ready) {
     // Offsets of the run's tokens. With E(t) the exclusive scan of the kept
     // counts over the run (from t_begin) and pre the kept count of t_begin's
     // sample before t_begin, a token whose sample starts at or before
@@ -154,47 +200,8 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
   }
   __syncthreads();
 
-  // this workgroup's tokens of head h; rows past t_end load as zero
-  const uint32_t tstride = static_cast<uint32_t>(H) * DH * 2;
-  const rsrc_t r_v = make_rsrc(static_cast<const bf16*>(p.v) + (static_cast<size_t>(t_begin) * H + h) * DH,
-                               static_cast<uint32_t>(t_end - t_begin - 1) * tstride + DH * 2);
-  // PACK: group masks and cache offsets of the run's tokens
-  const rsrc_t r_m = make_rsrc(p.mask + t_begin, static_cast<uint32_t>(t_end - t_begin) * 4u);
-  // rotate only: this run's rows of z
-  const rsrc_t r_z = make_rsrc(static_cast<bf16*>(p.z) + (static_cast<size_t>(t_begin) * H + h) * DH,
-                               PACK ? 0u : static_cast<uint32_t>(t_end - t_begin - 1) * tstride + DH * 2);
-  const int ds = DH / p.G;
-  // G divides dh (a power of two), so ds is one too: shifts, no divisions
-  const int lds = __builtin_ctz(ds);
-  const int cap32 = static_cast<int>(p.cap);  // < 2^31: the cache per (sample, head) is < 2 GiB
   bf16* ost = Ost[w];
   char* ostb = reinterpret_cast<char*>(ost);
-
-  struct Tile {
-    bf16x8 v[KS];
-    uint32_t mask;
-    int32_t off;
-  };
-  // Loads are unconditional (rows past the run read as zeros through the
-  // buffer bounds): a branch around them makes later waits cover every
-  // outstanding memory operation.
-  auto load = [&](Tile& x, int tt) {
-    const int tok = tt + l16;
-    const bool ok = tok < t_end;
-    const uint32_t o = static_cast<uint32_t>(tok - t_begin) * tstride + 16u * g4;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) x.v[ks] = __builtin_bit_cast(bf16x8, bload16(r_v, oob_unless(ok, o + 64u * ks)));
-    x.mask = 0;
-    x.off = 0;
-    if constexpr (PACK) {
-      x.mask = bload4(r_m, oob_unless(ok, 4u * (tok - t_begin)));
-      // the token's offset from the run's scan (see the prologue)
-      const int ss = (tok / p.T) * p.T;
-      const int e = Sexc[min(tok - t_begin, kRotMaxRun - 1)];
-      const int es = Sexc[min(max(ss - t_begin, 0), kRotMaxRun - 1)];
-      x.off = ok ? (ss <= t_begin ? pre + e : e - es) : 0;
-    }
-  };
   auto process = [&](const Tile& x, int tt) {
     // keep the R^T fragments in LDS: without this the compiler hoists the
     // loop-invariant LDS reads into ~128 registers and occupancy collapses
@@ -232,9 +239,17 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       }
     } else {
       const int tok = tt + l16;
+      // the token's offset from the run's scan (see the prologue)
+      int off = x.off;
+      if (!p.off_ready) {
+        const int ss = (tok / p.T) * p.T;
+        const int e = Sexc[min(tok - t_begin, kRotMaxRun - 1)];
+        const int es = Sexc[min(max(ss - t_begin, 0), kRotMaxRun - 1)];
+        off = tok < t_end ? (ss <= t_begin ? pre + e : e - es) : 0;
+      }
       const uint32_t cmask = x.mask & gm;  // zero for rows past the run
       // groups of this token that fit the cache, and its first local slot
-      const int cnt = min(__popc(cmask), max(cap32 - x.off, 0));
+      const int cnt = min(__popc(cmask), max(cap32 - off, 0));
       int incl = cnt;
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) {
@@ -253,7 +268,7 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       if (g4 == 0) {
         Obase[w][l16] = static_cast<int32_t>(static_cast<uint32_t>((tok / p.T - b0) * H) *
                                                  static_cast<uint32_t>(hstride) +
-                                             (static_cast<uint32_t>(x.off) << lds));
+                                             (static_cast<uint32_t>(off) << lds));
         Opre[w][l16] = pre;
       }
 #pragma unroll
@@ -314,11 +329,6 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       }
     }
   };
-  // one tile in flight ahead of the one being processed; A and B alternate
-  // roles so that no register copy forces an early wait
-  Tile A, B;
-  int t0 = t_begin + 16 * w;
-  load(A, t0);
   for (; t0 < t_end; t0 += 128) {
     load(B, t0 + 64);
     process(A, t0);
@@ -420,9 +430,11 @@ hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, con
   const int ntok = B * T;
   if (B == 0) return hipSuccess;
   const bool mfma = bf16 && (dh == 128 || dh == 64) && dh / G >= 2;
-  // the matrix-core kernel forms the offsets itself; otherwise (or when it
-  // does not run) they come first from their own kernel
-  if (!mfma || ntok == 0 || H == 0 || cap == 0) {
+  // the matrix-core kernel forms the offsets itself for prefixes of at most
+  // kRotMaxRun tokens; otherwise (or when it does not run) they come first
+  // from their own kernel
+  const bool off_ready = !mfma || T > kRotMaxRun;
+  if (off_ready || ntok == 0 || H == 0 || cap == 0) {
     const hipError_t e = launch_pack_offsets(B, T, G, mask, offsets, s);
     if (e != hipSuccess) return e;
   }
@@ -438,6 +450,7 @@ hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, con
   p.offsets = offsets;
   p.Vp = Vp;
   p.cap = cap;
+  p.off_ready = off_ready ? 1 : 0;
   if (mfma) {
     p.tok_per_wg = rotate_tokens_per_wg(ntok, H);
     const dim3 grid(static_cast<unsigned>(((ntok + p.tok_per_wg - 1) / p.tok_per_wg) * H));

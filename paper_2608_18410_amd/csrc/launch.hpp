@@ -106,7 +106,8 @@ struct RotateParams {
   const void* R;
   void* z;                  // rotate only
   const uint32_t* mask;     // fused rotate + pack
-  int32_t* offsets;         // written by the matrix-core kernel (head 0's workgroups)
+  int32_t* offsets;         // written by the matrix-core kernel (head 0's workgroups) unless off_ready
+  int off_ready;            // offsets already hold the scan (long prefixes)
   void* Vp;
   int64_t cap;
 };

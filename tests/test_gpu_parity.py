@@ -190,8 +190,8 @@ def test_rotate(cid, B, T, H, dh):
     (3, 2, 150, 8, 64, 4),       # head dim 64, 16-dim groups
     # the offsets the matrix-core kernel forms for its run of tokens:
     (3, 300, 1, 4, 128, 8),      # one token per sample: 64 samples start inside each run
-    (3, 3, 700, 4, 64, 8),       # 64-token runs inside 700-token samples (counts carried from the sample start)
-    (2, 2, 2000, 32, 128, 8),    # 128-token runs, up to 1999 earlier tokens of the sample
+    (3, 3, 500, 4, 64, 8),       # 64-token runs inside 500-token samples (counts carried from the sample start)
+    (2, 2, 2000, 32, 128, 8),    # prefixes past 512 tokens: offsets from the scan kernel
     (3, 30, 177, 64, 64, 8),     # 512-token runs over three or four samples, ragged last run
 ])
 def test_rotate_pack_fused(cid, B, T, H, dh, G):
