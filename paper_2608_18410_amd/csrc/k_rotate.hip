@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
   load(A, t0);
 
   uint32_t mk0 = 0, mk1 = 0;
-  int cpre = 0, pre = 0;
+  int cpre = 0, run_pre = 0;  // run_pre: kept count of t_begin's sample before the run
   {
     // Transposed staging. An item is (row pair p, 8-column chunk jc): rows 2p
     // and 2p+1 of R_h are read 16 bytes each and written as 8 dwords
@@ -154,10 +154,10 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
   }
   if (PACK && !p.off_ready) {
     // Offsets of the run's tokens. With E(t) the exclusive scan of the kept
-    // counts over the run (from t_begin) and pre the kept count of t_begin's
+    // counts over the run (from t_begin) and run_pre the kept count of t_begin's
     // sample before t_begin, a token whose sample starts at or before
-    // t_begin has offset pre + E(t), one whose sample starts at ss inside the
-    // run E(t) - E(ss).
+    // t_begin has offset run_pre + E(t), one whose sample starts at ss inside
+    // the run E(t) - E(ss).
     int* Sred = reinterpret_cast<int*>(Ost[0]);  // the output tiles are not in use yet
     const int c0 = __popc(mk0), c1 = __popc(mk1);
     int x = c0 + c1;
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
     __syncthreads();
     int e0 = x - c0 - c1;
     for (int i = 0; i < w; ++i) e0 += Sred[i];
-    pre = Sred[4] + Sred[5] + Sred[6] + Sred[7];
+    run_pre = Sred[4] + Sred[5] + Sred[6] + Sred[7];
     const int T = p.T, ta = t_begin + 2 * tid;
     const bool in0 = ta < t_end, in1 = ta + 1 < t_end;
     if (in0) Sexc[2 * tid] = static_cast<uint16_t>(e0);
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
     if (h == 0) {
       auto fin = [&](int t, int e) {
         const int ss = (t / T) * T;
-        return ss <= t_begin ? pre + e : e - Sexc[ss - t_begin];
+        return ss <= t_begin ? run_pre + e : e - Sexc[ss - t_begin];
       };
       const int o0 = in0 ? fin(ta, e0) : 0, o1 = in1 ? fin(ta + 1, e0 + c0) : 0;
       if (in0) {
@@ -245,7 +245,7 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
         const int ss = (tok / p.T) * p.T;
         const int e = Sexc[min(tok - t_begin, kRotMaxRun - 1)];
         const int es = Sexc[min(max(ss - t_begin, 0), kRotMaxRun - 1)];
-        off = tok < t_end ? (ss <= t_begin ? pre + e : e - es) : 0;
+        off = tok < t_end ? (ss <= t_begin ? run_pre + e : e - es) : 0;
       }
       const uint32_t cmask = x.mask & gm;  // zero for rows past the run
       // groups of this token that fit the cache, and its first local slot
