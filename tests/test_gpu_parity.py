@@ -191,6 +191,8 @@ def test_rotate(cid, B, T, H, dh):
     # the offsets the matrix-core kernel forms for its run of tokens:
     (3, 300, 1, 4, 128, 8),      # one token per sample: 64 samples start inside each run
     (3, 3, 500, 4, 64, 8),       # 64-token runs inside 500-token samples (counts carried from the sample start)
+    (3, 2, 512, 4, 64, 8),       # the longest prefix whose offsets the kernel forms itself
+    (3, 2, 513, 4, 64, 8),       # one token more: offsets from the scan kernel
     (2, 2, 2000, 32, 128, 8),    # prefixes past 512 tokens: offsets from the scan kernel
     (3, 30, 177, 64, 64, 8),     # 512-token runs over three or four samples, ragged last run
 ])
