@@ -382,13 +382,30 @@ __global__ __launch_bounds__(256) void k_rotate_pack_generic(RotateParams p, int
 }  // namespace
 
 namespace {
-int rotate_tokens_per_wg(int ntok, int H) {
-  // Long token runs amortise staging R_h (32 KB at dh = 128, as much as 128
-  // tokens of values); shorten them only while there would be fewer than
-  // about 2.5 workgroups per CU (256 CUs) to spread the stream over.
-  int tpw = kRotMaxRun;
-  while (tpw > 64 && static_cast<long>((ntok + tpw - 1) / tpw) * H < 640) tpw >>= 1;
-  return tpw;
+int rotate_tokens_per_wg(int ntok, int H, int dh) {
+  // A workgroup stages R_h (32 KB at dh = 128, as much as 128 tokens of
+  // values) and then streams its run of tokens; the workgroups resident at
+  // once (three per CU at dh = 128, four at dh = 64) form a round, and a
+  // second, partly filled round costs nearly a whole one. Runs (multiples of
+  // 16 tokens, 64 to 512) are chosen to minimise rounds x (run + 128), the
+  // longer run on ties; past four rounds of 512-token runs, 512.
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
+    ncu = 256;
+  const long slots = static_cast<long>(dh == 128 ? 3 : 4) * ncu;
+  if (static_cast<long>((ntok + kRotMaxRun - 1) / kRotMaxRun) * H > 4 * slots) return kRotMaxRun;
+  int best = kRotMaxRun;
+  long best_cost = -1;
+  for (int tpw = kRotMaxRun; tpw >= 64; tpw -= 16) {
+    const long wgs = static_cast<long>((ntok + tpw - 1) / tpw) * H;
+    const long cost = (wgs + slots - 1) / slots * (tpw + 128);
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best = tpw;
+    }
+  }
+  return best;
 }
 }  // namespace
 
@@ -403,7 +420,7 @@ hipError_t launch_rotate(bool bf16, int ntok, int H, int dh, const void* v, cons
     p.R = R;
     p.z = z;
     p.G = 1;
-    p.tok_per_wg = rotate_tokens_per_wg(ntok, H);
+    p.tok_per_wg = rotate_tokens_per_wg(ntok, H, dh);
     const dim3 grid(static_cast<unsigned>(((ntok + p.tok_per_wg - 1) / p.tok_per_wg) * H));
     if (dh == 128)
       hipLaunchKernelGGL((k_rotate_bf16<128, kZ>), grid, dim3(256), 0, s, p);
@@ -452,7 +469,7 @@ hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, con
   p.cap = cap;
   p.off_ready = off_ready ? 1 : 0;
   if (mfma) {
-    p.tok_per_wg = rotate_tokens_per_wg(ntok, H);
+    p.tok_per_wg = rotate_tokens_per_wg(ntok, H, dh);
     const dim3 grid(static_cast<unsigned>(((ntok + p.tok_per_wg - 1) / p.tok_per_wg) * H));
     // G <= 32, so 2-dim groups occur only at dh = 64
     const int ds = dh / G;

@@ -194,7 +194,7 @@ def test_rotate(cid, B, T, H, dh):
     (3, 2, 512, 4, 64, 8),       # the longest prefix whose offsets the kernel forms itself
     (3, 2, 513, 4, 64, 8),       # one token more: offsets from the scan kernel
     (2, 2, 2000, 32, 128, 8),    # prefixes past 512 tokens: offsets from the scan kernel
-    (3, 30, 177, 64, 64, 8),     # 512-token runs over three or four samples, ragged last run
+    (3, 30, 177, 64, 64, 8),     # runs over two to four samples, ragged last run
 ])
 def test_rotate_pack_fused(cid, B, T, H, dh, G):
     w = synth.workload(cid).replace(B=B, n_vis=T, n_lang=0, n_prop=0, H=H, dh=dh, G=G)
