@@ -40,7 +40,7 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
 // into the cache (PACK: v -> Vp) or from it into the head-major values
 // (!PACK: Vp -> Vh, at the given offsets). kPrepChunks workgroups per sample
 // share the copies; the first one writes the list, count and offsets, and
-// (PACK) the per-group lists instead of copying.
+// (PACK) workgroup c builds the per-group lists of groups c, c + kPrepChunks.
 template <bool PACK>
 __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
   // offsets, the value-space token list and (PACK) the masks of the sample,
@@ -94,60 +94,65 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
       int32_t* off = p.offsets + static_cast<size_t>(b) * (T + 1);
       for (int t = tid; t < T; t += 256) off[t] = s_off[t];
       if (tid == 0) off[T] = run_pc;
-      // per group: the routed tokens that keep it, in token order. The first
-      // pass counts every group's tokens (one ballot per group, one barrier
-      // per chunk), the second places them after the earlier groups'.
-      int32_t* pr = p.pairs + static_cast<size_t>(b) * T * S;
-      int run_g[32];
+    }
+  }
+  if (PACK) {
+    // Per group: the routed tokens that keep it, in token order, after the
+    // earlier groups' lists. Every workgroup of the sample counts every
+    // group's tokens (one ballot per group per 256 tokens) and then lists
+    // the tokens of its own groups (chunk, chunk + kPrepChunks).
+    int32_t* pr = p.pairs + static_cast<size_t>(b) * T * S;
+    int run_g[32];
 #pragma unroll
-      for (int gg = 0; gg < 32; ++gg) run_g[gg] = 0;
-      for (int pass = 0; pass < 2; ++pass) {
-        if (pass == 1) {
-          int start = 0;
+    for (int gg = 0; gg < 32; ++gg) run_g[gg] = 0;
+    for (int c0 = 0; c0 < T; c0 += 256) {
+      const int t = c0 + tid;
+      const uint32_t m = t < T ? s_mask[t] : full;
+      const uint32_t kept = m != full ? m : 0u;
 #pragma unroll
-          for (int gg = 0; gg < 32; ++gg) {
-            const int n = run_g[gg];
-            if (gg < S && tid == 0) {
-              p.counts_g[static_cast<size_t>(b) * S + gg] = n;
-              p.starts_g[static_cast<size_t>(b) * S + gg] = start;
-            }
-            run_g[gg] = start;
-            start += n;
-          }
+      for (int gg = 0; gg < 32; ++gg) {
+        if (gg < S) {
+          const uint64_t bal = __ballot((kept >> gg) & 1u);
+          if (lane == 0) wcnt[w][gg] = __popcll(bal);
         }
-        for (int c0 = 0; c0 < T; c0 += 256) {
-          const int t = c0 + tid;
-          const uint32_t m = t < T ? s_mask[t] : full;
-          const uint32_t kept = m != full ? m : 0u;
-          uint64_t bal[32];
+      }
+      __syncthreads();
 #pragma unroll
-          for (int gg = 0; gg < 32; ++gg) {
-            bal[gg] = gg < S ? __ballot((kept >> gg) & 1u) : 0ull;
-            if (lane == 0 && gg < S) wcnt[w][gg] = __popcll(bal[gg]);
-          }
-          __syncthreads();
+      for (int gg = 0; gg < 32; ++gg)
+        if (gg < S) run_g[gg] += wcnt[0][gg] + wcnt[1][gg] + wcnt[2][gg] + wcnt[3][gg];
+      __syncthreads();
+    }
+    for (int g = chunk; g < S; g += kPrepChunks) {
+      int start = 0;
 #pragma unroll
-          for (int gg = 0; gg < 32; ++gg) {
-            if (gg < S) {
-              if (pass == 1 && ((kept >> gg) & 1u)) {
-                int o = run_g[gg] + __popcll(bal[gg] & ((1ull << lane) - 1ull));
-                for (int v = 0; v < w; ++v) o += wcnt[v][gg];
-                pr[o] = t;
-              }
-              run_g[gg] += wcnt[0][gg] + wcnt[1][gg] + wcnt[2][gg] + wcnt[3][gg];
-            }
-          }
-          __syncthreads();
-        }
+      for (int gg = 0; gg < 32; ++gg) start += gg < g ? run_g[gg] : 0;
+      int n_g = 0;
+#pragma unroll
+      for (int gg = 0; gg < 32; ++gg) n_g = gg == g ? run_g[gg] : n_g;
+      if (tid == 0) {
+        p.counts_g[static_cast<size_t>(b) * S + g] = n_g;
+        p.starts_g[static_cast<size_t>(b) * S + g] = start;
+      }
+      int run = start;
+      for (int c0 = 0; c0 < T; c0 += 256) {
+        const int t = c0 + tid;
+        const uint32_t m = t < T ? s_mask[t] : full;
+        const bool keeps = m != full && ((m >> g) & 1u);
+        const uint64_t bal = __ballot(keeps);
+        if (lane == 0) wtot[w] = __popcll(bal);
+        __syncthreads();
+        int o = run + __popcll(bal & ((1ull << lane) - 1ull));
+        for (int v = 0; v < w; ++v) o += wtot[v];
+        if (keeps) pr[o] = t;
+        run += wtot[0] + wtot[1] + wtot[2] + wtot[3];
+        __syncthreads();
       }
     }
   }
   // value-space copies of the full tokens: d_v/8 16-byte pieces each, work
   // items (token, piece) spread over the chunks' threads, 8 loads in flight.
-  // With PACK the first chunk builds the group lists above and copies nothing.
   const int pieces = p.dv / 8, dh = p.dv / p.H;
-  const int cc = PACK ? chunk - 1 : chunk, ncc = PACK ? kPrepChunks - 1 : kPrepChunks;
-  if (cc < 0) return;
+  const int cc = chunk, ncc = kPrepChunks;
   const int n_items = run_full * pieces;
   const rsrc_t r_cache = make_rsrc(static_cast<const bf16*>(p.Vp) + static_cast<size_t>(b) * p.cap * p.ds,
                                    clamp_bytes(static_cast<size_t>(p.cap) * p.ds * 2));
