@@ -18,8 +18,8 @@
 namespace rolesub {
 namespace {
 
-constexpr int kBM0 = 64, kBM1 = 128, kBN = 128, kBK = 32;  // row tiles: rotate, values
-constexpr int kLd = kBK + 8;  // LDS row stride (elements): 80 bytes, conflict-free 16-byte fragment reads
+constexpr int kBM0 = 64, kBM1 = 128, kBN = 128, kBK = 64;  // row tiles: rotate, values
+constexpr int kLd = kBK + 8;  // LDS row stride (elements): 144 bytes, conflict-free 16-byte fragment reads
 constexpr int kPrepChunks = 16;
 
 __device__ __forceinline__ uint32_t full_bits(int S) { return S >= 32 ? 0xFFFFFFFFu : ((1u << S) - 1u); }
@@ -200,11 +200,11 @@ __global__ __launch_bounds__(256) void k_full_prep(FullParams p) {
 }
 
 // C[m][n] = sum_k A[m][k] * Bt[n][k] on 16x16x32 bf16 MFMA; 128 x 128 tile per
-// workgroup, four waves of 64 x 64, k in steps of 32 through a double-buffered
-// LDS tile (one barrier per step), the operands of the next three steps in
+// workgroup, four waves of 64 x 64, k in steps of 64 (two MFMA k-steps per
+// barrier) through a double-buffered LDS tile, the next step's operands in
 // flight in registers.
-// 128-row tiles: about 46 KB of LDS and up to 256 registers (the four
-// register sets), two workgroups per CU; 64-row tiles: 35 KB, four per CU.
+// 128-row tiles: about 78 KB of LDS and 224 registers, two workgroups per CU;
+// 64-row tiles: 59 KB, two per CU.
 //   MODE 0 (rotate): rows are the routed tokens of all samples that keep the
 //   workgroup's group g (per-sample lists from the preparation kernel), so only
 //   kept groups are computed; A = v, Bt = the rows of R^T for group g's output
@@ -219,7 +219,7 @@ template <int MODE, int TBM, int NS>
 __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
   // A and B tiles (double-buffered) in one region, reused for the output tile
   constexpr int kTileA = TBM * kLd, kTileB = kBN * kLd;
-  constexpr int NA = TBM / 64, MI = TBM / 32;  // A pieces per thread, 16-row blocks per wave
+  constexpr int NA = TBM / 32, NB = kBN / 32, MI = TBM / 32;  // A, B pieces per thread, 16-row blocks per wave
   __shared__ __attribute__((aligned(16))) bf16 smem[2 * kTileA + 2 * kTileB];
   // tile i of A at smem + i * kTileA, of B at smem + 2 * kTileA + i * kTileB
   __shared__ int pre[kFullMaxB + 1];
@@ -306,13 +306,14 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
       ? make_rsrc(p.v, clamp_bytes(static_cast<size_t>(B) * T * dv * 2))
       : make_rsrc(p.Vp, clamp_bytes(static_cast<size_t>(B) * p.cap * ds * 2));
   const rsrc_t r_B = make_rsrc(p.Rm, clamp_bytes(static_cast<size_t>(dv) * dv * 2));
-  // this thread's NA A pieces and two B pieces per step: piece q = tid + 256 u,
-  // row q / 4, 16-byte chunk q % 4
-  int arow[2], ach[2];
+  // this thread's NA A pieces and NB B pieces per step: piece q = tid + 256 u,
+  // row q / 8, 16-byte chunk q % 8
+  constexpr int NP = NA > NB ? NA : NB;
+  int arow[NP], ach[NP];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    arow[u] = (tid + 256 * u) >> 2;
-    ach[u] = (tid + 256 * u) & 3;
+  for (int u = 0; u < NP; ++u) {
+    arow[u] = (tid + 256 * u) >> 3;
+    ach[u] = (tid + 256 * u) & 7;
   }
   // this thread's A rows, read once: MODE 0 the byte offset of the token's
   // value row, MODE 1 the byte offset of the sample's cache and the token's
@@ -355,10 +356,12 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
     return k0 >= dv ? dv : (kn < dv ? kn : dv);
   };
   const int k_first = tile_or == 0 ? dv : static_cast<int>(__builtin_ctz(tile_or)) * ds;
-  // active steps: a multiple of 4 (ds is a multiple of 128: at least 4 steps
-  // per group), which NS divides. Eight sets for the rotation were measured
-  // slower (two workgroups per CU instead of four); the values product uses
-  // two (three workgroups per CU instead of two, about 3 % faster than four).
+  // active steps: a multiple of 2 (ds is a multiple of 128: at least 2 steps
+  // per group), which NS divides. Steps of 64 columns (two MFMA k-steps per
+  // barrier) took the values product from 110-121 to 100-109 us (prep
+  // included) with two operand sets; more sets were slower for both products
+  // (the rotation: 107 us with four sets of 64 columns, 104 with eight of 32,
+  // against 72-77).
   const int nsteps = MODE == 0 ? dv / kBK : __popc(tile_or) * (ds / kBK);
 
   // the loop body covers NS steps and picks the LDS buffer by step parity:
@@ -373,47 +376,52 @@ __global__ __launch_bounds__(256, 2) void k_full_gemm(FullParams p) {
   const int wm = w >> 1, wn = w & 1;
   // NS register sets: step s's operands arrive in set s % NS, issued NS - 1
   // steps before they are written to LDS
-  u32x4 ra[NS][NA], rbv[NS][2];
+  u32x4 ra[NS][NA], rbv[NS][NB];
   // MODE 1 computes the offsets unconditionally: with a branch around its
   // (longer) address computation the compiler reuses an in-flight load's
   // registers and waits for every load (values 117.6 -> 110.4 us). The
   // rotation's short computation is faster with the select (71.7 vs 82.2 us;
   // both measured in one process).
-  auto load_set = [&](u32x4 (&a)[NA], u32x4 (&bb)[2], int k0) {
+  auto load_set = [&](u32x4 (&a)[NA], u32x4 (&bb)[NB], int k0) {
     const bool real = k0 < dv;
     if constexpr (MODE == 1) {
       const int kk = real ? k0 : 0;
 #pragma unroll
       for (int u = 0; u < NA; ++u) a[u] = bload16(r_A, oob_unless(real, a_off(u, kk)));
 #pragma unroll
-      for (int u = 0; u < 2; ++u) bb[u] = bload16(r_B, oob_unless(real, b_off(u, kk)));
+      for (int u = 0; u < NB; ++u) bb[u] = bload16(r_B, oob_unless(real, b_off(u, kk)));
     } else {
 #pragma unroll
       for (int u = 0; u < NA; ++u) a[u] = bload16(r_A, real ? a_off(u, k0) : kOOB);
 #pragma unroll
-      for (int u = 0; u < 2; ++u) bb[u] = bload16(r_B, real ? b_off(u, k0) : kOOB);
+      for (int u = 0; u < NB; ++u) bb[u] = bload16(r_B, real ? b_off(u, k0) : kOOB);
     }
   };
-  auto store_set = [&](const u32x4 (&a)[NA], const u32x4 (&bb)[2], int buf) {
+  auto store_set = [&](const u32x4 (&a)[NA], const u32x4 (&bb)[NB], int buf) {
 #pragma unroll
     for (int u = 0; u < NA; ++u)
       *reinterpret_cast<u32x4*>(&(smem + buf * kTileA)[arow[u] * kLd + 8 * ach[u]]) = a[u];
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < NB; ++u)
       *reinterpret_cast<u32x4*>(&(smem + 2 * kTileA + buf * kTileB)[arow[u] * kLd + 8 * ach[u]]) = bb[u];
   };
   auto compute = [&](int buf) {
-    bf16x8 af[MI], bfr[4];
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
-      af[i] = *reinterpret_cast<const bf16x8*>(&(smem + buf * kTileA)[((TBM / 2) * wm + 16 * i + l16) * kLd + 8 * g4]);
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      bf16x8 af[MI], bfr[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      bfr[i] = *reinterpret_cast<const bf16x8*>(&(smem + 2 * kTileA + buf * kTileB)[(64 * wn + 16 * i + l16) * kLd + 8 * g4]);
+      for (int i = 0; i < MI; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(
+            &(smem + buf * kTileA)[((TBM / 2) * wm + 16 * i + l16) * kLd + 32 * ks + 8 * g4]);
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
+      for (int i = 0; i < 4; ++i)
+        bfr[i] = *reinterpret_cast<const bf16x8*>(
+            &(smem + 2 * kTileA + buf * kTileB)[(64 * wn + 16 * i + l16) * kLd + 32 * ks + 8 * g4]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x32(af[i], bfr[j], acc[i][j]);
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x32(af[i], bfr[j], acc[i][j]);
+    }
   };
   // prologue: steps 0..NS-1 issued in the same order the loop keeps
   int kq = k_first;
@@ -497,7 +505,7 @@ hipError_t launch_full(const FullParams& p, int mode, hipStream_t s) {
     hipLaunchKernelGGL(k_full_prep<true>, gprep, dim3(256), shm_pack, s, p);
     const unsigned ncol = static_cast<unsigned>(p.S * (p.ds / kBN));
     const unsigned nmt = static_cast<unsigned>((rows + kBM0 - 1) / kBM0);
-    hipLaunchKernelGGL((k_full_gemm<0, kBM0, 4>), dim3(ncol * nmt), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((k_full_gemm<0, kBM0, 2>), dim3(ncol * nmt), dim3(256), 0, s, p);
   } else {
     hipLaunchKernelGGL(k_full_prep<false>, gprep, dim3(256), shm_vals, s, p);
     const unsigned ntn = static_cast<unsigned>(p.dv / kBN);
