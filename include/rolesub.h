@@ -156,9 +156,11 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype,
  * ROLESUB_ROUTE_NOALLOC_MAX_BYTES that each device holds until the process
  * ends (its address is looked up once per device, with that device current).
  * Nothing is allocated or freed, by the library or any routine it calls.
- *   - Calls whose rolesub_route_workspace_size() exceeds the maximum return
+ *   - Calls whose route workspace exceeds the maximum return
  *     ROLESUB_ERR_UNSUPPORTED before anything is enqueued (with d = 4096 and
- *     Hr = 128: more than 333 samples).
+ *     Hr = 128: more than 333 samples). That workspace is
+ *     rolesub_route_workspace_size() less the split-K partial products and
+ *     tile counters, which the single kernel does not use.
  *   - stream must belong to the current device (else ROLESUB_ERR_INVALID_ARG).
  *   - Every call on one device shares that device's array and overwrites it
  *     (every byte the kernels read is written earlier in the same call, so
