@@ -158,7 +158,7 @@ rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype,
  * Nothing is allocated or freed, by the library or any routine it calls.
  *   - Calls whose route workspace exceeds the maximum return
  *     ROLESUB_ERR_UNSUPPORTED before anything is enqueued (with d = 4096 and
- *     Hr = 128: more than 333 samples). That workspace is
+ *     Hr = 128: more than 334 samples). That workspace is
  *     rolesub_route_workspace_size() less the split-K partial products and
  *     tile counters, which the single kernel does not use.
  *   - stream must belong to the current device (else ROLESUB_ERR_INVALID_ARG).

@@ -1,8 +1,9 @@
 """rolesub_route_noalloc (the route call that allocates nothing: its workspace
 is a fixed device array inside the library) against rolesub_route, through the
 C ABI: identical scores, masks, kept-group lists and counts, on two calls in a
-row, the second with a smaller input, then a selection-only call and a size
-beyond the array, refused on the host."""
+row, the second with a smaller input, then a selection-only call, a size
+beyond the array, refused on the host, and the exact sample limit at
+d = 4096."""
 import numpy as np
 import pytest
 import torch
@@ -78,3 +79,29 @@ def test_route_noalloc_selection_only_and_limit():
     assert e.value.status == 2
     torch.cuda.synchronize()
     assert bool((out["mask"] == -1).all())          # nothing was written
+
+
+def test_route_noalloc_sample_limit_at_d4096():
+    # d = 4096, Hr = 128: the array holds the route workspace of 334 samples
+    # (cb, F, pooled states and 16 column blocks of language terms); 335 are
+    # refused on the host, 334 give rolesub_route's results
+    for B, fits in ((335, False), (334, True)):
+        w = synth.workload(4).replace(B=B, n_vis=1, n_lang=0, n_prop=0)
+        wt = synth.layer_weights(w, 0)
+        router = router_tensors(wt, torch.bfloat16)
+        h = put(np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(B)]), torch.bfloat16)
+        types = put_u8(stack_types(w, B))
+        budget = rs.make_budget(rs.TOPK, w.k_by_type)
+        print(f"route_noalloc sample limit: B={B}", flush=True)
+        out = _outs(B, w.T, w.G)
+        if not fits:
+            with pytest.raises(rs.RolesubError, match="above the") as e:
+                rs.route_noalloc(types, budget, w.G, h=h, router=router, out=out)
+            assert e.value.status == 2
+            torch.cuda.synchronize()
+            assert bool((out["mask"] == -1).all())
+            continue
+        got = rs.route_noalloc(types, budget, w.G, h=h, router=router, out=out)
+        ref = rs.route(types, budget, w.G, h=h, router=router, out=_outs(B, w.T, w.G))
+        torch.cuda.synchronize()
+        _same(got, ref)
