@@ -4,7 +4,9 @@ caller memory (the split-K router's tile tickets, the partial language terms,
 the cache offsets the rotate+pack kernel forms), so a replay that found stale
 values there would differ. Replays alternate with eager work on other
 buffers and with synchronisations, and the outputs are overwritten with
-sentinels before each replay, so that every output must be written again."""
+sentinels before each replay, so that every output must be written again.
+Also: two layers with their own workspaces on two streams at once give the
+bits of the same layers run one after the other."""
 import numpy as np
 import pytest
 import torch
@@ -148,3 +150,36 @@ def test_full_width_layer_graph_replays():
         torch.cuda.synchronize()
         for name, a, t in zip(("offsets", "Vp", "Vh", "out"), want, outs(bufs)):
             assert torch.equal(a, _bits(t)), (rep, name)
+
+
+def test_two_layers_on_two_streams_match_sequential():
+    # independent calls with their own workspaces may run concurrently: two
+    # 7B-stack layers enqueued on two streams (default priority) at once give
+    # the bits of the same layers run one after the other
+    w = synth.workload(4).replace(B=8)
+    budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
+    cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
+    Ls = [_stack_layer(w, 0), _stack_layer(w, 1)]
+    ws = rs.route_workspace_size(w.B, w.T, w.G, w.d, Ls[0]["router"])
+    mk = lambda: LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, torch.bfloat16, device=DEV,
+                                       with_z=False, ws_bytes=ws)
+    seq, par = [mk(), mk()], [mk(), mk()]
+    run = lambda X, b: run_layer(X["h"], X["q"], X["k"], X["v"], X["types"], X["R"], budget, w.G, b,
+                                 router=X["router"], type_counts=w.type_counts())
+    _say(f"two streams, 7B-stack layers B={w.B}")
+    for X, b in zip(Ls, seq):
+        run(X, b)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for rep in range(3):
+        for b in par:
+            _sentinel((b.mask, b.idx, b.count, b.scores, b.offsets, b.out))
+        torch.cuda.synchronize()
+        for X, b, st in zip(Ls, par, streams):
+            st.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(st):
+                run(X, b)
+        torch.cuda.synchronize()
+        for a, b in zip(seq, par):
+            for name in ("mask", "idx", "count", "scores", "offsets", "out"):
+                assert torch.equal(_bits(getattr(a, name)), _bits(getattr(b, name))), (rep, name)
