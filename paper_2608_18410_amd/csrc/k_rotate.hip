@@ -126,15 +126,20 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       hi[r] = *reinterpret_cast<const u32x4*>(Rh + (2 * pr + 1) * DH + 8 * jc);
     }
     // PACK: the masks of this thread's two tokens of the run (2 tid, 2 tid + 1)
-    // and the kept count of the earlier tokens of t_begin's sample, requested
-    // while R_h is in flight
+    // and the kept count of the earlier tokens of t_begin's sample (fewer
+    // than T <= kRotMaxRun, two per thread), requested while R_h is in
+    // flight. The loads are unconditional, bounded by their buffers: a load
+    // under a branch is waited for at once, and that wait also drains R_h
+    // and the first tile, one more full round trip per load.
     if (PACK && !p.off_ready) {
-      const int ta = t_begin + 2 * tid;
-      mk0 = ta < t_end ? p.mask[ta] & gm : 0u;
-      mk1 = ta + 1 < t_end ? p.mask[ta + 1] & gm : 0u;
+      // two 4-byte loads (the pinned offset keeps them from being merged
+      // into one 8-byte load, whose bounds check would drop a run's last
+      // token when the run is odd)
+      mk0 = bload4(r_m, 8u * tid) & gm;
+      mk1 = bload4(r_m, oob_unless(true, 8u * tid + 4u)) & gm;
       const int s0 = (t_begin / p.T) * p.T;
-#pragma unroll 4
-      for (int t = s0 + tid; t < t_begin; t += 256) cpre += __popc(p.mask[t] & gm);
+      const rsrc_t r_pm = make_rsrc(p.mask + s0, static_cast<uint32_t>(t_begin - s0) * 4u);
+      cpre = __popc(bload4(r_pm, 4u * tid) & gm) + __popc(bload4(r_pm, 4u * tid + 1024u) & gm);
     }
 #pragma unroll
     for (int r = 0; r < NI; ++r) {
