@@ -103,10 +103,25 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
   };
   // one tile in flight ahead of the one being processed (A and B alternate);
   // the first is requested before R_h is staged, so that its round trip
-  // overlaps the staging
+  // overlaps the staging. Tiles w and w + 4 of the run go to wave w. When
+  // every workgroup is resident at once (dyn_tiles) the others are handed
+  // out in order from an LDS counter to whichever wave asks next, so that
+  // waves slowed by their memory requests take fewer and the workgroup ends
+  // with its last tile; otherwise (later workgroups fill the CUs that free
+  // up) wave w takes every fourth tile.
+  __shared__ int s_next;
+  const int ntile = (t_end - t_begin + 15) >> 4;
+  if (tid == 0) s_next = 8;
+  int snext = w + 4;
+  auto grab = [&]() {
+    if (!p.dyn_tiles) return snext += 4;
+    int i = 0;
+    if (lane == 0) i = atomicAdd(&s_next, 1);
+    return __builtin_amdgcn_readfirstlane(__shfl(i, 0, kWave));
+  };
   Tile A, B;
-  int t0 = t_begin + 16 * w;
-  load(A, t0);
+  int ia = w, ib = w + 4;
+  load(A, t_begin + 16 * ia);
 
   uint32_t mk0 = 0, mk1 = 0;
   int cpre = 0, run_pre = 0;  // run_pre: kept count of t_begin's sample before the run
@@ -334,12 +349,25 @@ __global__ __launch_bounds__(256) void k_rotate_bf16(RotateParams p) {
       }
     }
   };
-  for (; t0 < t_end; t0 += 128) {
-    load(B, t0 + 64);
-    process(A, t0);
-    if (t0 + 64 >= t_end) break;
-    load(A, t0 + 128);
-    process(B, t0 + 64);
+  // Every wave's tiles come in increasing order: the first past the run
+  // ends its loop (its loads read nothing). A wave asks for a tile one step
+  // before it requests its data, so the counter's round trip overlaps a
+  // tile's work; the index it holds when it stops is past the run as well.
+  if (ia < ntile) {
+    int nx = grab();
+    load(B, t_begin + 16 * ib);
+    for (;;) {
+      process(A, t_begin + 16 * ia);
+      if (ib >= ntile) break;
+      ia = nx;
+      nx = grab();
+      load(A, t_begin + 16 * ia);
+      process(B, t_begin + 16 * ib);
+      if (ia >= ntile) break;
+      ib = nx;
+      nx = grab();
+      load(B, t_begin + 16 * ib);
+    }
   }
 }
 
@@ -387,18 +415,24 @@ __global__ __launch_bounds__(256) void k_rotate_pack_generic(RotateParams p, int
 }  // namespace
 
 namespace {
-int rotate_tokens_per_wg(int ntok, int H, int dh) {
-  // A workgroup stages R_h (32 KB at dh = 128, as much as 128 tokens of
-  // values) and then streams its run of tokens; the workgroups resident at
-  // once (three per CU at dh = 128, four at dh = 64) form a round, and a
-  // second, partly filled round costs nearly a whole one. Runs (multiples of
-  // 16 tokens, 64 to 512) are chosen to minimise rounds x (run + 128), the
-  // longer run on ties; past four rounds of 512-token runs, 512.
+// workgroups of the matrix-core rotation resident at once: three per CU at
+// dh = 128, four at dh = 64
+long rotate_slots(int dh) {
   int dev = 0, ncu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
     ncu = 256;
-  const long slots = static_cast<long>(dh == 128 ? 3 : 4) * ncu;
+  return static_cast<long>(dh == 128 ? 3 : 4) * ncu;
+}
+
+int rotate_tokens_per_wg(int ntok, int H, int dh) {
+  // A workgroup stages R_h (32 KB at dh = 128, as much as 128 tokens of
+  // values) and then streams its run of tokens; the workgroups resident at
+  // once form a round, and a second, partly filled round costs nearly a
+  // whole one. Runs (multiples of 16 tokens, 64 to 512) are chosen to
+  // minimise rounds x (run + 128), the longer run on ties; past four rounds
+  // of 512-token runs, 512.
+  const long slots = rotate_slots(dh);
   if (static_cast<long>((ntok + kRotMaxRun - 1) / kRotMaxRun) * H > 4 * slots) return kRotMaxRun;
   int best = kRotMaxRun;
   long best_cost = -1;
@@ -427,6 +461,7 @@ hipError_t launch_rotate(bool bf16, int ntok, int H, int dh, const void* v, cons
     p.G = 1;
     p.tok_per_wg = rotate_tokens_per_wg(ntok, H, dh);
     const dim3 grid(static_cast<unsigned>(((ntok + p.tok_per_wg - 1) / p.tok_per_wg) * H));
+    p.dyn_tiles = static_cast<long>(grid.x) <= rotate_slots(dh) ? 1 : 0;
     if (dh == 128)
       hipLaunchKernelGGL((k_rotate_bf16<128, kZ>), grid, dim3(256), 0, s, p);
     else
@@ -476,6 +511,7 @@ hipError_t launch_rotate_pack(bool bf16, int B, int T, int H, int dh, int G, con
   if (mfma) {
     p.tok_per_wg = rotate_tokens_per_wg(ntok, H, dh);
     const dim3 grid(static_cast<unsigned>(((ntok + p.tok_per_wg - 1) / p.tok_per_wg) * H));
+    p.dyn_tiles = static_cast<long>(grid.x) <= rotate_slots(dh) ? 1 : 0;
     // G <= 32, so 2-dim groups occur only at dh = 64
     const int ds = dh / G;
     if (dh == 128 && ds >= 8)

@@ -108,6 +108,7 @@ struct RotateParams {
   const uint32_t* mask;     // fused rotate + pack
   int32_t* offsets;         // written by the matrix-core kernel (head 0's workgroups) unless off_ready
   int off_ready;            // offsets already hold the scan (long prefixes)
+  int dyn_tiles;            // all workgroups resident at once: tiles handed out on demand
   void* Vp;
   int64_t cap;
 };
