@@ -138,6 +138,10 @@ rolesub_status rolesub_rotate_values(const rolesub_dims* dims, rolesub_dtype dty
  *   workspace  device scratch of at least rolesub_route_workspace_size()
  *              bytes (may be NULL if that size is 0). Nothing in it needs
  *              clearing; calls sharing one workspace must not overlap.
+ * The environment variable ROLESUB_SK_POLLS (0..1000, default 32), read at
+ * each call, bounds how long the first workgroup of a split-K router tile
+ * waits for the second to share the tile's epilogue; the outputs are the
+ * same bits for every value.
  * ------------------------------------------------------------------------ */
 size_t rolesub_route_workspace_size(const rolesub_dims* dims, const rolesub_router* router);
 rolesub_status rolesub_route(const rolesub_dims* dims, rolesub_dtype dtype,

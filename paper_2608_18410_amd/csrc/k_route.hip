@@ -906,11 +906,15 @@ __global__ __launch_bounds__(256) void k_route_mlp2_bf16(RouteParams p, int npcb
 // workgroups of six waves (16 tokens each), each over one half of the hidden
 // size: a workgroup reads half of the weight panel (0.6 MB rather than
 // 1.2 MB per 64 tokens), and 64 prefixes of 177 tokens make 236 workgroups,
-// one per CU on almost every CU. Both halves store their partial products;
-// the second to finish (one atomic ticket per tile, nobody waits) adds the
-// other half's and runs the epilogue. The single kernel accumulates the two
-// halves separately too, so both give the same bits: every product, sum and
-// epilogue step is the same per token.
+// one per CU on almost every CU. Both halves store their partial products
+// and take a ticket (one atomic counter per tile). The first to finish waits
+// a bounded time for the other; if it comes, each adds the other's partials
+// for 48 of the 96 tokens and runs their epilogue (three waves each, one per
+// SIMD, instead of six waves on four SIMDs for all 96); if not, the first
+// gives the tile up (a compare-and-swap decides against a late arrival) and
+// the second completes all of it. The single kernel accumulates the two
+// halves separately too, so all forms give the same bits: every product,
+// sum and epilogue step is the same per token.
 constexpr int kSkW = 6, kSkNB = 4;
 constexpr int kSkHBytes = kRouteSkTok * 128, kSkStage = kRtWBytes + kSkHBytes;
 constexpr int kSkLoads = kRtRows / 8 + kRouteSkTok / 8;  // 1 KB wave-loads per stage (30: five per wave)
@@ -923,7 +927,7 @@ __global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int 
   __shared__ __attribute__((aligned(16))) char ring[kSkNB * kSkStage];
   __shared__ float b2s[GP], brs[16], wps[16];
   __shared__ __attribute__((aligned(16))) float cbs[kSkW / 2][Hr];
-  __shared__ int s_ticket;
+  __shared__ int s_ticket, s_state;
   const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, uniform
   const int d = p.d, C = p.C, G = p.G;
@@ -1068,10 +1072,37 @@ __global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int 
   }
   wait_vmcnt<0>();  // this wave's partial has been written
   __syncthreads();
+  // Ticket states: 0 none arrived, 1 the first arrived and waits, 2 both
+  // arrived (shared epilogue), 3 the first gave up (4 once the second came).
   if (tid == 0) s_ticket = __hip_atomic_fetch_add(p.rcnt + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __syncthreads();
-  if (s_ticket == 0) return;  // the other half completes the tile
-  {
+  bool shared_epi = s_ticket == 1;  // second to arrive: 1 = the first waits for it, 3 = it gave up
+  if (s_ticket == 0) {
+    // first to arrive: poll the counter (system scope, past the caches) up
+    // to sk_polls times, then give the tile up unless the other came first
+    if (tid == 0) {
+      int st = 1;
+      for (int i = 0; i < p.sk_polls && st == 1; ++i) {
+        __builtin_amdgcn_s_sleep(4);
+        st = __hip_atomic_load(p.rcnt + tile, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      }
+      if (st == 1) {
+        int expect = 1;
+        st = __hip_atomic_compare_exchange_strong(p.rcnt + tile, &expect, 3, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_SYSTEM)
+                 ? 3
+                 : expect;
+      }
+      s_state = st;
+    }
+    __syncthreads();
+    if (s_state == 3) return;  // the other half completes the tile
+    shared_epi = true;
+  }
+  // with a shared epilogue half 0 finishes the tile's tokens 0..47 (waves
+  // 0-2), half 1 tokens 48..95 (waves 3-5)
+  const bool my_share = !shared_epi || ((w < kSkW / 2) == (half == 0));
+  if (my_share) {
     const uint32_t o = static_cast<uint32_t>(blockIdx.x ^ 1) * part_bytes + static_cast<uint32_t>(w * 64 + lane) * 16u;
 #pragma unroll
     for (int m = 0; m < 9; ++m)
@@ -1101,6 +1132,7 @@ __global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int 
     cbs[tid >> 7][tid & 127] = sum + b1v;
   }
   __syncthreads();
+  if (!my_share) return;  // no barrier follows
   float cbl[32];
   {
     const float* src = cbs[valid ? b - b0 : 0];

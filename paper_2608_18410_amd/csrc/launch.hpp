@@ -18,6 +18,7 @@ struct RouteParams {
   float* pcb;   // [ncb][B][Hr] partial language terms per column block (bf16 MLP2; workspace)
   float* rpart;  // split-K router: both halves' partial products per 96-token tile, or null (workspace)
   int* rcnt;     // split-K router: finished halves per tile, zeroed by the pool kernel (workspace)
+  int sk_polls;  // split-K router: polls the first half of a tile makes for the second (0: never shares)
   int mode;
   int k_by_type[4];
   float tau;

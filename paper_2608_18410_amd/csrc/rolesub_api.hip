@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <mutex>
 #include <string>
 
@@ -122,6 +123,17 @@ size_t route_ws_bytes(const rolesub_dims* d, const rolesub_router* r, bool split
                 : 0);
 }
 
+// Polls the first half of a split-K router tile makes for the second before
+// leaving the tile to it (a poll is one round trip to memory, about a
+// microsecond; the halves of a tile usually finish within a few of each
+// other). ROLESUB_SK_POLLS overrides it (0 to 1000); with 0 the halves share
+// the epilogue only when the second has already arrived.
+int route_sk_polls() {
+  const char* e = std::getenv("ROLESUB_SK_POLLS");
+  if (e && *e) return std::min(1000, std::max(0, std::atoi(e)));
+  return 32;
+}
+
 // Checks the router and hidden states and fills the router part of p (B, T,
 // d, G already set); the route workspace sits at the start of `workspace`.
 rolesub_status setup_router(const char* fn, const rolesub_dims* dims, rolesub_dtype dtype,
@@ -189,6 +201,7 @@ rolesub_status setup_router(const char* fn, const rolesub_dims* dims, rolesub_dt
     const size_t off_c = off_s + align256(route_sk_part_floats(p.B, p.T, p.Hr, p.kind) * sizeof(float));
     p.rpart = reinterpret_cast<float*>(ws + off_s);
     p.rcnt = reinterpret_cast<int*>(ws + off_c);
+    p.sk_polls = route_sk_polls();
   }
   return ROLESUB_OK;
 }

@@ -657,14 +657,19 @@ def test_route_mlp2_launch_paths(B, d, Hr, n_vis, n_lang):
 # of 128) against the single kernel, which the no-alloc call runs: the same
 # bits for every token, including tiles that end inside a sample or past the
 # last token, tiles over three samples, 16 and 32 groups, and a second call on
-# the same workspace.
+# the same workspace. With the default poll count the two halves of a tile
+# share its epilogue; with ROLESUB_SK_POLLS=0 the first to finish leaves the
+# tile to the other (unless it has already arrived).
+@pytest.mark.parametrize("polls", [None, "0"])
 @pytest.mark.parametrize("cid,B,n_vis,G", [(4, 3, 47, 8),      # T = 96: every tile is one whole sample
                                            (4, 2, 48, 8),      # T = 97: tiles straddle samples
                                            (4, 5, 1, 8),       # T = 50: tiles over three samples
                                            (4, 7, 32, 16),     # T = 81: the full-width prefix
                                            (4, 5, 151, 16),    # 16 groups, ragged last tile
                                            (4, 2, 300, 32)])   # 32 groups
-def test_route_split_k_matches_single_kernel(cid, B, n_vis, G):
+def test_route_split_k_matches_single_kernel(cid, B, n_vis, G, polls, monkeypatch):
+    if polls is not None:
+        monkeypatch.setenv("ROLESUB_SK_POLLS", polls)
     w = synth.workload(cid).replace(B=B, n_vis=n_vis, G=G, k_vis=min(4, G), k_lang=min(6, G), k_prop=min(8, G))
     wt = synth.layer_weights(w, 0)
     h = put(np.stack([synth.sample_activations(w, 0, b, ("h",))["h"] for b in range(B)]), torch.bfloat16)
