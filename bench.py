@@ -80,13 +80,37 @@ def dist(xs) -> dict:
             "p90": float(np.percentile(a, 90)), "n": int(a.size)}
 
 
+# After the GPU has idled for tens of milliseconds (the eager pass, graph
+# capture, creating events), the next 20 or so milliseconds of kernels run
+# up to 15 % slower (every kernel of the first five 7B-stack steps, in a
+# kernel trace; idle gaps of under 0.1 ms between steps do not do this). So
+# the warm-up runs the requested number of steps and then keeps stepping
+# until it has lasted WARM_S, and timed work follows it directly.
+WARM_S = 0.25
+
+
+def warm_up(step, n: int) -> int:
+    """Runs step() n times, then more until WARM_S seconds of warm-up have
+    passed; returns the number of steps run."""
+    import torch
+    t0 = time.perf_counter()
+    runs = 0
+    while runs < n or time.perf_counter() - t0 < WARM_S:
+        # steps back to back, as in the timed region, in batches of ten
+        for _ in range(n - runs if runs < n else 10):
+            step()
+            runs += 1
+        torch.cuda.synchronize()
+    return runs
+
+
 def timed_replays(fn, reps: int, per: int = 1) -> list:
-    """HIP events on the current stream around each of `reps` calls of fn;
-    returns the time per unit (fn does `per` units) of each call, in us."""
+    """HIP events on the current stream around each of `reps` calls of fn,
+    after WARM_S of warm-up calls; returns the time per unit (fn does `per`
+    units) of each call, in us."""
     import torch
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
-    fn()
-    torch.cuda.synchronize()
+    warm_up(fn, 1)
     ev[0].record()
     for i in range(reps):
         fn()
@@ -339,25 +363,22 @@ def full_width(args, w):
             for L in layers:
                 fn(L)
         graphs[name] = gr
-    for _ in range(args.warmup):
-        graphs["step"].replay()
-    torch.cuda.synchronize()
-    if not torch.equal(layers[-1]["fb"].out, eager_out):
-        raise RuntimeError("graph replay output differs from the eager pass")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_warm = warm_up(graphs["step"].replay, args.warmup)
     e0.record()
     for _ in range(args.steps):
         graphs["step"].replay()
     e1.record()
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
+    if not torch.equal(layers[-1]["fb"].out, eager_out):
+        raise RuntimeError("graph replay output differs from the eager pass")
     # each call type alone: HIP events around back-to-back replays of the
     # graph holding the 32 layers' calls of that type (same inputs)
     reps = max(2, args.steps // 4)
     per_call = {}
     for name in ("route", "rotate", "values", "attend"):
-        graphs[name].replay()
-        torch.cuda.synchronize()
+        warm_up(graphs[name].replay, 1)
         e0.record()
         for _ in range(reps):
             graphs[name].replay()
@@ -392,7 +413,7 @@ def full_width(args, w):
                      "frac": tflops / BF16_MFMA_PEAK_TFLOPS, "traffic": None,
                      "algorithmic_flops_per_launch": flops, "avg_launch_us": per_call[dom],
                      "dense_flops_per_launch": dense_flops},
-        "detail": {"per_layer_us": per_call, "routed_tokens_per_layer": n_routed,
+        "detail": {"warmup_steps_run": n_warm, "per_layer_us": per_call, "routed_tokens_per_layer": n_routed,
                    "routed_groups_per_layer": routed_groups,
                    "dense_tflops_executed": dense_flops / (per_call[dom] * 1e-6) / 1e12},
     }
@@ -635,18 +656,16 @@ def prefix_attention(args, w):
     with torch.cuda.graph(g, stream=stream):
         for L in layers:
             att(L)
-    for _ in range(args.warmup):
-        g.replay()
-    torch.cuda.synchronize()
-    if not torch.equal(layers[-1]["out"], eager_out):
-        raise RuntimeError("graph replay output differs from the eager pass")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_warm = warm_up(g.replay, args.warmup)
     e0.record()
     for _ in range(args.steps):
         g.replay()
     e1.record()
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
+    if not torch.equal(layers[-1]["out"], eager_out):
+        raise RuntimeError("graph replay output differs from the eager pass")
     call_us = ms_step * 1e3 / w.L
     sum_k = int(layers[0]["offsets"][:, -1].sum().item()) // w.B
     a_bytes = attend_bytes(w, sum_k, 2)
@@ -666,6 +685,7 @@ def prefix_attention(args, w):
                      "traffic": None, "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": call_us,
                      "mfma": {"achieved": tflops, "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                               "frac": tflops / BF16_MFMA_PEAK_TFLOPS, "flops_per_launch": causal_flops(w)}},
+        "detail": {"warmup_steps_run": n_warm},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline_causal(w, masks0)
@@ -708,17 +728,15 @@ def retention(args, w):
     with torch.cuda.graph(g, stream=stream):
         for S in sets:
             call(S)
-    for _ in range(args.warmup):
-        g.replay()
-    torch.cuda.synchronize()
-    if not torch.equal(sets[0]["out"], ref):
-        raise RuntimeError("graph replay output differs from the eager pass")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_warm = warm_up(g.replay, args.warmup)
     e0.record()
     for _ in range(args.steps):
         g.replay()
     e1.record()
     torch.cuda.synchronize()
+    if not torch.equal(sets[0]["out"], ref):
+        raise RuntimeError("graph replay output differs from the eager pass")
     call_us = e0.elapsed_time(e1) * 1e3 / (args.steps * n_sets)
     row = d * 2
     moved = B * N * 4 + B * K * 4 * 2 + 2 * B * K * row  # scores, indices (written, read), rows read + written
@@ -734,6 +752,7 @@ def retention(args, w):
         "roofline": {"kernel": "rolesub_retain_tokens + rolesub_gather_tokens", "bound": "hbm", "achieved": gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "traffic": None,
                      "algorithmic_bytes_per_launch": moved, "avg_launch_us": call_us},
+        "detail": {"warmup_steps_run": n_warm},
     }
     if not args.no_cpu_baseline:
         import oracle as O
@@ -914,16 +933,13 @@ def main():
             for L in layers:
                 att(L)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    if not torch.equal(layers[-1]["bufs"].out, eager_out):
-        raise RuntimeError("graph replay output differs from the eager pass")
-
     # K timed steps back to back, an event after each (the mean is the
-    # reported step time; the spread comes from the same events)
+    # reported step time; the spread comes from the same events). The events
+    # exist before the warm-up, which ends with a synchronize, so the timed
+    # steps follow it without an idle gap; the replays' output is checked
+    # against the eager pass afterwards.
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
+    n_warm = warm_up(step, args.warmup)
     ev[0].record()
     for i in range(args.steps):
         step()
@@ -931,6 +947,8 @@ def main():
     torch.cuda.synchronize()
     step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     ms_step = ev[0].elapsed_time(ev[-1]) / args.steps
+    if not torch.equal(layers[-1]["bufs"].out, eager_out):
+        raise RuntimeError("graph replay output differs from the eager pass")
 
     # Attention kernel duration: HIP events on the launch stream around each
     # of >= 50 back-to-back replays of the attention calls of every layer
@@ -959,8 +977,7 @@ def main():
             alloc_run = g_alloc.replay
         else:
             alloc_run = alloc_all
-        alloc_run()
-        torch.cuda.synchronize()
+        warm_up(alloc_run, 1)
         a0.record()
         for _ in range(reps):
             alloc_run()
@@ -1013,7 +1030,7 @@ def main():
                      "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": att_ms * 1e3,
                      "launch_us": dist(att_us), "copy_GBs_same_run": copy_gbs,
                      "frac_of_copy": achieved / copy_gbs},
-        "detail": {"step_ms": dist(step_ms),
+        "detail": {"warmup_steps_run": n_warm, "step_ms": dist(step_ms),
                    "copy": copy,
                    "attend_query_tokens_per_s": w.B * w.Tq / (att_ms * 1e-3),
                    "layers_per_s": w.L / (ms_step * 1e-3),
