@@ -786,6 +786,9 @@ def main():
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the other workloads (G = 32 stress, one-layer and batch-16 shapes) after the step")
     ap.add_argument("--eager", action="store_true", help="issue the calls directly, no HIP graphs")
+    ap.add_argument("--micro-batches", type=int, default=2,
+                    help="split the step's prefixes into this many contiguous micro-batches, each through "
+                         "every layer on its own stream (1: the whole batch per call on one stream)")
     ap.add_argument("--prefix-attention", action="store_true",
                     help="time prefix self-attention (rolesub_attend_causal) at the same shape instead")
     ap.add_argument("--full-width", action="store_true",
@@ -811,7 +814,7 @@ def main():
 
     import paper_2608_18410_amd as rs
     import synth
-    from paper_2608_18410_amd.pipeline import LayerBuffers, pack_capacity, run_layer
+    from paper_2608_18410_amd.pipeline import LayerBuffers, micro_batches, pack_capacity, run_layer
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_probe:
@@ -847,6 +850,11 @@ def main():
     budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
     cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
     types = torch.from_numpy(np.broadcast_to(w.types(), (w.B, w.T)).copy()).to(dev)
+    # Micro-batches: contiguous ranges of prefixes, each taken through every
+    # layer on its own stream. Prefixes do not interact, so the calls of one
+    # range depend only on that range's earlier calls, and the kernels of the
+    # ranges overlap on the GPU, filling each other's ramp-up and tail.
+    mbs = micro_batches(w.B, args.micro_batches)
 
     # ---- inputs resident in HBM
     t_gen = time.time()
@@ -870,54 +878,78 @@ def main():
         scores = None
         if w.scores_in:
             scores = torch.from_numpy(np.stack([synth.sample_scores(w, l, b) for b in range(w.B)])).to(dev)
-        if args.allocation:
-            ws = rs.route_allocate_workspace_size(w.B, w.T, w.G, w.d, router)
-        else:
-            ws = rs.route_workspace_size(w.B, w.T, w.G, w.d, router)
-        bufs = LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, dt, ws_bytes=ws, device=dev,
+        # one route workspace per micro-batch (calls on one workspace must not
+        # overlap), carved from the layer's workspace at 256-byte boundaries
+        wsz = [(rs.route_allocate_workspace_size if args.allocation else rs.route_workspace_size)(
+            b1 - b0, w.T, w.G, w.d, router) for b0, b1 in mbs]
+        ws_off = [0]
+        for n in wsz:
+            ws_off.append(ws_off[-1] + (n + 255) // 256 * 256)
+        bufs = LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, dt, ws_bytes=ws_off[-1], device=dev,
                                      with_z=False)
+        mb_bufs = [bufs.rows(b0, b1, bufs.workspace[ws_off[i]:ws_off[i] + max(wsz[i], 1)])
+                   for i, (b0, b1) in enumerate(mbs)]
         alloc = None
         if args.allocation:
             alloc = dict(w_pri=put(synth.priority_weights(w, l)),
                          priority=torch.empty((w.B, w.T), dtype=torch.float32, device=dev),
                          k=torch.empty((w.B, w.T), dtype=torch.uint8, device=dev))
         layers.append(dict(acts=acts, router=router if scores is None else None, scores=scores,
-                           R=put(wt["R"]), bufs=bufs, alloc=alloc))
+                           R=put(wt["R"]), bufs=bufs, mb_bufs=mb_bufs, alloc=alloc))
         print(f"# layer {l} inputs resident ({time.time() - t_gen:.1f} s)", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
 
-    def pre(L):
-        a, bf, al = L["acts"], L["bufs"], L["alloc"]
+    def pre(L, i):
+        # route -> rotate + pack for micro-batch i of layer L
+        (b0, b1), bf, al = mbs[i], L["mb_bufs"][i], L["alloc"]
+        a = {n: t[b0:b1] for n, t in L["acts"].items()}
         if al is not None:
-            rs.route_allocate(types, w.k_by_type, w.G, a["h"], L["router"], al["w_pri"], workspace=bf.workspace,
+            rs.route_allocate(types[b0:b1], w.k_by_type, w.G, a["h"], L["router"], al["w_pri"],
+                              workspace=bf.workspace,
                               out={"mask": bf.mask, "idx": bf.idx, "count": bf.count, "scores": bf.scores,
-                                   "priority": al["priority"], "k": al["k"]})
+                                   "priority": al["priority"][b0:b1], "k": al["k"][b0:b1]})
         else:
-            rs.route(types, budget, w.G, h=a.get("h"), router=L["router"], scores_in=L["scores"],
-                     workspace=bf.workspace,
+            rs.route(types[b0:b1], budget, w.G, h=a.get("h"), router=L["router"],
+                     scores_in=None if L["scores"] is None else L["scores"][b0:b1], workspace=bf.workspace,
                      out={"mask": bf.mask, "idx": bf.idx, "count": bf.count, "scores": bf.scores})
         rs.rotate_pack(a["v"], L["R"], bf.mask, w.G, cap, out=(bf.offsets, bf.Vp))
 
-    def att(L):
-        a, bf = L["acts"], L["bufs"]
+    def att(L, i=None):
+        # attention for micro-batch i of layer L, or for the whole batch
+        if i is None:
+            a, bf = L["acts"], L["bufs"]
+        else:
+            (b0, b1), bf = mbs[i], L["mb_bufs"][i]
+            a = {n: t[b0:b1] for n, t in L["acts"].items()}
         rs.attend(a["q"], a["k"], bf.mask, bf.offsets, bf.Vp, L["R"], w.G, out=bf.out)
 
-    # ---- one eager pass (also the reference for the graph replays)
-    for L in layers:
-        pre(L)
-        att(L)
+    def run_mb(i):
+        for L in layers:
+            pre(L, i)
+            att(L, i)
+
+    # ---- one eager pass, micro-batch after micro-batch on one stream (also
+    # the reference for the graph replays)
+    for i in range(len(mbs)):
+        run_mb(i)
     torch.cuda.synchronize()
     eager_out = layers[-1]["bufs"].out.clone()
 
     if not args.eager:
-        # the whole step (every layer's calls) is one graph; a second graph
-        # holds only the layers' attention calls, for timing that kernel
+        # the whole step (every micro-batch through every layer, each
+        # micro-batch on its own stream) is one graph; a second graph holds
+        # only the layers' whole-batch attention calls, for timing that kernel
         stream = torch.cuda.Stream()
+        mb_streams = [torch.cuda.Stream() for _ in mbs]
         g_step, g_att = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
         with torch.cuda.graph(g_step, stream=stream):
-            for L in layers:
-                pre(L)
-                att(L)
+            for s_ in mb_streams:
+                s_.wait_stream(stream)
+            for i, s_ in enumerate(mb_streams):
+                with torch.cuda.stream(s_):
+                    run_mb(i)
+            for s_ in mb_streams:
+                stream.wait_stream(s_)
         with torch.cuda.graph(g_att, stream=stream):
             for L in layers:
                 att(L)
@@ -925,9 +957,8 @@ def main():
         att_all = g_att.replay
     else:
         def step():
-            for L in layers:
-                pre(L)
-                att(L)
+            for i in range(len(mbs)):
+                run_mb(i)
 
         def att_all():
             for L in layers:
@@ -1023,8 +1054,11 @@ def main():
                    if args.allocation else ("fixed per type" if w.mode == 0 else
                                             "threshold on given logits (selection only)"),
                    "value_counts": "query tokens x layers per second (B*Tq*L / step time)",
-                   "graphs": not args.eager},
-        "roofline": {"kernel": "rolesub_attend (k_attend_bf16)", "bound": "hbm",
+                   "graphs": not args.eager,
+                   "micro_batches": [b1 - b0 for b0, b1 in mbs],
+                   "schedule": "each micro-batch of prefixes through every layer on its own stream"
+                   if len(mbs) > 1 else "the whole batch per call on one stream"},
+        "roofline": {"kernel": "rolesub_attend (k_attend_bf16), whole-batch launches", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": _traffic(w.name),
                      "algorithmic_bytes_per_launch": a_bytes, "avg_launch_us": att_ms * 1e3,

@@ -1,7 +1,9 @@
 """One layer of the hot path, route -> rotate -> pack -> attend, through the C ABI.
 
 Orchestration only: buffers are allocated once per shape and reused, and the
-four library calls are issued in order on one stream.
+four library calls are issued in order on one stream. A batch may also be
+split into micro-batches (contiguous ranges of prefixes, each with views of
+the buffers and its own route workspace) whose calls run on separate streams.
 """
 from __future__ import annotations
 
@@ -45,6 +47,23 @@ class LayerBuffers:
             out=torch.empty((B, Tq, H, dh), dtype=out_dtype or dtype, device=device),
             workspace=torch.empty(max(int(ws_bytes), 256), dtype=u8, device=device),
         )
+
+    def rows(self, b0: int, b1: int, workspace: torch.Tensor) -> "LayerBuffers":
+        """The buffers of prefixes b0..b1-1 (views: every per-prefix buffer is
+        sliced along its first dimension, so the calls on them write into this
+        object's tensors), with their own route workspace."""
+        sl = lambda t: t[b0:b1] if t.dim() > 1 else t
+        return LayerBuffers(mask=self.mask[b0:b1], idx=self.idx[b0:b1], count=self.count[b0:b1],
+                            scores=self.scores[b0:b1], z=sl(self.z), offsets=self.offsets[b0:b1],
+                            Vp=self.Vp[b0:b1], out=self.out[b0:b1], workspace=workspace)
+
+
+def micro_batches(B: int, n: int) -> list:
+    """n contiguous, nearly equal ranges (b0, b1) of B prefixes. Prefixes do
+    not interact, so the calls of one range may run on their own stream,
+    concurrently with the others."""
+    n = max(1, min(int(n), B))
+    return [((i * B) // n, ((i + 1) * B) // n) for i in range(n)]
 
 
 def run_layer(h, q, k, v, types, R, budget: rs.Budget, G: int, bufs: LayerBuffers,

@@ -138,3 +138,21 @@ def test_full_width_shapes():
     refused(rs.full_values, z(dv, dv), z(B, T, dtype=i32), good[0], good[1], S, 3, match="heads")
     reaches_device_check(rs.attend_values, z(B, Tq, H, dh), z(B, T, H, dh), z(B, H, T, dh))
     refused(rs.attend_values, z(B, Tq, H, dh), z(B, T, H, dh), z(B, T, H, dh))            # token-major values
+
+
+def test_micro_batches_and_buffer_rows():
+    from paper_2608_18410_amd.pipeline import LayerBuffers, micro_batches
+    assert micro_batches(64, 2) == [(0, 32), (32, 64)]
+    assert micro_batches(8, 3) == [(0, 2), (2, 5), (5, 8)]
+    assert micro_batches(2, 5) == [(0, 1), (1, 2)]      # never more ranges than prefixes
+    assert micro_batches(7, 0) == [(0, 7)]
+    for B, n in ((64, 2), (177, 7), (5, 5)):
+        r = micro_batches(B, n)
+        assert r[0][0] == 0 and r[-1][1] == B and all(a[1] == b[0] for a, b in zip(r, r[1:]))
+        assert max(b1 - b0 for b0, b1 in r) - min(b1 - b0 for b0, b1 in r) <= 1
+    bufs = LayerBuffers.allocate(5, 7, 2, 64, 4, 3, 9, torch.bfloat16, ws_bytes=1024, device="cpu", with_z=False)
+    ws = torch.empty(512, dtype=torch.uint8)
+    v = bufs.rows(1, 4, ws)
+    assert v.mask.shape == (3, 7) and v.offsets.shape == (3, 8) and v.Vp.shape == (3, 2, 9, 16)
+    assert v.out.shape == (3, 3, 2, 64) and v.workspace is ws and v.z.numel() == 0
+    assert v.mask.data_ptr() == bufs.mask[1].data_ptr() and v.Vp.is_contiguous()

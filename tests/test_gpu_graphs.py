@@ -13,7 +13,8 @@ import torch
 
 import paper_2608_18410_amd as rs
 import synth
-from paper_2608_18410_amd.pipeline import FullWidthBuffers, LayerBuffers, pack_capacity, run_full_layer, run_layer
+from paper_2608_18410_amd.pipeline import (FullWidthBuffers, LayerBuffers, micro_batches, pack_capacity,
+                                          run_full_layer, run_layer)
 from tests._gpu_util import DEV, put, put_mask, put_u8, router_tensors, stack_types
 
 pytestmark = pytest.mark.gpu
@@ -183,3 +184,63 @@ def test_two_layers_on_two_streams_match_sequential():
         for a, b in zip(seq, par):
             for name in ("mask", "idx", "count", "scores", "offsets", "out"):
                 assert torch.equal(_bits(getattr(a, name)), _bits(getattr(b, name))), (rep, name)
+
+
+def test_micro_batches_on_streams_match_whole_batch():
+    # a batch split into micro-batches (views of the layer's buffers, one
+    # route workspace each), every micro-batch through two layers on its own
+    # stream and captured in one graph, gives the bits of whole-batch calls
+    w = synth.workload(4).replace(B=8)
+    budget = rs.make_budget(w.mode, w.k_by_type, w.tau, w.kmin, w.kmax)
+    cap = pack_capacity(w.mode, w.k_by_type, w.type_counts(), w.T, w.G, w.kmax)
+    Ls = [_stack_layer(w, 0), _stack_layer(w, 1)]
+    mbs = micro_batches(w.B, 3)
+    assert [b1 - b0 for b0, b1 in mbs] == [2, 3, 3]
+    wsz = [rs.route_workspace_size(b1 - b0, w.T, w.G, w.d, Ls[0]["router"]) for b0, b1 in mbs]
+    off = np.concatenate([[0], np.cumsum([(n + 255) // 256 * 256 for n in wsz])]).astype(int)
+    whole = [LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, torch.bfloat16, device=DEV, with_z=False,
+                                   ws_bytes=rs.route_workspace_size(w.B, w.T, w.G, w.d, Ls[0]["router"]))
+             for _ in Ls]
+    split = [LayerBuffers.allocate(w.B, w.T, w.H, w.dh, w.G, w.Tq, cap, torch.bfloat16, device=DEV, with_z=False,
+                                   ws_bytes=int(off[-1])) for _ in Ls]
+    views = [[b.rows(b0, b1, b.workspace[off[i]:off[i] + wsz[i]]) for i, (b0, b1) in enumerate(mbs)] for b in split]
+    _say(f"micro-batches {mbs} on streams, 7B-stack layers B={w.B}")
+    for X, b in zip(Ls, whole):
+        run_layer(X["h"], X["q"], X["k"], X["v"], X["types"], X["R"], budget, w.G, b, router=X["router"],
+                  type_counts=w.type_counts())
+
+    def mb(i):
+        b0, b1 = mbs[i]
+        for X, v in zip(Ls, views):
+            run_layer(X["h"][b0:b1], X["q"][b0:b1], X["k"][b0:b1], X["v"][b0:b1], X["types"][b0:b1], X["R"],
+                      budget, w.G, v[i], router=X["router"], type_counts=w.type_counts())
+
+    g = torch.cuda.CUDAGraph()
+    main = torch.cuda.Stream()
+    streams = [torch.cuda.Stream() for _ in mbs]
+    main.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(main):
+        for i in range(len(mbs)):  # warm-up on the capture stream
+            mb(i)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=main):
+            for s in streams:
+                s.wait_stream(main)
+            for i, s in enumerate(streams):
+                with torch.cuda.stream(s):
+                    mb(i)
+            for s in streams:
+                main.wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for b in split:
+            _sentinel((b.mask, b.idx, b.count, b.scores, b.offsets, b.out))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(whole, split):
+            for name in ("mask", "idx", "count", "scores", "offsets", "out"):
+                assert torch.equal(_bits(getattr(a, name)), _bits(getattr(b, name))), (rep, name)
+            for s in range(w.B):
+                n = int(a.offsets[s, -1])
+                assert torch.equal(a.Vp[s, :, :n].view(torch.int16), b.Vp[s, :, :n].view(torch.int16)), (rep, "Vp", s)
