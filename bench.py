@@ -814,7 +814,7 @@ def main():
 
     import paper_2608_18410_amd as rs
     import synth
-    from paper_2608_18410_amd.pipeline import LayerBuffers, micro_batches, pack_capacity, run_layer
+    from paper_2608_18410_amd.pipeline import LayerBuffers, micro_batches, on_streams, pack_capacity, run_layer
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_probe:
@@ -943,13 +943,7 @@ def main():
         mb_streams = [torch.cuda.Stream() for _ in mbs]
         g_step, g_att = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
         with torch.cuda.graph(g_step, stream=stream):
-            for s_ in mb_streams:
-                s_.wait_stream(stream)
-            for i, s_ in enumerate(mb_streams):
-                with torch.cuda.stream(s_):
-                    run_mb(i)
-            for s_ in mb_streams:
-                stream.wait_stream(s_)
+            on_streams(lambda i, b0, b1: run_mb(i), mbs, mb_streams)
         with torch.cuda.graph(g_att, stream=stream):
             for L in layers:
                 att(L)

@@ -66,6 +66,21 @@ def micro_batches(B: int, n: int) -> list:
     return [((i * B) // n, ((i + 1) * B) // n) for i in range(n)]
 
 
+def on_streams(issue, ranges, streams) -> None:
+    """Calls issue(i, b0, b1) for every range with streams[i] current: each
+    stream first waits for the work already queued on the current stream,
+    and the current stream then waits for all of them (also inside a HIP
+    graph capture, where this makes parallel branches)."""
+    cur = torch.cuda.current_stream()
+    for s in streams:
+        s.wait_stream(cur)
+    for i, ((b0, b1), s) in enumerate(zip(ranges, streams)):
+        with torch.cuda.stream(s):
+            issue(i, b0, b1)
+    for s in streams:
+        cur.wait_stream(s)
+
+
 def run_layer(h, q, k, v, types, R, budget: rs.Budget, G: int, bufs: LayerBuffers,
               router: rs.Router | None = None, scores_in=None, type_counts=None, fused=True,
               stream=None):

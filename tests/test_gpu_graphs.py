@@ -13,8 +13,8 @@ import torch
 
 import paper_2608_18410_amd as rs
 import synth
-from paper_2608_18410_amd.pipeline import (FullWidthBuffers, LayerBuffers, micro_batches, pack_capacity,
-                                          run_full_layer, run_layer)
+from paper_2608_18410_amd.pipeline import (FullWidthBuffers, LayerBuffers, micro_batches, on_streams,
+                                          pack_capacity, run_full_layer, run_layer)
 from tests._gpu_util import DEV, put, put_mask, put_u8, router_tensors, stack_types
 
 pytestmark = pytest.mark.gpu
@@ -224,13 +224,7 @@ def test_micro_batches_on_streams_match_whole_batch():
             mb(i)
         torch.cuda.synchronize()
         with torch.cuda.graph(g, stream=main):
-            for s in streams:
-                s.wait_stream(main)
-            for i, s in enumerate(streams):
-                with torch.cuda.stream(s):
-                    mb(i)
-            for s in streams:
-                main.wait_stream(s)
+            on_streams(lambda i, b0, b1: mb(i), mbs, streams)
     torch.cuda.synchronize()
     for rep in range(3):
         for b in split:
