@@ -1053,9 +1053,10 @@ __global__ __launch_bounds__(64 * kSkW) void k_route_mlp2_sk(RouteParams p, int 
   wait_vmcnt<0>();  // trailing dummy loads land before the LDS is released
   __syncthreads();  // every wave is done with the ring
 
-  // Both halves store their partial products; the second to finish adds the
-  // other's (a + b: the same bits in either order) and completes the tile.
-  // The two workgroups of a tile may sit on different XCDs, whose L2 caches
+  // Both halves store their partial products; whoever completes a token adds
+  // the other half's (a + b: the same bits in either order), both halves for
+  // 48 tokens each or the second to finish for all 96 (see the kernel's
+  // header). The two workgroups of a tile may sit on different XCDs, whose L2 caches
   // are not coherent with each other: the partials are written and read with
   // system-scope cache bits (written through to memory, read past the
   // caches), and the ticket is a system-scope atomic. No fence is needed for
